@@ -1,0 +1,226 @@
+"""Pins for the stage-1 oracle (per-expert counts, plan split, padded groups,
+stable permutation).  The definition follows the fixed-charge problem of
+Sec. 3.1 (n_e, R(e), shares x_{e,g}, activations z_{e,g}), the M-tiles of
+Sec. 2.2 / Eq. 2 and the integration semantics of Sec. 4.4 (padding rows
+masked, rows renormalised at use, zero-sum rows uniform over replicas).
+
+Nothing here re-types the oracle's formulas: the checks are invariants the
+definition implies, a special case that reduces to numpy's stable argsort,
+proportional-share bounds, and hand-worked tiny cases."""
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle
+
+
+def _rand_case(rng, T, K, E, S, M, p_bad=0.0, p_neg=0.1, remote=True, zero_w=0.1):
+    ids = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    ids[rng.random((T, K)) < p_neg] = -1
+    if p_bad:
+        bad = rng.random((T, K)) < p_bad
+        ids[bad] = rng.choice([E, E + 3, -2, -7], size=bad.sum())
+    se = rng.integers(0, E, size=S).astype(np.int32)
+    sw = rng.integers(0, 4, size=S).astype(np.uint32)
+    sw[rng.random(S) < zero_w] = 0
+    rw = (rng.integers(0, 3, size=E) * (rng.random(E) < 0.5)).astype(np.uint32) if remote else np.zeros(E, np.uint32)
+    rr = np.where(rw > 0, rng.integers(1, 3, size=E), (rng.random(E) < 0.2).astype(np.int64)).astype(np.int32)
+    if not remote:
+        rr[:] = 0
+    T_valid = int(rng.integers(0, T + 1))
+    return ids, T_valid, se, sw, rw, rr
+
+
+def _check_invariants(ids, T_valid, E, M, se, sw, rw, rr, d):
+    T, K = ids.shape
+    S = len(se)
+    ec, sc, so, rt, pr = d["expert_counts"], d["slot_counts"], d["slot_offsets"], d["row_token"], d["pair_row"]
+    valid = np.zeros((T, K), bool)
+    valid[:T_valid] = (ids[:T_valid] >= 0) & (ids[:T_valid] < E)
+    # counts over valid pairs only (padding rows and bad ids excluded)
+    assert np.array_equal(ec, np.bincount(ids[valid], minlength=E))
+    # padded sizes and offsets
+    P = so[1:] - so[:-1]
+    assert so[0] == 0
+    assert np.all(P % M == 0) and np.all(P >= sc) and np.all(P - sc < M)
+    assert np.all((P == 0) == (sc == 0))
+    # rows: inverse maps; rows of a slot in ascending pair index
+    assert len(rt) == so[-1]
+    placed = pr.reshape(-1) >= 0
+    assert np.all(valid.reshape(-1)[placed]), "an invalid pair was placed"
+    rows = pr.reshape(-1)[placed]
+    assert len(np.unique(rows)) == len(rows), "two pairs share a row"
+    pidx = np.nonzero(placed)[0]
+    assert np.array_equal(rt[rows], pidx // K)
+    assert (rt >= 0).sum() == len(rows)
+    for s in range(S):
+        lo, c = so[s], sc[s]
+        seg = rt[lo:so[s + 1]]
+        assert np.all(seg[:c] >= 0) and np.all(seg[c:] == -1)
+        # pair indices of the slot's rows, ascending
+        inv = {r: p for r, p in zip(rows.tolist(), pidx.tolist())}
+        ps = [inv[r] for r in range(lo, lo + c)]
+        assert ps == sorted(ps)
+        assert all(ids.reshape(-1)[p] == se[s] for p in ps)
+    # per expert: local counts + remote remainder = n_e; within one of the
+    # proportional share; only experts with a remote entry leave pairs unplaced
+    for e in range(E):
+        loc = [s for s in range(S) if se[s] == e]
+        has_remote = rw[e] > 0 or rr[e] > 0
+        n = ec[e]
+        placed_e = sum(int(sc[s]) for s in loc)
+        if not loc:
+            assert placed_e == 0
+            continue
+        if not has_remote:
+            assert placed_e == n
+        w = [int(sw[s]) for s in loc] + ([int(rw[e])] if has_remote else [])
+        W = sum(w)
+        if W == 0:
+            w = [1] * len(loc) + ([int(rr[e])] if has_remote else [])
+            W = sum(w)
+        for j, s in enumerate(loc):
+            assert abs(int(sc[s]) - n * w[j] / W) < 1.0 + 1e-12
+        assert placed_e <= n
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 40), st.integers(1, 4), st.integers(1, 9), st.integers(1, 10),
+       st.sampled_from([1, 2, 4, 16, 32, 128]))
+def test_invariants_random(seed, T, K, E, S, M):
+    rng = np.random.default_rng(seed)
+    ids, T_valid, se, sw, rw, rr = _rand_case(rng, T, K, E, S, M)
+    d = oracle.dispatch(ids, T_valid, E, M, se, sw, rw, rr)
+    assert d["err"] == 0
+    _check_invariants(ids, T_valid, E, M, se, sw, rw, rr, d)
+
+
+@settings(max_examples=100, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 30), st.integers(1, 3), st.integers(1, 6), st.integers(1, 6))
+def test_bad_ids_dropped_and_flagged(seed, T, K, E, S):
+    rng = np.random.default_rng(seed)
+    ids, T_valid, se, sw, rw, rr = _rand_case(rng, T, K, E, S, 4, p_bad=0.2)
+    d = oracle.dispatch(ids, T_valid, E, 4, se, sw, rw, rr)
+    bad = ((ids[:T_valid] < -1) | (ids[:T_valid] >= E)).any()
+    assert bool(d["err"] & oracle.ERR_BAD_ID) == bool(bad)
+    _check_invariants(ids, T_valid, E, 4, se, sw, rw, rr, d)
+
+
+def test_single_replica_is_stable_argsort():
+    """One local slot per expert, nothing remote: the non-padding rows in
+    slot order are numpy's stable argsort of the pairs by expert."""
+    rng = np.random.default_rng(7)
+    for trial in range(50):
+        E = int(rng.integers(1, 12))
+        T, K, M = int(rng.integers(1, 60)), int(rng.integers(1, 5)), int(rng.choice([1, 8, 64]))
+        ids = rng.integers(0, E, size=(T, K)).astype(np.int32)
+        ids[rng.random((T, K)) < 0.1] = -1
+        se = rng.permutation(E).astype(np.int32)  # slot order != expert order
+        d = oracle.dispatch(ids, T, E, M, se, np.ones(E, np.uint32), np.zeros(E, np.uint32), np.zeros(E, np.int32))
+        flat = ids.reshape(-1)
+        key = np.array([np.nonzero(se == e)[0][0] if e >= 0 else 10**9 for e in flat])
+        order = np.argsort(key, kind="stable")
+        order = order[key[order] < 10**9]
+        rt = d["row_token"]
+        inv = {r: p for p, r in enumerate(d["pair_row"].reshape(-1).tolist()) if r >= 0}
+        got = [inv[r] for r in range(len(rt)) if rt[r] >= 0]
+        assert got == order.tolist()
+
+
+def test_even_halves_and_uniform_fallback():
+    ids = np.zeros((10, 1), np.int32)  # expert 0 gets 10 pairs
+    se = np.array([0, 0], np.int32)
+    z = np.zeros(1, np.uint32)
+    d = oracle.dispatch(ids, 10, 1, 4, se, np.array([1, 1], np.uint32), z, np.zeros(1, np.int32))
+    assert d["slot_counts"].tolist() == [5, 5]
+    # first half of the pairs (ascending index) on the first slot
+    assert d["pair_row"].reshape(-1).tolist() == [0, 1, 2, 3, 4, 8, 9, 10, 11, 12]
+    assert d["slot_offsets"].tolist() == [0, 8, 16]
+    # a row that sums to zero is renormalised to uniform over its replicas
+    d0 = oracle.dispatch(ids, 10, 1, 4, se, np.array([0, 0], np.uint32), z, np.zeros(1, np.int32))
+    assert d0["slot_counts"].tolist() == [5, 5] and d0["err"] == 0
+    # zero row with a remote replica: uniform over 2 local + 2 remote replicas
+    d1 = oracle.dispatch(ids, 10, 1, 4, se, np.array([0, 0], np.uint32), z, np.array([2], np.int32))
+    assert d1["slot_counts"].tolist() == [2, 3]
+    # weights are renormalised at use: scaling a row changes nothing
+    d2 = oracle.dispatch(ids, 10, 1, 4, se, np.array([7, 7], np.uint32), z, np.zeros(1, np.int32))
+    assert np.array_equal(d2["pair_row"], d["pair_row"])
+
+
+def test_hand_worked_three_way_split():
+    """n = 7 pairs of expert 1 over local slots with weights 1, 2 and a remote
+    share of 4 (W = 7): shares are exactly 1, 2, 4.  Remote pairs are the
+    last four by pair index."""
+    ids = np.array([[1, 0], [1, 1], [0, 1], [1, 1], [1, 2]], np.int32)  # expert-1 pairs p = 0,2,3,5,6,7,8
+    se = np.array([1, 0, 1], np.int32)
+    d = oracle.dispatch(ids, 5, 3, 2, se, np.array([1, 5, 2], np.uint32), np.array([0, 4, 0], np.uint32),
+                        np.array([0, 1, 0], np.int32))
+    assert d["expert_counts"].tolist() == [2, 7, 1]
+    assert d["slot_counts"].tolist() == [1, 2, 2]
+    assert d["slot_offsets"].tolist() == [0, 2, 4, 6]
+    pr = d["pair_row"].reshape(-1).tolist()
+    assert pr[0] == 0  # rank 0 -> slot 0
+    assert pr[2] == 4 and pr[3] == 5  # ranks 1,2 -> slot 2 (rows 4, 5)
+    assert pr[5] == pr[6] == pr[7] == pr[8] == -1  # ranks 3..6 -> remote
+    assert pr[1] == 2 and pr[4] == 3  # expert 0 pairs on slot 1
+    assert pr[9] == -1  # expert 2 has no slot
+    assert d["row_token"].tolist() == [0, -1, 0, 2, 1, 1]
+
+
+def test_padding_rows_masked_and_cumulative_counter_wraps():
+    rng = np.random.default_rng(3)
+    ids = rng.integers(0, 4, size=(12, 2)).astype(np.int32)
+    ids2 = ids.copy()
+    ids2[8:] = 0  # degenerate routing on graph-padding rows ("phantom hot expert")
+    se = np.arange(4, dtype=np.int32)
+    args = (np.ones(4, np.uint32), np.zeros(4, np.uint32), np.zeros(4, np.int32))
+    a = oracle.dispatch(ids, 8, 4, 16, se, *args)
+    b = oracle.dispatch(ids2, 8, 4, 16, se, *args)
+    for k in ("expert_counts", "slot_counts", "slot_offsets", "row_token", "pair_row"):
+        assert np.array_equal(a[k], b[k])
+    cum = np.array([2**32 - 3, 0, 5, 2**32 - 1], np.uint32)
+    c = oracle.dispatch(ids, 8, 4, 16, se, *args, cum_counts=cum)
+    expect = (cum.astype(np.uint64) + a["expert_counts"].astype(np.uint64)) % 2**32
+    assert np.array_equal(c["cum_counts"], expect.astype(np.uint32))
+    # wrap-safe window difference recovers the window's counts
+    assert np.array_equal((c["cum_counts"] - cum).astype(np.uint32), a["expert_counts"].astype(np.uint32))
+
+
+def test_empty_and_degenerate():
+    se = np.array([0, 1], np.int32)
+    args = (np.ones(2, np.uint32), np.zeros(2, np.uint32), np.zeros(2, np.int32))
+    d = oracle.dispatch(np.zeros((5, 2), np.int32), 0, 2, 8, se, *args)  # T_valid = 0
+    assert d["slot_counts"].tolist() == [0, 0] and d["slot_offsets"].tolist() == [0, 0, 0]
+    assert np.all(d["pair_row"] == -1) and len(d["row_token"]) == 0
+    d = oracle.dispatch(np.full((5, 2), -1, np.int32), 5, 2, 8, se, *args)  # all dropped
+    assert d["expert_counts"].tolist() == [0, 0] and d["err"] == 0
+    # a bad slot_expert is flagged and that slot receives nothing
+    d = oracle.dispatch(np.zeros((5, 1), np.int32), 5, 2, 8, np.array([0, 9], np.int32), *args)
+    assert d["err"] & oracle.ERR_BAD_SLOT_EXPERT and d["slot_counts"].tolist() == [5, 0]
+    # plan weights that overflow 32 bits: flagged, split uniformly
+    d = oracle.dispatch(np.zeros((6, 1), np.int32), 6, 2, 8, np.array([0, 0], np.int32),
+                        np.array([2**31, 2**31], np.uint32), np.zeros(2, np.uint32), np.zeros(2, np.int32))
+    assert d["err"] & oracle.ERR_WEIGHT_OVERFLOW and d["slot_counts"].tolist() == [3, 3]
+
+
+def test_tile_count_matches_paper_staircase():
+    """Eq. 2: T = sum ceil(n/128); 1..128 tokens take one tile, 129 two."""
+    import json, os
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_values.json")))["tile_count"]
+    for n, tiles in g["cases"]:
+        d = oracle.dispatch(np.zeros((n, 1), np.int32), n, 1, g["m_tile"], np.array([0], np.int32),
+                            np.ones(1, np.uint32), np.zeros(1, np.uint32), np.zeros(1, np.int32))
+        assert d["slot_offsets"][-1] // g["m_tile"] == tiles
+
+
+def test_synthetic_workloads_dispatch_invariants():
+    from paper_2608_13057_amd import synth
+    for name in synth.WORKLOADS:
+        wl = synth.make_workload(name, T=256 if "prefill" in name else None)
+        for plan in wl.plans.values():
+            for M in (32, 128):
+                d = oracle.dispatch(wl.topk_ids, wl.T_valid, wl.E, M, wl.placement.slot_expert, plan.slot_weight,
+                                    plan.remote_weight, plan.remote_replicas)
+                assert d["err"] == 0
+                _check_invariants(wl.topk_ids, wl.T_valid, wl.E, M, wl.placement.slot_expert, plan.slot_weight,
+                                  plan.remote_weight, plan.remote_replicas, d)

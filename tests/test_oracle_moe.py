@@ -1,0 +1,167 @@
+"""Pins for the stage-2/3 oracle (gate/up, SwiGLU, down, routing-weighted
+combine; Sec. 2.1) and its number formats.
+
+* bf16 and OCP e4m3 decoding and rounding are checked against torch's own
+  bfloat16 / float8_e4m3fn conversions on the CPU (library routines);
+* the whole forward is checked against a dense numpy formulation (matmul,
+  scipy's expit) on small shapes -- a library computation of the same
+  definition, written independently;
+* the dense-FFN reduction (K = 1, w = 1, one expert), linearity in the routing
+  weights and independence from how an expert's tokens are split across local
+  replicas (split invariance) are checked as properties."""
+import numpy as np
+import pytest
+import torch
+from scipy.special import expit
+
+import oracle
+from paper_2608_13057_amd import synth
+
+
+def test_bf16_decode_matches_torch():
+    codes = np.arange(0, 65536, 97, dtype=np.uint16)
+    ref = torch.from_numpy(codes.view(np.int16)).view(torch.bfloat16).float().numpy()
+    got = np.array([oracle.bf16_value(int(c)) for c in codes])
+    fin = np.isfinite(ref)
+    assert np.array_equal(got[fin], ref[fin].astype(np.float64))
+
+
+def test_e4m3_decode_matches_torch_all_codes():
+    codes = np.arange(256, dtype=np.uint8)
+    ref = torch.from_numpy(codes).view(torch.float8_e4m3fn).float().numpy().astype(np.float64)
+    got = np.array([oracle.e4m3_value(int(c)) for c in codes])
+    assert np.array_equal(np.isnan(got), np.isnan(ref))
+    m = ~np.isnan(ref)
+    assert np.array_equal(got[m], ref[m])
+    assert got[0x7E] == 448.0 and np.isnan(got[0x7F])
+
+
+def test_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    # exact midpoints between neighbouring e4m3 values and between bf16
+    # values: the tie-to-even rule decides these
+    e4 = np.sort(torch.arange(0, 127, dtype=torch.int32).to(torch.uint8).view(torch.float8_e4m3fn).double().numpy())
+    mid_e4 = (e4[1:] + e4[:-1]) / 2
+    bf = torch.from_numpy(np.arange(0x3F00, 0x4100, dtype=np.int16)).view(torch.bfloat16).double().numpy()
+    mid_bf = (bf[1:] + bf[:-1]) / 2
+    v = np.concatenate([rng.standard_normal(3000) * 10.0 ** rng.integers(-3, 3, 3000),
+                        rng.uniform(-448, 448, 2000), mid_e4, -mid_e4, mid_bf, -mid_bf]).astype(np.float32)
+    rb = torch.from_numpy(v).to(torch.bfloat16).float().numpy()
+    re = torch.from_numpy(v).to(torch.float8_e4m3fn).float().numpy()
+    for i in range(len(v)):
+        assert oracle.round_bf16(float(v[i])) == float(rb[i])
+        assert oracle.round_e4m3(float(v[i])) == float(re[i])
+    # the generator's encoder agrees with the same library conversion
+    codes = synth.to_e4m3_codes(v)
+    ref_codes = torch.from_numpy(v).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(codes[np.abs(v) > 0], ref_codes[np.abs(v) > 0])
+
+
+def _small_problem(dtype, T=24, K=2, E=3, S=4, H=256, I=256, seed=5):
+    rng = np.random.default_rng(seed)
+    ids = rng.integers(0, E, size=(T, K)).astype(np.int32)
+    for t in range(T):  # distinct experts per token, as a router emits
+        ids[t] = rng.permutation(E)[:K]
+    w = rng.random((T, K)).astype(np.float32)
+    se = np.array([0, 1, 2, 0][:S], np.int32)
+    x, xs = synth.activations(T, H, seed, dtype)
+    w13, s13, w2, s2 = synth.slot_weights(se, H, I, seed, dtype)
+    return ids, w, se, x, xs, w13, s13, w2, s2
+
+
+def _dense_numpy(x, xs, w13, s13, w2, s2, ids_slot, w, dtype):
+    """Independent dense formulation with numpy matmul and scipy expit."""
+    T, K = ids_slot.shape
+    S, I2, H = w13.shape
+    I = I2 // 2
+    if dtype == "bf16":
+        X = synth.bf16_bits_to_f32(x).astype(np.float64)
+        W13 = synth.bf16_bits_to_f32(w13).astype(np.float64)
+        W2 = synth.bf16_bits_to_f32(w2).astype(np.float64)
+    else:
+        dec = torch.arange(256, dtype=torch.int32).to(torch.uint8).view(torch.float8_e4m3fn).double().numpy()
+        X = dec[x] * np.repeat(xs.astype(np.float64), 128, axis=1)
+        W13 = dec[w13] * np.kron(s13.astype(np.float64), np.ones((1, 128, 128)))
+        W2 = dec[w2] * np.kron(s2.astype(np.float64), np.ones((1, 128, 128)))
+    y = np.zeros((T, H))
+    for s in range(S):
+        U = X @ W13[s].T
+        g, u = U[:, :I], U[:, I:]
+        h = g * expit(g) * u
+        O = h @ W2[s].T
+        for k in range(K):
+            m = ids_slot[:, k] == s
+            y[m] += w[m, k:k + 1].astype(np.float64) * O[m]
+    return y
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_moe_matches_dense_numpy(dtype):
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem(dtype)
+    E, S = 3, len(se)
+    # plan: expert 0 split over slots 0 and 3
+    d = oracle.dispatch(ids, ids.shape[0], E, 16, se, np.ones(S, np.uint32), np.zeros(E, np.uint32),
+                        np.zeros(E, np.int32))
+    ps = oracle.pair_slot(d)
+    y = oracle.moe(x, w, ps, w13, w2, dtype, x_scale=xs, w13_scale=s13, w2_scale=s2)
+    ref = _dense_numpy(x, xs, w13, s13, w2, s2, ps, w, dtype)
+    assert np.max(np.abs(y - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+def test_dense_ffn_reduction():
+    """K = 1, weight 1, one expert: y is the plain SwiGLU FFN of x."""
+    T, H, I = 8, 128, 256
+    x, _ = synth.activations(T, H, 11, "bf16")
+    w13, _, w2, _ = synth.slot_weights(np.array([0], np.int32), H, I, 11, "bf16")
+    ps = np.zeros((T, 1), np.int32)
+    y = oracle.moe(x, np.ones((T, 1), np.float32), ps, w13, w2, "bf16")
+    X = torch.from_numpy(synth.bf16_bits_to_f32(x)).double()
+    A = torch.from_numpy(synth.bf16_bits_to_f32(w13[0])).double()
+    B = torch.from_numpy(synth.bf16_bits_to_f32(w2[0])).double()
+    ref = (torch.nn.functional.silu(X @ A[:I].T) * (X @ A[I:].T)) @ B.T
+    assert np.max(np.abs(y - ref.numpy())) < 1e-12
+
+
+def test_linearity_in_routing_weights():
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem("bf16", T=10)
+    d = oracle.dispatch(ids, 10, 3, 8, se, np.ones(4, np.uint32), np.zeros(3, np.uint32), np.zeros(3, np.int32))
+    ps = oracle.pair_slot(d)
+    y1 = oracle.moe(x, w, ps, w13, w2, "bf16")
+    y2 = oracle.moe(x, (w * np.float32(0.25)), ps, w13, w2, "bf16")  # exact power-of-two scaling
+    assert np.array_equal(y2, y1 * 0.25)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_split_invariance(dtype):
+    """y does not depend on how expert 0's tokens are split over its two
+    local slots (both hold copies of the same weights)."""
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem(dtype)
+    outs = []
+    for sw in ([1, 1, 1, 1], [1, 1, 1, 0], [0, 1, 1, 1], [3, 1, 1, 1]):
+        d = oracle.dispatch(ids, ids.shape[0], 3, 16, se, np.array(sw, np.uint32), np.zeros(3, np.uint32),
+                            np.zeros(3, np.int32))
+        outs.append(oracle.moe(x, w, oracle.pair_slot(d), w13, w2, dtype, x_scale=xs, w13_scale=s13,
+                               w2_scale=s2))
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+def test_mirror_mode_rounds_output_and_stays_close():
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem("fp8")
+    d = oracle.dispatch(ids, ids.shape[0], 3, 16, se, np.ones(4, np.uint32), np.zeros(3, np.uint32),
+                        np.zeros(3, np.int32))
+    ps = oracle.pair_slot(d)
+    ye = oracle.moe(x, w, ps, w13, w2, "fp8", "exact", xs, s13, s2)
+    ym = oracle.moe(x, w, ps, w13, w2, "fp8", "mirror", xs, s13, s2)
+    # mirror-mode y values are bf16-representable
+    yb = torch.from_numpy(ym.astype(np.float32)).to(torch.bfloat16).double().numpy()
+    assert np.array_equal(yb, ym)
+    rel = np.max(np.abs(ym - ye)) / np.max(np.abs(ye))
+    assert 0 < rel < 0.1
+
+
+def test_nonlocal_and_padding_tokens_are_zero():
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem("bf16", T=12)
+    d = oracle.dispatch(ids, 6, 3, 8, se, np.ones(4, np.uint32), np.zeros(3, np.uint32), np.zeros(3, np.int32))
+    y = oracle.moe(x, w, oracle.pair_slot(d), w13, w2, "bf16")
+    assert np.all(y[6:] == 0)
