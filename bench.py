@@ -1,0 +1,236 @@
+#!/usr/bin/env python3
+"""Benchmark: one GPU's share of the expert-parallel MoE block (TEMPO).
+
+A step is one pass of the whole block -- stage 1 dispatch (counts, plan split,
+M-tile padded permute), stage 2 grouped expert FFN (gate/up + SwiGLU, down)
+and stage 3 combine -- over one synthetic batch already resident in HBM.
+Default workload: the Qwen3-235B-shaped decode share (18 local slots = 16 home
+experts of 128 + 2 replicas of the hottest, H 4096, I 1536, bf16, 512
+tokens, top-8, Zipf(1.0) popularity, token-balancing plan).
+
+Prints ONE JSON line with the block time (us/batch, lower is better), the
+roofline of the dominant kernel (the gate/up GEMM, HBM-bound in decode),
+per-stage times, and the CPU oracle timed on the host cores as a baseline.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}  # dense
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="qwen3_decode_bf16")
+    ap.add_argument("--plan", default=None)
+    ap.add_argument("--m-tile", type=int, default=128)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copies", type=int, default=0, help="weight copies rotated per step (0 = auto)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def gemm_bytes(wl, dtype, G, N, which):
+    """Algorithmic HBM bytes of one launch of a stage-2 GEMM: the weights of
+    the G activated slots once, the N real activation rows in, the N real
+    output rows out (padding rows and re-reads are not counted)."""
+    H, I = wl.H, wl.I
+    ew = 2 if dtype == "bf16" else 1
+    if which == "gateup":
+        w = 2 * I * H * ew + (0 if dtype == "bf16" else (2 * I // 128) * (H // 128) * 4)
+        a = H * ew + (0 if dtype == "bf16" else H // 128 * 4)
+        o = I * ew + (0 if dtype == "bf16" else I // 128 * 4)
+    else:
+        w = H * I * ew + (0 if dtype == "bf16" else (H // 128) * (I // 128) * 4)
+        a = I * ew + (0 if dtype == "bf16" else I // 128 * 4)
+        o = H * 2
+    return G * w + N * (a + o)
+
+
+def gemm_flops(wl, N, which):
+    """Useful flops (padding rows excluded): 2 * N * K * Nout."""
+    return 2.0 * N * wl.H * (2 * wl.I if which == "gateup" else wl.I)
+
+
+def cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, m_tile, budget_s):
+    """The oracle as it stands, on the host cores: stage-1 dispatch over the
+    whole batch, then the fp64 expert FFN + combine on a bounded sample of
+    tokens, scaled to the whole batch's local pairs."""
+    import oracle
+
+    t0 = time.perf_counter()
+    d = oracle.dispatch(wl.topk_ids, wl.T_valid, wl.E, m_tile, wl.placement.slot_expert, plan.slot_weight,
+                        plan.remote_weight, plan.remote_replicas)
+    t_disp = time.perf_counter() - t0
+    ps = oracle.pair_slot(d)
+    npairs = ps >= 0
+    loc = np.nonzero(npairs.any(axis=1))[0]
+    total_pairs = int(npairs.sum())
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    # calibrate on a few tokens, then size the sample to the budget
+    rng = np.random.default_rng(0)
+    order = rng.permutation(loc)
+    probe = order[: min(len(order), max(1, threads))]
+    sel = np.zeros(wl.T, np.uint8)
+    sel[probe] = 1
+    t0 = time.perf_counter()
+    oracle.moe(x, wl.topk_w, ps, w13, w2, wl.dtype, "exact", xs, s13, s2, token_sel=sel)
+    t_probe = time.perf_counter() - t0
+    probe_pairs = int(npairs[probe].sum())
+    per_pair = t_probe / max(1, probe_pairs)
+    n_more = int(max(0, budget_s - t_probe) / max(per_pair, 1e-9))
+    sample = order[: min(len(order), len(probe) + max(0, n_more // max(1, wl.K)))]
+    sel = np.zeros(wl.T, np.uint8)
+    sel[sample] = 1
+    t0 = time.perf_counter()
+    oracle.moe(x, wl.topk_w, ps, w13, w2, wl.dtype, "exact", xs, s13, s2, token_sel=sel)
+    t_moe = time.perf_counter() - t0
+    sample_pairs = int(npairs[sample].sum())
+    est = t_disp + t_moe * total_pairs / max(1, sample_pairs)
+    return {
+        "value": est * 1e6,
+        "unit": "us/batch",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"stage-1 oracle on the whole batch ({t_disp * 1e3:.1f} ms) + fp64 expert FFN/combine oracle on "
+                   f"{len(sample)} of {len(loc)} tokens with local pairs ({sample_pairs} of {total_pairs} pairs, "
+                   f"{t_moe:.1f} s), scaled to all {total_pairs} pairs"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs one GPU's share of the EP MoE block on one GPU only; multi-GPU runs (dispatch/"
+              "combine all-to-all over xGMI) are not part of this build.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2608_13057_amd import moe, synth
+    from paper_2608_13057_amd.moe import to_device as to_dev
+
+    wl = synth.make_workload(args.workload, seed=args.seed)
+    plan_name = args.plan or next(iter(wl.plans))
+    plan = wl.plans[plan_name]
+    log(f"workload {args.workload} plan {plan_name} T={wl.T} K={wl.K} E={wl.E} S={wl.S} H={wl.H} I={wl.I}")
+    t0 = time.perf_counter()
+    x, xs = synth.activations(wl.T, wl.H, wl.seed, wl.dtype)
+    w13, s13, w2, s2 = synth.slot_weights(wl.placement.slot_expert, wl.H, wl.I, wl.seed, wl.dtype)
+    log(f"generated inputs in {time.perf_counter() - t0:.1f} s")
+
+    dev = "cuda"
+    shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=args.m_tile, dtype=wl.dtype)
+    d_ids, d_w, d_x = to_dev(wl.topk_ids), to_dev(wl.topk_w), to_dev(x)
+    d_xs = None if xs is None else to_dev(xs)
+    d_plan = moe.PlanTensors(to_dev(wl.placement.slot_expert), to_dev(plan.slot_weight),
+                             to_dev(plan.remote_weight), to_dev(plan.remote_replicas))
+    weights0 = moe.WeightTensors(to_dev(w13), to_dev(w2), None if s13 is None else to_dev(s13),
+                                 None if s2 is None else to_dev(s2))
+    wbytes = weights0.w13.numel() * weights0.w13.element_size() + weights0.w2.numel() * weights0.w2.element_size()
+    # rotate weight copies so that one cycle streams > 2 x the 256 MB Infinity Cache
+    copies = args.copies or max(2, math.ceil(1.0e9 / wbytes))
+    wsets = [weights0] + [moe.WeightTensors(*(None if t is None else t.clone() for t in
+                                              (weights0.w13, weights0.w2, weights0.w13_scale, weights0.w2_scale)))
+                          for _ in range(copies - 1)]
+    ws = moe.Workspace(shape, dev)
+    disp = moe.DispatchBuffers.allocate(shape, ws.row_cap, dev)
+    y = torch.empty(wl.T, wl.H, dtype=torch.int16, device=dev)
+
+    def step(i, evs=None):
+        moe.forward(shape, d_plan, d_ids, d_w, d_x, d_xs, wsets[i % copies], disp, y, ws, stage_events=evs)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    if moe.device_error(ws) != 0:
+        raise RuntimeError("device reported a data error")
+    sc = disp.slot_counts.cpu().numpy()
+    G, N = int((sc > 0).sum()), int(sc.sum())
+    tiles = int(sum(-(-int(c) // args.m_tile) for c in sc))
+    log(f"G={G} N={N} tiles={tiles} slot_counts={sc.tolist()}")
+
+    K = args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(K):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    st = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(K)])  # ms
+    total_ms = evs[0][0].elapsed_time(evs[K - 1][4])
+    ms_per_step = total_ms / K
+    stage_us = {n: float(st[:, j].mean() * 1e3) for j, n in enumerate(("dispatch", "gate_up", "down", "combine"))}
+    log(f"ms/step {ms_per_step:.4f} (wall {t_wall / K * 1e3:.4f}) stages_us {stage_us}")
+
+    gu_s = st[:, 1].mean() * 1e-3
+    dn_s = st[:, 2].mean() * 1e-3
+    gu_bytes = gemm_bytes(wl, wl.dtype, G, N, "gateup")
+    dn_bytes = gemm_bytes(wl, wl.dtype, G, N, "down")
+    block_bytes = gu_bytes + dn_bytes
+    roof = {"bound": "hbm", "achieved": gu_bytes / gu_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gu_bytes / gu_s / 1e9 / HBM_PEAK_GBS, "traffic": None,
+            "kernel": "k_gemm_bf16<gate_up>" if wl.dtype == "bf16" else "k_gemm_fp8<gate_up>",
+            "bytes_per_launch": gu_bytes}
+    mfma = {
+        "gate_up_tflops": gemm_flops(wl, N, "gateup") / gu_s / 1e12,
+        "down_tflops": gemm_flops(wl, N, "down") / dn_s / 1e12,
+        "peak_tflops": MFMA_PEAK_TFLOPS[wl.dtype],
+    }
+    out = {
+        "metric": "per-GPU MoE block us/batch",
+        "value": ms_per_step * 1e3,
+        "unit": "us/batch",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic",
+        "config": {
+            "workload": args.workload,
+            "description": synth.describe(args.workload, plan_name),
+            "m_tile": args.m_tile,
+            "plan": plan_name,
+            "G": G, "N": N, "tiles": tiles,
+            "weight_copies_rotated": copies,
+        },
+        "roofline": roof,
+        "stages_us": stage_us,
+        "block_hbm_gbs": block_bytes / ((gu_s + dn_s)) / 1e9,
+        "mfma": mfma,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle")
+        out["cpu_baseline"] = cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, args.m_tile, args.cpu_budget_s)
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

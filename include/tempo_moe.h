@@ -1,0 +1,230 @@
+/*
+ * tempo_moe.h -- C ABI of an MI355X (gfx950) library that runs one GPU's
+ * share of an expert-parallel MoE block under a per-batch dispatch plan.
+ *
+ * Source of the method: TEMPO, "Makespan-Aware Expert-Parallel Load Balancing
+ * Across Memory- and Compute-Bound Regimes" (arXiv 2608.13057).  The calls
+ * follow the paper's problem statement (Sec. 3.1, Eq. 3): per-expert token
+ * counts n_e come from the router, replica sets R(e) from the placement layer,
+ * and a dispatch assigns each expert's tokens to its replicas in shares
+ * x_{e,g}; a replica with x > 0 is "activated".  On one GPU that is:
+ *
+ *   stage 1  tempo_moe_dispatch  count + plan application + permute into
+ *                                M-tile-padded groups (Sec. 4.4, Sec. 2.2/Eq. 2)
+ *   stage 2  tempo_moe_experts   per local slot: gate/up GEMM, SwiGLU, down
+ *                                GEMM (Sec. 2.1, Sec. 2.2)
+ *   stage 3  tempo_moe_combine   routing-weighted sum over the top-k pairs
+ *                                (Sec. 2.1)
+ *   all      tempo_moe_forward   stages 1-3 in order on one stream
+ *
+ * Conventions for every call
+ *   - Pointers marked "device" are HIP device pointers owned by the caller;
+ *     the library never allocates, frees or keeps them.  Pointers marked
+ *     "host" are read during the call only.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream)
+ *     and the call returns without synchronising.  Inputs must stay valid
+ *     and unmodified until the stream has passed the enqueued work.  No call
+ *     allocates device memory or synchronises (except tempo_moe_device_error),
+ *     so the enqueued work can be captured into a HIP graph.
+ *   - Return value: TEMPO_OK (0) or a TEMPO_E* code.  Argument errors are
+ *     detected on the host before anything is enqueued; nothing is written
+ *     then.  Errors in the *data* (routing ids, plan rows) are detected on the
+ *     device: the offending pair or slot is dropped and a bit is OR-ed into a
+ *     sticky word in the workspace (see tempo_moe_device_error).
+ *   - Matrices are row-major.  bf16 values are stored as their 16-bit
+ *     patterns; fp8 values are OCP E4M3 ("e4m3fn") bytes with fp32 block
+ *     scales: activations use 1 x 128 blocks along the hidden/intermediate
+ *     dimension, weights use 128 x 128 blocks.
+ */
+#ifndef TEMPO_MOE_H
+#define TEMPO_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* return codes */
+#define TEMPO_OK 0
+#define TEMPO_EINVAL 1       /* a null pointer, a bad dimension or m_tile, a mis-sized buffer */
+#define TEMPO_EWORKSPACE 2   /* workspace_bytes smaller than tempo_moe_query's answer */
+#define TEMPO_EDEVICE 3      /* the HIP runtime refused a launch or a copy */
+#define TEMPO_EUNSUPPORTED 4 /* valid but outside what the kernels cover (see tempo_moe_query) */
+
+/* bits of the sticky device error word */
+#define TEMPO_DERR_BAD_ID 1u           /* a routing id not -1 and outside [0, E): pair dropped */
+#define TEMPO_DERR_BAD_SLOT_EXPERT 2u  /* slot_expert[s] outside [0, E): slot receives nothing */
+#define TEMPO_DERR_WEIGHT_OVERFLOW 4u  /* an expert's plan weights sum to >= 2^32: split uniformly */
+
+/* element types */
+#define TEMPO_BF16 0
+#define TEMPO_FP8_E4M3 1
+
+/*
+ * Problem shape.
+ *   T        token rows in the batch buffer (>= 1)
+ *   T_valid  rows [0, T_valid) are real; rows beyond are graph padding, their
+ *            pairs are neither counted nor placed and their y rows are zero
+ *            (Sec. 4.4: counts are masked against graph-padding rows)
+ *   K        experts per token (top-k), 1 <= K <= 32
+ *   E        logical experts, 1 <= E <= 1024
+ *   S        local expert slots (replicas held by this GPU), 1 <= S <= 256
+ *   H, I     hidden and expert-intermediate sizes, multiples of 128
+ *   m_tile   M-tile: every activated slot's rows are padded to a multiple of
+ *            it (Sec. 2.2, Eq. 2); 64 or 128
+ *   dtype    TEMPO_BF16 or TEMPO_FP8_E4M3 (activations and weights)
+ */
+typedef struct tempo_moe_shape {
+  int32_t T, T_valid, K, E, S, H, I, m_tile, dtype;
+} tempo_moe_shape;
+
+/*
+ * Per-batch plan (all device pointers).  Sec. 3.1: x_{e,g} >= 0 with
+ * sum_g x_{e,g} = n_e over the replicas R(e).  On this GPU the replicas of
+ * expert e are its local slots (slot_expert[s] == e, in ascending s) plus,
+ * when remote_weight[e] > 0 or remote_replicas[e] > 0, one entry standing for
+ * all replicas on other GPUs, ordered last.  With weights w_j and W = sum w_j,
+ * entry j receives the expert's pairs of rank [floor(n_e C_{j-1} / W),
+ * floor(n_e C_j / W)) where C_j = w_0 + ... + w_j and ranks order the expert's
+ * valid pairs by p = t*K + k.  Rows are renormalised at use, so any scaling
+ * of a row is the same plan; a row with W = 0 is split uniformly over the
+ * replicas holding the expert (weight 1 per local slot, remote_replicas[e]
+ * for the remote entry), as the paper's kernel does for a torn table row
+ * (Sec. 4.4).
+ *   slot_expert     [S] int32   logical expert held by slot s
+ *   slot_weight     [S] uint32  share weight of slot s
+ *   remote_weight   [E] uint32  share weight kept by replicas on other GPUs
+ *   remote_replicas [E] int32   number of replicas on other GPUs (>= 0)
+ */
+typedef struct tempo_plan {
+  const int32_t* slot_expert;
+  const uint32_t* slot_weight;
+  const uint32_t* remote_weight;
+  const int32_t* remote_replicas;
+} tempo_plan;
+
+/*
+ * Stage-1 outputs (all device pointers, caller-allocated).  row_cap comes
+ * from tempo_moe_query.  Slot s owns rows [slot_offsets[s], slot_offsets[s+1])
+ * = P_s = m_tile * ceil(c_s / m_tile) rows, of which the first c_s are real
+ * and the rest are padding.
+ *   expert_counts [E] int32   n_e over valid pairs, for all E experts
+ *   slot_counts   [S] int32   c_s
+ *   slot_offsets  [S+1] int32 exclusive prefix sum of P_s
+ *   row_token     [row_cap] int32  token of each row; -1 on padding rows.
+ *                 Entries at or beyond slot_offsets[S] are not written.
+ *   pair_row      [T*K] int32 row of pair p = t*K + k, -1 if the pair is not
+ *                 placed on this GPU (remote share, dropped id, padding row)
+ *   cum_counts    [E] uint32  nullable; if given, cum_counts[e] += n_e
+ *                 (mod 2^32): the paper's persistent cumulative counter whose
+ *                 window counts are recovered by wrap-safe differencing
+ *   x_perm        [row_cap, H] bf16 or fp8: x_perm[row] = x[row_token[row]]
+ *                 on real rows; padding rows are not written
+ *   x_perm_scale  [row_cap, H/128] fp32, fp8 only (NULL for bf16)
+ */
+typedef struct tempo_dispatch_out {
+  int32_t* expert_counts;
+  int32_t* slot_counts;
+  int32_t* slot_offsets;
+  int32_t* row_token;
+  int32_t* pair_row;
+  uint32_t* cum_counts;
+  void* x_perm;
+  float* x_perm_scale;
+} tempo_dispatch_out;
+
+/*
+ * Expert weights of the S local slots (device pointers).  A replica slot
+ * holds its own copy of its expert's weights.
+ *   w13       [S, 2I, H]  rows 0..I-1 gate projection, rows I..2I-1 up projection
+ *   w13_scale [S, 2I/128, H/128] fp32, fp8 only
+ *   w2        [S, H, I]   down projection
+ *   w2_scale  [S, H/128, I/128] fp32, fp8 only
+ */
+typedef struct tempo_expert_weights {
+  const void* w13;
+  const float* w13_scale;
+  const void* w2;
+  const float* w2_scale;
+} tempo_expert_weights;
+
+/*
+ * Sizes for a shape.  *workspace_bytes: the workspace every other call needs
+ * (one per stream in flight); *row_cap = T*K + S*(m_tile-1), the rows of the
+ * permuted buffers.  The workspace must be zero-filled once before its first
+ * use (it holds the sticky error word); after that it is reused without
+ * clearing.  Returns TEMPO_EINVAL / TEMPO_EUNSUPPORTED for shapes the library
+ * rejects.  Either output pointer may be NULL.
+ */
+int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap);
+
+/*
+ * Stage 1 (Sec. 4.4 fused count collection + dispatch, Sec. 2.2 / Eq. 2
+ * M-tile padding).  topk_ids [T, K] int32 device, -1 = no expert.
+ * x [T, H] device (bf16 or fp8), x_scale [T, H/128] fp32 device (fp8 only,
+ * else NULL).  Deterministic: positions come from a stable counting sort,
+ * never from atomics.
+ */
+int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
+                       const void* x, const float* x_scale, const tempo_dispatch_out* out, void* workspace,
+                       size_t workspace_bytes, void* stream);
+
+/*
+ * Stage 2 (Sec. 2.1 "gate/up, activation, down"; Sec. 2.2 weight streaming).
+ * For every slot with c_s > 0: h = silu(x_perm W_gate^T) * (x_perm W_up^T)
+ * with silu(z) = z / (1 + e^-z), then y_perm = h W2^T.  Slots with c_s = 0
+ * read no weights.  Reads slot_counts / slot_offsets / x_perm (and
+ * x_perm_scale) of a stage-1 result from device memory, so no host round
+ * trip is needed.  y_perm [row_cap, H] bf16 device: real rows written,
+ * padding rows not.  Accumulation is fp32; h is rounded to bf16 (bf16 path)
+ * or quantised to e4m3 with 1 x 128 fp32 scales amax/448 (fp8 path); y_perm
+ * is rounded to bf16.  The arithmetic of a row does not depend on which slot
+ * or tile it lands in.
+ */
+int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* disp,
+                      const tempo_expert_weights* weights, void* y_perm, void* workspace, size_t workspace_bytes,
+                      void* stream);
+
+/*
+ * Stage 3 (Sec. 2.1 combine).  y[t] = sum over k ascending of
+ * topk_w[t,k] * y_perm[pair_row[t,k]] over pairs with pair_row >= 0, in fp32,
+ * rounded to bf16; rows with no local pair and rows t >= T_valid are zero.
+ * topk_w [T, K] fp32 device; y [T, H] bf16 device.  On an EP group, y is
+ * this GPU's partial sum that the combine all-to-all would add up.
+ */
+int tempo_moe_combine(const tempo_moe_shape* shape, const int32_t* pair_row, const float* topk_w,
+                      const void* y_perm, void* y, void* stream);
+
+/*
+ * Stages 1-3 on one stream.  disp receives the stage-1 outputs (caller
+ * buffers as for tempo_moe_dispatch); y_perm lives in the workspace.
+ * slot_time_ns [S] uint64 device, nullable: per slot, the span from the
+ * first stage-2 tile that started on it to the last that ended, measured
+ * with the GPU's 100 MHz real-time counter (0 for slots with c_s = 0).
+ * Spans of concurrently running slots overlap; it is exact for one slot.
+ * stage_events: nullable host array of 5 hipEvent_t (created by the caller)
+ * recorded on `stream` before stage 1, after stage 1, after the gate/up GEMM,
+ * after the down GEMM and after stage 3, for per-stage timing.
+ */
+int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
+                      const float* topk_w, const void* x, const float* x_scale, const tempo_expert_weights* weights,
+                      const tempo_dispatch_out* disp, void* y, uint64_t* slot_time_ns, void* const* stage_events,
+                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Synchronises `stream`, returns the sticky device error word (OR of the
+ * TEMPO_DERR_* bits seen by every dispatch since the last read) in *bits and
+ * clears it.  Returns TEMPO_EDEVICE if the synchronisation fails.
+ */
+int tempo_moe_device_error(void* workspace, void* stream, uint32_t* bits);
+
+/* A static string describing a TEMPO_* return code. */
+const char* tempo_moe_strerror(int code);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TEMPO_MOE_H */

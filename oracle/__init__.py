@@ -57,6 +57,10 @@ def _load():
         lib.oracle_dispatch.argtypes = [i32] * 6 + [P] * 11
         lib.oracle_moe.restype = None
         lib.oracle_moe.argtypes = [i32] * 7 + [P] * 10
+        lib.oracle_ffn_rows.restype = None
+        lib.oracle_ffn_rows.argtypes = [i32] * 5 + [P] * 9
+        lib.oracle_combine.restype = None
+        lib.oracle_combine.argtypes = [i32] * 4 + [P] * 4
         for n in ("oracle_bf16_value",):
             getattr(lib, n).restype = ctypes.c_double
             getattr(lib, n).argtypes = [ctypes.c_uint16]
@@ -158,6 +162,42 @@ def moe(x, topk_w, pslot, w13, w2, dtype: str, mode: str = "exact", x_scale=None
     lib.oracle_moe(T, K, H, I, S, dt, md, _p(x), None if xs is None else _p(xs), _p(w13c),
                    None if s13 is None else _p(s13), _p(w2c), None if s2 is None else _p(s2), _p(tw), _p(ps),
                    _p(sel), _p(y))
+    return y
+
+
+def ffn_rows(x, tok, slot, w13, w2, dtype: str, mode: str = "exact", x_scale=None, w13_scale=None,
+             w2_scale=None) -> np.ndarray:
+    """Stage 2 alone, per row: o[r] = FFN of expert slot[r] applied to
+    x[tok[r]] (fp64).  Rows with slot < 0 are zero."""
+    lib = _load()
+    x = np.ascontiguousarray(x)
+    T, H = x.shape
+    S, I2, _ = w13.shape
+    I = I2 // 2
+    tok = np.ascontiguousarray(tok, np.int32)
+    slot = np.ascontiguousarray(slot, np.int32)
+    R = len(tok)
+    out = np.zeros((R, H), np.float64)
+    dt = {"bf16": 0, "fp8": 1}[dtype]
+    md = {"exact": 0, "mirror": 1}[mode]
+    keep = [np.ascontiguousarray(a, np.float32) if a is not None else None for a in (x_scale, w13_scale, w2_scale)]
+    w13c, w2c = np.ascontiguousarray(w13), np.ascontiguousarray(w2)
+    lib.oracle_ffn_rows(R, H, I, dt, md, _p(x), None if keep[0] is None else _p(keep[0]), _p(tok), _p(slot),
+                        _p(w13c), None if keep[1] is None else _p(keep[1]), _p(w2c),
+                        None if keep[2] is None else _p(keep[2]), _p(out))
+    return out
+
+
+def combine(pair_row, topk_w, y_perm_bits, T_valid) -> np.ndarray:
+    """Stage 3 alone: routing-weighted sum of bf16 rows, fp64."""
+    lib = _load()
+    pr = np.ascontiguousarray(pair_row, np.int32)
+    T, K = pr.shape
+    yp = np.ascontiguousarray(y_perm_bits, np.uint16)
+    H = yp.shape[1]
+    tw = np.ascontiguousarray(topk_w, np.float32)
+    y = np.zeros((T, H), np.float64)
+    lib.oracle_combine(T, T_valid, K, H, _p(pr), _p(tw), _p(yp), _p(y))
     return y
 
 

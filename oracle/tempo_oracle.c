@@ -261,6 +261,42 @@ static double w_at(int dtype, const void* w, const float* ws, size_t slot_elems,
   return e4m3_value(((const uint8_t*)w)[idx]) * (double)ws[sidx];
 }
 
+/* One pair's expert FFN: o = W2_s (silu(W_gate,s x) * (W_up,s x)), x given in
+ * fp64 (already dequantised).  hv [I] is scratch; o [H] receives the result.
+ * mode 1 rounds h (bf16, or e4m3 with 1 x 128 scales amax/448) and o (bf16). */
+static void ffn_one(int H, int I, int dtype, int mode, const double* xv, int s, const void* w13,
+                    const float* w13_scale, const void* w2, const float* w2_scale, double* hv, double* o) {
+  size_t w13_elems = (size_t)2 * I * H, w2_elems = (size_t)H * I;
+  /* gate/up projections and SwiGLU: h = silu(g) * u, silu(g) = g/(1+e^-g) */
+  for (int i = 0; i < I; i++) {
+    double g = 0.0, u = 0.0;
+    for (int h = 0; h < H; h++) {
+      g += w_at(dtype, w13, w13_scale, w13_elems, 2 * I, H, s, i, h) * xv[h];
+      u += w_at(dtype, w13, w13_scale, w13_elems, 2 * I, H, s, I + i, h) * xv[h];
+    }
+    hv[i] = g / (1.0 + exp(-g)) * u;
+  }
+  if (mode == 1) {
+    if (dtype == 0) {
+      for (int i = 0; i < I; i++) hv[i] = round_bf16(hv[i]);
+    } else {
+      /* 1 x 128 block quantisation: scale = amax / 448, q = e4m3(h / scale) */
+      for (int b = 0; b < I / 128; b++) {
+        double amax = 0.0;
+        for (int i = b * 128; i < b * 128 + 128; i++) amax = fmax(amax, fabs(hv[i]));
+        double sc = amax > 0.0 ? amax / 448.0 : 1.0;
+        for (int i = b * 128; i < b * 128 + 128; i++) hv[i] = round_e4m3(hv[i] / sc) * sc;
+      }
+    }
+  }
+  /* down projection */
+  for (int j = 0; j < H; j++) {
+    double acc = 0.0;
+    for (int i = 0; i < I; i++) acc += w_at(dtype, w2, w2_scale, w2_elems, H, I, s, j, i) * hv[i];
+    o[j] = (mode == 1) ? round_bf16(acc) : acc;
+  }
+}
+
 /*
  *   x [T, H], x_scale [T, H/128] (fp8 only)
  *   w13 [S, 2I, H] rows 0..I-1 = gate, I..2I-1 = up; w13_scale [S, 2I/128, H/128]
@@ -268,60 +304,70 @@ static double w_at(int dtype, const void* w, const float* ws, size_t slot_elems,
  *   topk_w [T*K] fp32 routing weights
  *   pair_slot [T*K]  local slot of each pair, -1 = not local
  *   token_sel [T]    nonzero = compute this token's row of y (others untouched)
- *   y [T, H] double  output
+ *   y [T, H] double  output: y[t] = sum over k ascending of w[t,k] * o_{t,k}
+ *                    over the token's local pairs (mode 1: rounded to bf16)
  */
 void oracle_moe(int T, int K, int H, int I, int S, int dtype, int mode, const void* x, const float* x_scale,
                 const void* w13, const float* w13_scale, const void* w2, const float* w2_scale,
                 const float* topk_w, const int32_t* pair_slot, const uint8_t* token_sel, double* y) {
-  size_t w13_elems = (size_t)2 * I * H, w2_elems = (size_t)H * I;
   (void)S;
 #pragma omp parallel for schedule(dynamic, 1)
   for (int t = 0; t < T; t++) {
     if (!token_sel[t]) continue;
     double* xv = (double*)malloc(sizeof(double) * (size_t)H);
     double* hv = (double*)malloc(sizeof(double) * (size_t)I);
+    double* o = (double*)malloc(sizeof(double) * (size_t)H);
     double* yt = y + (size_t)t * H;
     for (int j = 0; j < H; j++) yt[j] = 0.0;
     for (int h = 0; h < H; h++) xv[h] = x_at(dtype, x, x_scale, H, t, h);
     for (int k = 0; k < K; k++) {
       int s = pair_slot[t * K + k];
       if (s < 0) continue;
-      /* gate/up projections and SwiGLU: h = silu(g) * u, silu(g) = g/(1+e^-g) */
-      for (int i = 0; i < I; i++) {
-        double g = 0.0, u = 0.0;
-        for (int h = 0; h < H; h++) {
-          g += w_at(dtype, w13, w13_scale, w13_elems, 2 * I, H, s, i, h) * xv[h];
-          u += w_at(dtype, w13, w13_scale, w13_elems, 2 * I, H, s, I + i, h) * xv[h];
-        }
-        hv[i] = g / (1.0 + exp(-g)) * u;
-      }
-      if (mode == 1) {
-        if (dtype == 0) {
-          for (int i = 0; i < I; i++) hv[i] = round_bf16(hv[i]);
-        } else {
-          /* 1 x 128 block quantisation: scale = amax / 448, q = e4m3(h / scale) */
-          for (int b = 0; b < I / 128; b++) {
-            double amax = 0.0;
-            for (int i = b * 128; i < b * 128 + 128; i++) amax = fmax(amax, fabs(hv[i]));
-            double sc = amax > 0.0 ? amax / 448.0 : 1.0;
-            for (int i = b * 128; i < b * 128 + 128; i++) hv[i] = round_e4m3(hv[i] / sc) * sc;
-          }
-        }
-      }
-      /* down projection, then the routing-weighted sum in ascending k */
+      ffn_one(H, I, dtype, mode, xv, s, w13, w13_scale, w2, w2_scale, hv, o);
       double wk = (double)topk_w[t * K + k];
-      for (int j = 0; j < H; j++) {
-        double o = 0.0;
-        for (int i = 0; i < I; i++) o += w_at(dtype, w2, w2_scale, w2_elems, H, I, s, j, i) * hv[i];
-        if (mode == 1) o = round_bf16(o);
-        yt[j] += wk * o;
-      }
+      for (int j = 0; j < H; j++) yt[j] += wk * o[j];
     }
     if (mode == 1)
       for (int j = 0; j < H; j++) yt[j] = round_bf16(yt[j]);
     free(xv);
     free(hv);
+    free(o);
   }
+}
+
+/* Stage 2 alone: o for each selected (token, slot) row.  tok [R], slot [R];
+ * out [R, H] double.  Rows with slot < 0 are left untouched. */
+void oracle_ffn_rows(int R, int H, int I, int dtype, int mode, const void* x, const float* x_scale,
+                     const int32_t* tok, const int32_t* slot, const void* w13, const float* w13_scale,
+                     const void* w2, const float* w2_scale, double* out) {
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int r = 0; r < R; r++) {
+    if (slot[r] < 0) continue;
+    double* xv = (double*)malloc(sizeof(double) * (size_t)H);
+    double* hv = (double*)malloc(sizeof(double) * (size_t)I);
+    for (int h = 0; h < H; h++) xv[h] = x_at(dtype, x, x_scale, H, tok[r], h);
+    ffn_one(H, I, dtype, mode, xv, slot[r], w13, w13_scale, w2, w2_scale, hv, out + (size_t)r * H);
+    free(xv);
+    free(hv);
+  }
+}
+
+/* Stage 3 alone: y[t] = sum over k ascending with pair_row >= 0 of
+ * w[t,k] * y_perm[pair_row[t,k]] (y_perm given as bf16 bits), for t < T_valid;
+ * zero elsewhere.  y [T, H] double. */
+void oracle_combine(int T, int T_valid, int K, int H, const int32_t* pair_row, const float* topk_w,
+                    const uint16_t* y_perm, double* y) {
+  for (int t = 0; t < T; t++)
+    for (int j = 0; j < H; j++) {
+      double acc = 0.0;
+      if (t < T_valid)
+        for (int k = 0; k < K; k++) {
+          int r = pair_row[t * K + k];
+          if (r < 0) continue;
+          acc += (double)topk_w[t * K + k] * bf16_value(y_perm[(size_t)r * H + j]);
+        }
+      y[(size_t)t * H + j] = acc;
+    }
 }
 
 /* exported helpers so the tests can pin the number formats themselves */

@@ -1,0 +1,213 @@
+// Host side of the C ABI declared in include/tempo_moe.h: argument
+// validation (before anything is enqueued), workspace layout, and the
+// stream-ordered launches of the stage kernels.  No call allocates device
+// memory or synchronises, except tempo_moe_device_error.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cstring>
+
+#include "internal.h"
+
+namespace tempo {
+
+static size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
+
+Layout make_layout(const tempo_moe_shape& s) {
+  Layout L{};
+  const size_t P = (size_t)s.T * s.K;
+  L.nblk = (int)((P + kCountChunk - 1) / kCountChunk);
+  L.row_cap = (int)(P + (size_t)s.S * (s.m_tile - 1));
+  const size_t eh = s.dtype == TEMPO_BF16 ? 2 : 1;
+  size_t o = 0;
+  L.header = o;
+  o = align_up(o + 256);
+  L.blk_hist = o;
+  o = align_up(o + (size_t)L.nblk * s.E * 4);
+  L.blk_err = o;
+  o = align_up(o + (size_t)L.nblk * 4);
+  L.local_rank = o;
+  o = align_up(o + P * 4);
+  L.slot_lo = o;
+  o = align_up(o + (size_t)s.S * 4);
+  L.slot_t0 = o;
+  o = align_up(o + (size_t)s.S * 8);
+  L.slot_t1 = o;
+  o = align_up(o + (size_t)s.S * 8);
+  L.h = o;
+  o = align_up(o + (size_t)L.row_cap * s.I * eh);
+  L.h_scale = o;
+  o = align_up(o + (s.dtype == TEMPO_BF16 ? 0 : (size_t)L.row_cap * (s.I / 128) * 4));
+  L.y_perm = o;
+  o = align_up(o + (size_t)L.row_cap * s.H * 2);
+  L.total = o;
+  return L;
+}
+
+int persistent_grid() {
+  static std::atomic<int> cached{0};
+  int g = cached.load();
+  if (g > 0) return g;
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  g = ((cus * 2 + 7) / 8) * 8;
+  cached.store(g);
+  return g;
+}
+
+static int check_shape(const tempo_moe_shape* s) {
+  if (!s) return TEMPO_EINVAL;
+  if (s->T < 1 || s->T_valid < 0 || s->T_valid > s->T || s->K < 1 || s->E < 1 || s->S < 1 || s->H < 128 ||
+      s->I < 128)
+    return TEMPO_EINVAL;
+  if (s->K > kMaxK || s->K > s->E || s->E > kMaxE || s->S > kMaxS) return TEMPO_EINVAL;
+  if (s->H % 128 || s->I % 128) return TEMPO_EINVAL;
+  if (s->m_tile != 64 && s->m_tile != 128) return TEMPO_EINVAL;
+  if (s->dtype != TEMPO_BF16 && s->dtype != TEMPO_FP8_E4M3) return TEMPO_EINVAL;
+  // row indices and element offsets stay within int32 / the addressable range
+  const long long P = (long long)s->T * s->K;
+  const long long cap = P + (long long)s->S * (s->m_tile - 1);
+  if (P > (1ll << 26) || cap * (long long)s->H > (1ll << 40)) return TEMPO_EUNSUPPORTED;
+  return TEMPO_OK;
+}
+
+static int check_plan(const tempo_plan* p) {
+  if (!p || !p->slot_expert || !p->slot_weight || !p->remote_weight || !p->remote_replicas) return TEMPO_EINVAL;
+  return TEMPO_OK;
+}
+
+static int check_disp(const tempo_moe_shape* s, const tempo_dispatch_out* d, bool need_index_outputs) {
+  if (!d || !d->slot_counts || !d->slot_offsets || !d->x_perm) return TEMPO_EINVAL;
+  if (need_index_outputs && (!d->expert_counts || !d->row_token || !d->pair_row)) return TEMPO_EINVAL;
+  if (s->dtype == TEMPO_FP8_E4M3 && !d->x_perm_scale) return TEMPO_EINVAL;
+  return TEMPO_OK;
+}
+
+static int check_weights(const tempo_moe_shape* s, const tempo_expert_weights* w) {
+  if (!w || !w->w13 || !w->w2) return TEMPO_EINVAL;
+  if (s->dtype == TEMPO_FP8_E4M3 && (!w->w13_scale || !w->w2_scale)) return TEMPO_EINVAL;
+  return TEMPO_OK;
+}
+
+static int dev_status(hipError_t e) { return e == hipSuccess ? TEMPO_OK : TEMPO_EDEVICE; }
+
+
+}  // namespace tempo
+
+using namespace tempo;
+
+extern "C" {
+
+int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  const Layout L = make_layout(*shape);
+  if (workspace_bytes) *workspace_bytes = L.total;
+  if (row_cap) *row_cap = L.row_cap;
+  return TEMPO_OK;
+}
+
+int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids, const void* x,
+                       const float* x_scale, const tempo_dispatch_out* out, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_plan(plan)) || (rc = check_disp(shape, out, true))) return rc;
+  if (!topk_ids || !x || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale)) return TEMPO_EINVAL;
+  const Layout L = make_layout(*shape);
+  if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
+  return dev_status(launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *out, static_cast<char*>(workspace), L,
+                                    false, static_cast<hipStream_t>(stream)));
+}
+
+int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* disp,
+                      const tempo_expert_weights* weights, void* y_perm, void* workspace, size_t workspace_bytes,
+                      void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_disp(shape, disp, false)) || (rc = check_weights(shape, weights))) return rc;
+  if (!y_perm || !workspace) return TEMPO_EINVAL;
+  const Layout L = make_layout(*shape);
+  if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
+  if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = shape->dtype == TEMPO_BF16
+                           ? launch_experts_bf16(*shape, *disp, *weights, y_perm, ws, L, false, nullptr, st)
+                           : launch_experts_fp8(*shape, *disp, *weights, y_perm, ws, L, false, nullptr, st);
+  if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
+  return dev_status(e);
+}
+
+int tempo_moe_combine(const tempo_moe_shape* shape, const int32_t* pair_row, const float* topk_w,
+                      const void* y_perm, void* y, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!pair_row || !topk_w || !y_perm || !y) return TEMPO_EINVAL;
+  return dev_status(launch_combine(*shape, pair_row, topk_w, y_perm, y, nullptr, nullptr, nullptr, nullptr,
+                                   static_cast<hipStream_t>(stream)));
+}
+
+int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
+                      const float* topk_w, const void* x, const float* x_scale, const tempo_expert_weights* weights,
+                      const tempo_dispatch_out* disp, void* y, uint64_t* slot_time_ns, void* const* stage_events,
+                      void* workspace, size_t workspace_bytes, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if ((rc = check_plan(plan)) || (rc = check_disp(shape, disp, true)) || (rc = check_weights(shape, weights)))
+    return rc;
+  if (!topk_ids || !topk_w || !x || !y || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale))
+    return TEMPO_EINVAL;
+  const Layout L = make_layout(*shape);
+  if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const bool timing = slot_time_ns != nullptr;
+  void* y_perm = ws + L.y_perm;
+  hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  if (stage_events)
+    for (int i = 0; i < 5; i++) ev[i] = static_cast<hipEvent_t>(stage_events[i]);
+  auto mark = [&](int i) { return !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
+  if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
+  if (!mark(0)) return TEMPO_EDEVICE;
+  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, st);
+  if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
+  e = shape->dtype == TEMPO_BF16 ? launch_experts_bf16(*shape, *disp, *weights, y_perm, ws, L, timing, ev[2], st)
+                                 : launch_experts_fp8(*shape, *disp, *weights, y_perm, ws, L, timing, ev[2], st);
+  if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
+  if (e != hipSuccess || !mark(3)) return TEMPO_EDEVICE;
+  e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,
+                     reinterpret_cast<const uint64_t*>(ws + L.slot_t0),
+                     reinterpret_cast<const uint64_t*>(ws + L.slot_t1), slot_time_ns, st);
+  if (e != hipSuccess || !mark(4)) return TEMPO_EDEVICE;
+  return TEMPO_OK;
+}
+
+int tempo_moe_device_error(void* workspace, void* stream, uint32_t* bits) {
+  if (!workspace || !bits) return TEMPO_EINVAL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  uint32_t v = 0;
+  uint32_t* word = reinterpret_cast<uint32_t*>(static_cast<char*>(workspace)) + kHdrSticky;
+  if (hipMemcpyAsync(&v, word, sizeof(v), hipMemcpyDeviceToHost, st) != hipSuccess) return TEMPO_EDEVICE;
+  if (hipStreamSynchronize(st) != hipSuccess) return TEMPO_EDEVICE;
+  const uint32_t zero = 0;
+  if (hipMemcpyAsync(word, &zero, sizeof(zero), hipMemcpyHostToDevice, st) != hipSuccess) return TEMPO_EDEVICE;
+  if (hipStreamSynchronize(st) != hipSuccess) return TEMPO_EDEVICE;
+  *bits = v;
+  return TEMPO_OK;
+}
+
+const char* tempo_moe_strerror(int code) {
+  switch (code) {
+    case TEMPO_OK: return "ok";
+    case TEMPO_EINVAL: return "invalid argument";
+    case TEMPO_EWORKSPACE: return "workspace too small";
+    case TEMPO_EDEVICE: return "HIP runtime error";
+    case TEMPO_EUNSUPPORTED: return "unsupported shape or type";
+    default: return "unknown error";
+  }
+}
+
+}  // extern "C"

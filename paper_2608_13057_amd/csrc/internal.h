@@ -1,0 +1,78 @@
+// Internal declarations shared by the HIP translation units of libtempo_moe.
+// Not part of the public ABI (include/tempo_moe.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/tempo_moe.h"
+
+namespace tempo {
+
+// Pairs handled by one block of the counting kernel (and the granularity of
+// the per-block histograms).
+constexpr int kCountChunk = 1024;
+constexpr int kCountThreads = 256;
+// Pairs handled by one block of the scatter/gather kernel.
+constexpr int kScatterPairs = 32;
+
+constexpr int kMaxE = 1024;
+constexpr int kMaxS = 256;
+constexpr int kMaxK = 32;
+
+// Workspace header words (uint32 slots at the start of the workspace).
+enum HeaderWord : int {
+  kHdrSticky = 0,  // OR of the device error bits since the last read
+  kHdrLastErr = 1, // error bits of the last dispatch
+  kHdrTiles = 2,   // sum over slots of P_s / m_tile
+  kHdrActive = 3,  // G: slots with c_s > 0
+  kHdrPairs = 4,   // N: pairs placed locally
+};
+
+// Byte offsets of the workspace regions for one shape.
+struct Layout {
+  size_t header;      // 256 B of uint32 words
+  size_t blk_hist;    // [nblk][E] int32 per-block counts, then per-block prefixes
+  size_t blk_err;     // [nblk] uint32
+  size_t local_rank;  // [T*K] int32 stable rank of a pair within its block and expert
+  size_t slot_lo;     // [S] int32 first rank (within its expert) taken by slot s
+  size_t slot_t0;     // [S] uint64 first stage-2 tile start (real-time counter)
+  size_t slot_t1;     // [S] uint64 last stage-2 tile end
+  size_t h;           // [row_cap, I] bf16 or e4m3
+  size_t h_scale;     // [row_cap, I/128] fp32 (fp8 only)
+  size_t y_perm;      // [row_cap, H] bf16
+  size_t total;
+  int nblk;
+  int row_cap;
+};
+
+Layout make_layout(const tempo_moe_shape& s);
+
+inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// ---- launchers (stream-ordered, no synchronisation) ----
+hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids,
+                           const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
+                           const Layout& L, bool timing, hipStream_t st);
+
+// mid_event (nullable) is recorded between the gate/up and the down GEMM.
+hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
+                               void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid_event,
+                               hipStream_t st);
+
+hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
+                              void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid_event,
+                              hipStream_t st);
+
+hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
+                          void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
+                          uint64_t* slot_time_ns, hipStream_t st);
+
+// Whether stage-2 kernels exist for this shape's element type and M-tile.
+bool experts_supported(const tempo_moe_shape& s);
+
+// Number of workgroups of the persistent stage-2 kernels.
+int persistent_grid();
+
+}  // namespace tempo

@@ -45,10 +45,14 @@ EP_GROUP = 8
 # --------------------------------------------------------------------------
 
 def to_bf16_bits(a: np.ndarray) -> np.ndarray:
-    """fp32 -> bf16 bit patterns (uint16), round to nearest even."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    r = ((u >> 16) & 1) + 0x7FFF
-    return ((u + r) >> 16).astype(np.uint16)
+    """fp32 -> bf16 bit patterns (uint16), round to nearest even (finite
+    inputs: the rounding increment cannot carry out of 32 bits)."""
+    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
+    r = (u >> 16) & np.uint32(1)
+    r += np.uint32(0x7FFF)
+    r += u
+    r >>= 16
+    return r.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -56,27 +60,23 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 
 
 def to_e4m3_codes(v: np.ndarray) -> np.ndarray:
-    """Values with |v| <= 448 (larger magnitudes saturate) -> OCP e4m3 codes,
-    round to nearest even."""
-    v = np.asarray(v, dtype=np.float64)
-    a = np.minimum(np.abs(v), 448.0)
-    sign = (v < 0).astype(np.uint8) << 7
-    code = np.zeros(a.shape, np.int64)
-    sub = a < 2.0 ** -6
-    # subnormals: multiples of 2^-9 (code = m); m == 8 lands on the first normal
-    code[sub] = np.round(a[sub] * 2.0 ** 9).astype(np.int64)
-    nrm = ~sub
-    an = a[nrm]
-    e = np.floor(np.log2(an)).astype(np.int64)
-    # guard log2 rounding at exact powers of two
-    e = np.where(2.0 ** e > an, e - 1, e)
-    e = np.where(2.0 ** (e + 1) <= an, e + 1, e)
-    m = np.round((an / 2.0 ** e - 1.0) * 8.0).astype(np.int64)
-    carry = m == 8
-    e = np.where(carry, e + 1, e)
-    m = np.where(carry, 0, m)
-    code[nrm] = ((e + 7) << 3) | m
-    return (code.astype(np.uint8) | sign).astype(np.uint8)
+    """fp32 values -> OCP e4m3 codes, round to nearest even, magnitudes
+    saturated at 448.  Normal range: round the fp32 significand to 3 bits
+    (the carry runs into the exponent field); subnormal range (|v| < 2^-6):
+    the nearest multiple of 2^-9, ties to even."""
+    f = np.ascontiguousarray(v, dtype=np.float32)
+    a = np.minimum(np.abs(f), np.float32(448.0))
+    ab = a.view(np.uint32)
+    r = (ab >> 20) & np.uint32(1)
+    r += np.uint32(0x7FFFF)
+    r += ab
+    r >>= 20
+    normal = a >= np.float32(2.0 ** -6)
+    # code = rounded (exponent, 3-bit mantissa) rebased from bias 127 to bias 7
+    code = np.where(normal, r.view(np.int32) - np.int32((127 - 7) << 3),
+                    np.rint(a * np.float32(512.0)).astype(np.int32))
+    sign = (f.view(np.uint32) >> 24).astype(np.uint8) & np.uint8(0x80)
+    return code.astype(np.uint8) | sign
 
 
 def quant_rows_1x128(x: np.ndarray):
@@ -93,7 +93,7 @@ def quant_blocks_128x128(w: np.ndarray):
     """[R, C] fp32 -> (e4m3 codes [R, C], fp32 scales [R/128, C/128])."""
     R, C = w.shape
     wb = w.reshape(R // 128, 128, C // 128, 128).astype(np.float32)
-    amax = np.abs(wb).max(axis=(1, 3))
+    amax = np.abs(wb).max(axis=3).max(axis=1)
     sc = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
     q = to_e4m3_codes(wb / sc[:, None, :, None])
     return q.reshape(R, C), sc
@@ -288,10 +288,12 @@ def slot_weights(slot_expert: np.ndarray, H: int, I: int, seed: int, dtype: str)
     if dtype == "fp8":
         s13 = np.empty((S, 2 * I // 128, H // 128), np.float32)
         s2 = np.empty((S, H // 128, I // 128), np.float32)
-    cache = {}
+    from concurrent.futures import ThreadPoolExecutor
+
+    uniq = sorted(set(slot_expert.tolist()))
+    with ThreadPoolExecutor(max_workers=min(8, len(uniq))) as ex:
+        cache = dict(zip(uniq, ex.map(lambda e: expert_weights(e, H, I, seed, dtype), uniq)))
     for s, e in enumerate(slot_expert.tolist()):
-        if e not in cache:
-            cache[e] = expert_weights(e, H, I, seed, dtype)
         a, sa, b, sb = cache[e]
         w13[s] = a
         w2[s] = b
@@ -360,3 +362,12 @@ def make_workload(name: str, seed: int = 0, T: int | None = None) -> Workload:
         else:
             P[p] = plan_token_balancing(pl, E, ids, T)
     return Workload(name, dtype, T, T, K, E, H, I, s, pl, P, ids, w, seed)
+
+
+def describe(name: str, plan: str | None = None) -> str:
+    """One-line description of a named workload."""
+    dtype, T, K, E, H, I, s, pk, plans = WORKLOADS[name]
+    S = {"local_hot": lambda: pk[1] + pk[2], "local_hot_strided": lambda: pk[1] + pk[2],
+         "remote_hot": lambda: E // EP_GROUP + pk[1]}[pk[0]]()
+    return (f"{S} local slots ({pk[0]} placement), H {H}, I {I}, {dtype}, {T} tokens, top-{K} of {E} experts, "
+            f"Zipf({s}) popularity, Gaussian logits sigma {SIGMA}, plan {plan or plans[0]}")

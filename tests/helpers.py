@@ -1,0 +1,79 @@
+"""Test helpers: turn a synthetic workload into device tensors for the HIP
+library and numpy arrays for the oracle.  The same generator output feeds
+both sides; nothing the HIP path produces is ever fed to the oracle."""
+from __future__ import annotations
+
+import numpy as np
+
+from paper_2608_13057_amd import synth
+
+
+def to_dev(a: np.ndarray, device="cuda"):
+    import torch
+
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        a = a.view(np.int16)
+    if a.dtype == np.uint32:
+        a = a.view(np.int32)
+    return torch.from_numpy(a).to(device)
+
+
+def to_host(t) -> np.ndarray:
+    a = t.detach().cpu().numpy()
+    if a.dtype == np.int16:
+        a = a.view(np.uint16)
+    return a
+
+
+def bf16_to_f64(bits: np.ndarray) -> np.ndarray:
+    return synth.bf16_bits_to_f32(bits.astype(np.uint16)).astype(np.float64)
+
+
+class Case:
+    """Everything one forward needs, on host (numpy) and device (torch)."""
+
+    def __init__(self, wl: synth.Workload, plan_name: str, m_tile: int = 128, weights=True, device="cuda",
+                 T_valid=None):
+        from paper_2608_13057_amd import moe
+
+        self.wl = wl
+        self.plan = wl.plans[plan_name]
+        self.dtype = wl.dtype
+        self.m_tile = m_tile
+        self.T_valid = wl.T_valid if T_valid is None else T_valid
+        self.shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=m_tile, dtype=wl.dtype,
+                                  T_valid=self.T_valid)
+        self.x, self.xs = synth.activations(wl.T, wl.H, wl.seed, wl.dtype)
+        if weights:
+            self.w13, self.s13, self.w2, self.s2 = synth.slot_weights(wl.placement.slot_expert, wl.H, wl.I, wl.seed,
+                                                                      wl.dtype)
+        self.dev = device
+        self.d_ids = to_dev(wl.topk_ids, device)
+        self.d_w = to_dev(wl.topk_w, device)
+        self.d_x = to_dev(self.x, device)
+        self.d_xs = None if self.xs is None else to_dev(self.xs, device)
+        self.d_plan = moe.PlanTensors(to_dev(wl.placement.slot_expert, device), to_dev(self.plan.slot_weight, device),
+                                      to_dev(self.plan.remote_weight, device),
+                                      to_dev(self.plan.remote_replicas, device))
+        if weights:
+            self.d_weights = moe.WeightTensors(to_dev(self.w13, device), to_dev(self.w2, device),
+                                               None if self.s13 is None else to_dev(self.s13, device),
+                                               None if self.s2 is None else to_dev(self.s2, device))
+        self.ws = moe.Workspace(self.shape, device)
+        self.disp = moe.DispatchBuffers.allocate(self.shape, self.ws.row_cap, device)
+
+    def oracle_dispatch(self):
+        import oracle
+
+        return oracle.dispatch(self.wl.topk_ids, self.T_valid, self.wl.E, self.m_tile, self.wl.placement.slot_expert,
+                               self.plan.slot_weight, self.plan.remote_weight, self.plan.remote_replicas)
+
+
+def rel_err_rows(y: np.ndarray, ref: np.ndarray, rows: np.ndarray) -> float:
+    """max over the given rows of ||y_t - r_t||_inf / ||r_t||_inf."""
+    if len(rows) == 0:
+        return 0.0
+    d = np.abs(y[rows] - ref[rows]).max(axis=1)
+    n = np.abs(ref[rows]).max(axis=1)
+    return float(np.max(d / np.maximum(n, 1e-30)))
