@@ -137,11 +137,14 @@ typedef struct tempo_dispatch_out {
 
 /*
  * Expert weights of the S local slots (device pointers).  A replica slot
- * holds its own copy of its expert's weights.
+ * holds its own copy of its expert's weights.  In the natural layout:
  *   w13       [S, 2I, H]  rows 0..I-1 gate projection, rows I..2I-1 up projection
  *   w13_scale [S, 2I/128, H/128] fp32, fp8 only
  *   w2        [S, H, I]   down projection
  *   w2_scale  [S, H/128, I/128] fp32, fp8 only
+ * tempo_moe_experts / tempo_moe_forward take w13 and w2 in the packed layout
+ * written by tempo_moe_pack_weights (same sizes; the scales keep the natural
+ * layout).
  */
 typedef struct tempo_expert_weights {
   const void* w13;
@@ -159,6 +162,21 @@ typedef struct tempo_expert_weights {
  * rejects.  Either output pointer may be NULL.
  */
 int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap);
+
+/*
+ * One-time re-layout of expert weights for the stage-2 kernels (not part of
+ * the per-batch path; run it when weights are loaded).  natural holds w13 /
+ * w2 in the natural layout above; packed->w13 / packed->w2 are caller
+ * buffers of the same byte sizes that receive the packed layout, in which
+ * every (output block of 128 weight rows, contraction step of 128 bytes)
+ * tile of a slot is one contiguous 16 KB block and the tiles of an output
+ * block follow each other along the contraction, so stage 2 streams each
+ * activated slot's weights front to back.  For w13 an output block holds 64
+ * gate rows and the same 64 up rows.  Scale pointers are ignored.  Returns
+ * TEMPO_EINVAL for null or aliasing buffers.
+ */
+int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weights* natural,
+                           const tempo_expert_weights* packed, void* stream);
 
 /*
  * Stage 1 (Sec. 4.4 fused count collection + dispatch, Sec. 2.2 / Eq. 2

@@ -21,7 +21,7 @@ TEMPO_DERR_WEIGHT_OVERFLOW = 4
 TEMPO_BF16 = 0
 TEMPO_FP8_E4M3 = 1
 
-SYMBOLS = ("tempo_moe_query", "tempo_moe_dispatch", "tempo_moe_experts", "tempo_moe_combine",
+SYMBOLS = ("tempo_moe_query", "tempo_moe_pack_weights", "tempo_moe_dispatch", "tempo_moe_experts", "tempo_moe_combine",
            "tempo_moe_forward", "tempo_moe_device_error", "tempo_moe_strerror")
 
 _P = ctypes.c_void_p
@@ -62,6 +62,7 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     SP = ctypes.POINTER(Shape)
     lib.tempo_moe_query.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_int32)]
+    lib.tempo_moe_pack_weights.argtypes = [SP, ctypes.POINTER(ExpertWeights), ctypes.POINTER(ExpertWeights), _P]
     lib.tempo_moe_dispatch.argtypes = [SP, ctypes.POINTER(Plan), _P, _P, _P, ctypes.POINTER(DispatchOut), _P,
                                        ctypes.c_size_t, _P]
     lib.tempo_moe_experts.argtypes = [SP, ctypes.POINTER(DispatchOut), ctypes.POINTER(ExpertWeights), _P, _P,

@@ -44,17 +44,17 @@ Layout make_layout(const tempo_moe_shape& s) {
   return L;
 }
 
-int persistent_grid() {
+int persistent_grid(int per_cu) {
   static std::atomic<int> cached{0};
-  int g = cached.load();
-  if (g > 0) return g;
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    cus = 256;
-  g = ((cus * 2 + 7) / 8) * 8;
-  cached.store(g);
-  return g;
+  int cus = cached.load();
+  if (cus <= 0) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    cached.store(cus);
+  }
+  return ((cus * per_cu + 7) / 8) * 8;  // a multiple of the 8 XCDs
 }
 
 static int check_shape(const tempo_moe_shape* s) {
@@ -107,6 +107,24 @@ int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32
   if (workspace_bytes) *workspace_bytes = L.total;
   if (row_cap) *row_cap = L.row_cap;
   return TEMPO_OK;
+}
+
+int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weights* natural,
+                           const tempo_expert_weights* packed, void* stream) {
+  int rc = check_shape(shape);
+  if (rc) return rc;
+  if (!natural || !packed || !natural->w13 || !natural->w2 || !packed->w13 || !packed->w2) return TEMPO_EINVAL;
+  const size_t es = shape->dtype == TEMPO_BF16 ? 2 : 1;
+  const size_t b13 = (size_t)shape->S * 2 * shape->I * shape->H * es, b2 = (size_t)shape->S * shape->H * shape->I * es;
+  auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
+    const char *x = static_cast<const char*>(a), *y = static_cast<const char*>(b);
+    return x < y + nb && y < x + na;
+  };
+  if (overlap(natural->w13, b13, packed->w13, b13) || overlap(natural->w2, b2, packed->w2, b2) ||
+      overlap(natural->w13, b13, packed->w2, b2) || overlap(natural->w2, b2, packed->w13, b13) ||
+      overlap(packed->w13, b13, packed->w2, b2))
+    return TEMPO_EINVAL;
+  return dev_status(launch_pack(*shape, *natural, *packed, static_cast<hipStream_t>(stream)));
 }
 
 int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids, const void* x,

@@ -4,7 +4,7 @@
 //   y[t] = sum_{k ascending, pair_row[t,k] >= 0} topk_w[t,k] * y_perm[pair_row[t,k]]
 // fp32 accumulation, one bf16 rounding at the end; rows t >= T_valid and rows
 // without a local pair are zero.  One wavefront per token row, 16-byte loads
-// and stores (8 bf16 per lane), HBM-bound.
+// and stores (8 bf16 per lane), up to 8 loads per lane in flight; HBM-bound.
 #include "internal.h"
 
 namespace tempo {
@@ -30,36 +30,60 @@ __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int 
     for (int s = threadIdx.x; s < S; s += 256)
       slot_time_ns[s] = slot_counts[s] > 0 ? (t1[s] - t0[s]) * 10ull : 0ull;  // 100 MHz counter
   if (t >= T) return;
-  // the token's K rows and weights, staged per wavefront (every lane of the
-  // wavefront reads all K of them below, also lanes that own no column)
-  if (lane < K) {
-    const bool ok = t < T_valid;
-    s_row[wv][lane] = ok ? pair_row[(size_t)t * K + lane] : -1;
-    s_w[wv][lane] = ok ? topk_w[(size_t)t * K + lane] : 0.f;
+  // the token's local pairs in ascending k, compacted per wavefront (every
+  // lane reads all of them below, also lanes that own no column)
+  int row = -1;
+  float wt = 0.f;
+  if (lane < K && t < T_valid) {
+    row = pair_row[(size_t)t * K + lane];
+    wt = topk_w[(size_t)t * K + lane];
+  }
+  const uint64_t m = __ballot(row >= 0);
+  const int nv = __popcll(m);
+  if (row >= 0) {
+    const int pos = __popcll(m & ((1ull << lane) - 1ull));
+    s_row[wv][pos] = row;
+    s_w[wv][pos] = wt;
   }
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront");
   uint4* __restrict__ yo = reinterpret_cast<uint4*>(y + (size_t)t * H);
-  for (int c = lane; c < H / 8; c += 64) {
-    float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    for (int k = 0; k < K; k++) {
-      const int r = s_row[wv][k];
-      const float wk = s_w[wv][k];
-      if (r < 0) continue;
-      const uint4 v = *reinterpret_cast<const uint4*>(y_perm + (size_t)r * H + c * 8);
-      const uint32_t u[4] = {v.x, v.y, v.z, v.w};
+  const int nch = H / 8;
+  constexpr int U = 8;  // 16-byte chunks per lane in flight
+  for (int c0 = lane; c0 < nch; c0 += 64 * U) {
+    float acc[U][8];
 #pragma unroll
-      for (int q = 0; q < 4; q++) {
-        acc[2 * q] += wk * __uint_as_float(u[q] << 16);
-        acc[2 * q + 1] += wk * __uint_as_float(u[q] & 0xFFFF0000u);
+    for (int u = 0; u < U; u++)
+#pragma unroll
+      for (int q = 0; q < 8; q++) acc[u][q] = 0.f;
+    for (int j = 0; j < nv; j++) {
+      const int r = s_row[wv][j];
+      const float wk = s_w[wv][j];
+      const uint4* __restrict__ src = reinterpret_cast<const uint4*>(y_perm + (size_t)r * H);
+      uint4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; u++)
+        if (c0 + u * 64 < nch) v[u] = src[c0 + u * 64];
+#pragma unroll
+      for (int u = 0; u < U; u++) {
+        const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+          acc[u][2 * q] += wk * __uint_as_float(w4[q] << 16);
+          acc[u][2 * q + 1] += wk * __uint_as_float(w4[q] & 0xFFFF0000u);
+        }
       }
     }
-    uint4 o;
-    o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
-    o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
-    o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
-    o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
-    yo[c] = o;
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+      if (c0 + u * 64 >= nch) continue;
+      uint4 o;
+      o.x = (uint32_t)f32_to_bf16_rne(acc[u][0]) | ((uint32_t)f32_to_bf16_rne(acc[u][1]) << 16);
+      o.y = (uint32_t)f32_to_bf16_rne(acc[u][2]) | ((uint32_t)f32_to_bf16_rne(acc[u][3]) << 16);
+      o.z = (uint32_t)f32_to_bf16_rne(acc[u][4]) | ((uint32_t)f32_to_bf16_rne(acc[u][5]) << 16);
+      o.w = (uint32_t)f32_to_bf16_rne(acc[u][6]) | ((uint32_t)f32_to_bf16_rne(acc[u][7]) << 16);
+      yo[c0 + u * 64] = o;
+    }
   }
 }
 

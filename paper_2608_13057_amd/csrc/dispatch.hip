@@ -12,32 +12,278 @@
 // split is the deterministic integer reading documented in the header, so
 // the outputs are reproducible bit for bit.
 //
-// Three launches, none of which needs zeroed memory:
-//   k_count   -- blocks of 1024 pairs: per-block histogram in LDS and the
-//                stable rank of each pair within (block, expert), from wave
-//                ballots (lanes of one wave with equal expert ids are found
-//                with one ballot per id bit; ranks = popcount of the lower
-//                lanes), plus per-wave counts for the waves before it.
-//   k_plan    -- one block: per-expert exclusive scan of the block counts,
-//                n_e, the plan split of each expert over its slots, padded
-//                sizes, slot offsets, the tile count, padding-row markers.
-//   k_scatter -- blocks of 32 pairs: rank -> slot -> row, index outputs, and
-//                the copy of the activation row (16-byte loads/stores, one
-//                wavefront per row).
+// Ranks.  The rank of a pair within its expert is the number of valid pairs
+// of the same expert with a smaller index p = t*K + k.  Pairs are processed
+// in rounds of one pair per thread; within a wavefront, lanes holding the same
+// expert are found with one ballot per bit of the expert id and the lane's
+// rank is the popcount of those lanes below it; per-wavefront counts in LDS
+// give the offset of earlier wavefronts and a running count the offset of
+// earlier rounds.  No atomics decide positions.
+//
+// Two paths, both free of zero-initialised memory:
+//   small batches (T*K <= 16384): k_dispatch_small -- one 1024-thread block
+//     ranks every pair into LDS, splits, scans and writes every index output;
+//     then k_gather copies the activation rows, one wavefront per pair.
+//   large batches: k_count (blocks of 1024 pairs, per-block histograms and
+//     in-block ranks) -> k_plan (one block: per-expert scan over blocks, split,
+//     offsets) -> k_scatter (index outputs) -> k_gather.
 #include "internal.h"
 
 namespace tempo {
 namespace {
 
+constexpr int kSmallMaxPairs = 16384;
+
+// ---------------------------------------------------------------------------
+// shared pieces
+// ---------------------------------------------------------------------------
+
+// Rank one round of pairs (one per thread) within (expert); wc is
+// [NW][E] of zeros on entry and is zero again on exit; run [E] holds the
+// counts of earlier rounds and is advanced.  Returns the rank (or -1).
+template <int NW>
+__device__ __forceinline__ int rank_round(int e, int E, int ebits, int32_t* run, int32_t* wc) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  uint64_t peers = __ballot(e >= 0);
+  for (int b = 0; b < ebits; b++) {
+    const int bit = (e >> b) & 1;
+    const uint64_t m = __ballot(e >= 0 && bit);
+    peers &= bit ? m : ~m;
+  }
+  int rank_w = 0;
+  if (e >= 0) {
+    rank_w = __popcll(peers & ((1ull << lane) - 1ull));
+    if (rank_w == 0) wc[w * E + e] = __popcll(peers);
+  }
+  __syncthreads();
+  int rk = -1;
+  if (e >= 0) {
+    rk = run[e] + rank_w;
+    for (int w2 = 0; w2 < w; w2++) rk += wc[w2 * E + e];
+  }
+  __syncthreads();
+  for (int x = tid; x < E; x += NW * 64) {
+    int s = 0;
+#pragma unroll
+    for (int w2 = 0; w2 < NW; w2++) {
+      s += wc[w2 * E + x];
+      wc[w2 * E + x] = 0;
+    }
+    run[x] += s;
+  }
+  __syncthreads();
+  return rk;
+}
+
+// Exclusive scan of v over the block (blockDim = 64 * NW <= 1024); one value
+// per thread.  Returns the thread's exclusive prefix; *total gets the sum.
+template <int NW>
+__device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp, int* total) {
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int x = v;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(x, d);
+    if (lane >= d) x += y;
+  }
+  if (lane == 63) s_tmp[w] = x;
+  __syncthreads();
+  if (w == 0) {
+    int t = lane < NW ? s_tmp[lane] : 0;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int y = __shfl_up(t, d);
+      if (lane >= d) t += y;
+    }
+    if (lane < NW) s_tmp[32 + lane] = t;  // inclusive wave totals
+  }
+  __syncthreads();
+  const int before = (w == 0 ? 0 : s_tmp[32 + w - 1]);
+  *total = s_tmp[32 + NW - 1];
+  __syncthreads();
+  return before + x - v;
+}
+
+// Slot tables in LDS (filled by plan_slots).
+struct SlotLds {
+  int32_t se[kMaxS];   // expert of slot
+  int32_t lo[kMaxS];   // first rank (within the expert) taken by the slot
+  int32_t c[kMaxS];    // c_s
+  int32_t off[kMaxS + 1];
+};
+
+// Plan split, padded sizes, offsets, padding-row markers and header.  n_e is
+// read from n (LDS or global); runs on one block of NW wavefronts.
+template <int NW>
+__device__ void plan_slots(const int32_t* n, int E, int S, int M, uint32_t err_in, const int32_t* __restrict__ slot_expert,
+                           const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
+                           const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ slot_counts,
+                           int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
+                           int32_t* __restrict__ slot_lo_out, uint32_t* __restrict__ hdr, SlotLds& L, uint32_t* s_err,
+                           uint32_t* s_w, int* s_tmp, int timing, uint64_t* __restrict__ t0,
+                           uint64_t* __restrict__ t1) {
+  const int tid = threadIdx.x, bd = NW * 64;
+  for (int s = tid; s < S; s += bd) {
+    L.se[s] = slot_expert[s];
+    s_w[s] = slot_weight[s];
+  }
+  __syncthreads();
+  int c = 0, P = 0;
+  if (tid < S) {
+    const int s = tid, e = L.se[s];
+    int lo = 0;
+    if (e < 0 || e >= E) {
+      atomicOr(s_err, TEMPO_DERR_BAD_SLOT_EXPERT);
+    } else {
+      uint64_t W = 0, before = 0;
+      int nloc = 0, nloc_before = 0;
+      for (int s2 = 0; s2 < S; s2++)
+        if (L.se[s2] == e) {
+          W += s_w[s2];
+          nloc++;
+          if (s2 < s) {
+            before += s_w[s2];
+            nloc_before++;
+          }
+        }
+      const int rr = remote_replicas[e];
+      const uint32_t rw = remote_weight[e];
+      const bool has_remote = rw > 0u || rr > 0;
+      if (has_remote) W += rw;
+      uint64_t mine = s_w[s];
+      bool uniform = (W == 0);
+      if (W >= (1ull << 32)) {
+        uniform = true;
+        atomicOr(s_err, TEMPO_DERR_WEIGHT_OVERFLOW);
+      }
+      if (uniform) {
+        W = (uint64_t)nloc + (has_remote && rr > 0 ? (uint64_t)rr : 0ull);
+        before = (uint64_t)nloc_before;
+        mine = 1;
+      }
+      const uint64_t ne = (uint64_t)n[e];
+      const uint64_t blo = ne * before / W, bhi = ne * (before + mine) / W;
+      lo = (int)blo;
+      c = (int)(bhi - blo);
+    }
+    L.c[s] = c;
+    L.lo[s] = lo;
+    slot_counts[s] = c;
+    if (slot_lo_out) slot_lo_out[s] = lo;
+    P = (c + M - 1) / M * M;
+  }
+  int total = 0;
+  const int off = block_exclusive_scan<NW>(P, s_tmp, &total);
+  if (tid < S) L.off[tid] = off;
+  if (tid == 0) L.off[S] = total;
+  // tiles, G, N
+  const int tiles = block_exclusive_scan<NW>(P / M, s_tmp, &total), ntiles = total;
+  (void)tiles;
+  block_exclusive_scan<NW>(c > 0 ? 1 : 0, s_tmp, &total);
+  const int G = total;
+  block_exclusive_scan<NW>(c, s_tmp, &total);
+  const int N = total;
+  if (tid == 0) {
+    hdr[kHdrTiles] = (uint32_t)ntiles;
+    hdr[kHdrActive] = (uint32_t)G;
+    hdr[kHdrPairs] = (uint32_t)N;
+    const uint32_t e = err_in | *s_err;
+    hdr[kHdrLastErr] = e;
+    hdr[kHdrSticky] = hdr[kHdrSticky] | e;
+  }
+  __syncthreads();
+  for (int s = tid; s <= S; s += bd) slot_offsets[s] = L.off[s];
+  // padding rows of every slot
+  for (int s = 0; s < S; s++) {
+    const int cs = L.c[s], Ps = L.off[s + 1] - L.off[s];
+    for (int r = cs + tid; r < Ps; r += bd) row_token[L.off[s] + r] = -1;
+  }
+  if (timing)
+    for (int s = tid; s < S; s += bd) {
+      t0[s] = ~0ull;
+      t1[s] = 0ull;
+    }
+}
+
+// Row of pair p with expert e and rank r (or -1 when the rank falls on the
+// remote share).
+__device__ __forceinline__ int row_of(const SlotLds& L, int S, int e, int r) {
+  for (int s = 0; s < S; s++)
+    if (L.se[s] == e && r >= L.lo[s] && r < L.lo[s] + L.c[s]) return L.off[s] + (r - L.lo[s]);
+  return -1;
+}
+
+// ---------------------------------------------------------------------------
+// small batches: everything but the row copy in one block
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(1024) void k_dispatch_small(const int32_t* __restrict__ ids, int P, int Pv, int K, int E,
+                                                         int ebits, int S, int M, const int32_t* __restrict__ slot_expert,
+                                                         const uint32_t* __restrict__ slot_weight,
+                                                         const uint32_t* __restrict__ remote_weight,
+                                                         const int32_t* __restrict__ remote_replicas,
+                                                         int32_t* __restrict__ expert_counts,
+                                                         uint32_t* __restrict__ cum_counts,
+                                                         int32_t* __restrict__ slot_counts,
+                                                         int32_t* __restrict__ slot_offsets,
+                                                         int32_t* __restrict__ row_token, int32_t* __restrict__ pair_row,
+                                                         uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0,
+                                                         uint64_t* __restrict__ t1) {
+  constexpr int NW = 16;
+  extern __shared__ int32_t dyn[];  // run[E], wc[NW][E], rank[P]
+  int32_t* run = dyn;
+  int32_t* wc = dyn + E;
+  int32_t* rank = dyn + E + NW * E;
+  __shared__ SlotLds L;
+  __shared__ uint32_t s_w[kMaxS];
+  __shared__ int s_tmp[64];
+  __shared__ uint32_t s_err;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < (NW + 1) * E; i += 1024) dyn[i] = 0;
+  if (tid == 0) s_err = 0;
+  __syncthreads();
+  int bad = 0;
+  for (int base = 0; base < P; base += 1024) {
+    const int p = base + tid;
+    int e = -1;
+    if (p < Pv) {
+      const int id = ids[p];
+      if (id >= 0 && id < E) e = id;
+      else if (id != -1) bad = 1;
+    }
+    const int rk = rank_round<NW>(e, E, ebits, run, wc);
+    if (p < P) rank[p] = e >= 0 ? rk : -1;
+  }
+  if (__syncthreads_or(bad) && tid == 0) s_err = TEMPO_DERR_BAD_ID;
+  for (int e = tid; e < E; e += 1024) {
+    expert_counts[e] = run[e];
+    if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)run[e];
+  }
+  __syncthreads();
+  plan_slots<NW>(run, E, S, M, 0u, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
+                 row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+  for (int p = tid; p < P; p += 1024) {
+    int row = -1;
+    if (rank[p] >= 0) row = row_of(L, S, ids[p], rank[p]);
+    pair_row[p] = row;
+    if (row >= 0) row_token[row] = p / K;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// large batches
+// ---------------------------------------------------------------------------
+
 __global__ __launch_bounds__(kCountThreads) void k_count(const int32_t* __restrict__ ids, int Pv, int E, int ebits,
                                                           int32_t* __restrict__ blk_hist,
                                                           uint32_t* __restrict__ blk_err,
                                                           int32_t* __restrict__ local_rank) {
-  extern __shared__ int32_t sm[];  // run[E] then wc[4][E]
+  constexpr int NW = kCountThreads / 64;
+  extern __shared__ int32_t sm[];  // run[E] then wc[NW][E]
   int32_t* run = sm;
   int32_t* wc = sm + E;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  for (int i = tid; i < 5 * E; i += kCountThreads) sm[i] = 0;
+  const int tid = threadIdx.x;
+  for (int i = tid; i < (NW + 1) * E; i += kCountThreads) sm[i] = 0;
   __syncthreads();
   int bad = 0;
   const int base = blockIdx.x * kCountChunk;
@@ -49,35 +295,8 @@ __global__ __launch_bounds__(kCountThreads) void k_count(const int32_t* __restri
       if (id >= 0 && id < E) e = id;
       else if (id != -1) bad = 1;
     }
-    // lanes of this wavefront that carry the same expert id
-    uint64_t peers = __ballot(e >= 0);
-    for (int b = 0; b < ebits; b++) {
-      const int bit = (e >> b) & 1;
-      const uint64_t m = __ballot(e >= 0 && bit);
-      peers &= bit ? m : ~m;
-    }
-    int rank_w = 0;
-    if (e >= 0) {
-      rank_w = __popcll(peers & ((1ull << lane) - 1ull));
-      if (rank_w == 0) wc[w * E + e] = __popcll(peers);
-    }
-    __syncthreads();
-    if (e >= 0) {
-      int rk = run[e] + rank_w;
-      for (int w2 = 0; w2 < w; w2++) rk += wc[w2 * E + e];
-      local_rank[p] = rk;
-    }
-    __syncthreads();
-    for (int x = tid; x < E; x += kCountThreads) {
-      int s = 0;
-#pragma unroll
-      for (int w2 = 0; w2 < kCountThreads / 64; w2++) {
-        s += wc[w2 * E + x];
-        wc[w2 * E + x] = 0;
-      }
-      run[x] += s;
-    }
-    __syncthreads();
+    const int rk = rank_round<NW>(e, E, ebits, run, wc);
+    if (e >= 0) local_rank[p] = rk;
   }
   for (int x = tid; x < E; x += kCountThreads) blk_hist[(size_t)blockIdx.x * E + x] = run[x];
   const int any_bad = __syncthreads_or(bad);
@@ -95,20 +314,34 @@ __global__ __launch_bounds__(1024) void k_plan(int nblk, int E, int S, int M, in
                                                int32_t* __restrict__ row_token, int32_t* __restrict__ slot_lo,
                                                uint64_t* __restrict__ t0, uint64_t* __restrict__ t1,
                                                uint32_t* __restrict__ hdr) {
+  constexpr int NW = 16;
   __shared__ int32_t s_n[kMaxE];
-  __shared__ int32_t s_c[kMaxS];
-  __shared__ int32_t s_off[kMaxS + 1];
+  __shared__ SlotLds L;
+  __shared__ uint32_t s_w[kMaxS];
+  __shared__ int s_tmp[64];
   __shared__ uint32_t s_err;
-  const int tid = threadIdx.x, bd = blockDim.x;
+  const int tid = threadIdx.x;
   if (tid == 0) s_err = 0;
   __syncthreads();
   uint32_t eb = 0;
-  for (int b = tid; b < nblk; b += bd) eb |= blk_err[b];
+  for (int b = tid; b < nblk; b += 1024) eb |= blk_err[b];
   if (eb) atomicOr(&s_err, eb);
-  // n_e and the exclusive prefix of the block counts, in place
-  for (int e = tid; e < E; e += bd) {
+  // n_e and the exclusive prefix of the block counts, in place; the loads of
+  // one expert's column are independent and issued back to back
+  for (int e = tid; e < E; e += 1024) {
     int acc = 0;
-    for (int b = 0; b < nblk; b++) {
+    int b = 0;
+    for (; b + 8 <= nblk; b += 8) {
+      int v[8];
+#pragma unroll
+      for (int u = 0; u < 8; u++) v[u] = blk_hist[(size_t)(b + u) * E + e];
+#pragma unroll
+      for (int u = 0; u < 8; u++) {
+        blk_hist[(size_t)(b + u) * E + e] = acc;
+        acc += v[u];
+      }
+    }
+    for (; b < nblk; b++) {
       const size_t i = (size_t)b * E + e;
       const int v = blk_hist[i];
       blk_hist[i] = acc;
@@ -119,143 +352,68 @@ __global__ __launch_bounds__(1024) void k_plan(int nblk, int E, int S, int M, in
     if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)acc;
   }
   __syncthreads();
-  // plan split: slot s is entry j of its expert; its ranks are
-  // [floor(n C_{j-1} / W), floor(n C_j / W))
-  for (int s = tid; s < S; s += bd) {
-    const int e = slot_expert[s];
-    int c = 0, lo = 0;
-    if (e < 0 || e >= E) {
-      atomicOr(&s_err, TEMPO_DERR_BAD_SLOT_EXPERT);
-    } else {
-      uint64_t W = 0, before = 0;
-      int nloc = 0, nloc_before = 0;
-      for (int s2 = 0; s2 < S; s2++)
-        if (slot_expert[s2] == e) {
-          W += slot_weight[s2];
-          nloc++;
-          if (s2 < s) {
-            before += slot_weight[s2];
-            nloc_before++;
-          }
-        }
-      const int rr = remote_replicas[e];
-      const bool has_remote = remote_weight[e] > 0u || rr > 0;
-      if (has_remote) W += remote_weight[e];
-      uint64_t mine = slot_weight[s];
-      bool uniform = (W == 0);
-      if (W >= (1ull << 32)) {
-        uniform = true;
-        atomicOr(&s_err, TEMPO_DERR_WEIGHT_OVERFLOW);
-      }
-      if (uniform) {
-        W = (uint64_t)nloc + (has_remote && rr > 0 ? (uint64_t)rr : 0ull);
-        before = (uint64_t)nloc_before;
-        mine = 1;
-      }
-      const uint64_t n = (uint64_t)s_n[e];
-      const uint64_t blo = n * before / W, bhi = n * (before + mine) / W;
-      lo = (int)blo;
-      c = (int)(bhi - blo);
-    }
-    s_c[s] = c;
-    slot_lo[s] = lo;
-    slot_counts[s] = c;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int off = 0, tiles = 0, G = 0, N = 0;
-    for (int s = 0; s < S; s++) {
-      s_off[s] = off;
-      const int P = (s_c[s] + M - 1) / M * M;
-      off += P;
-      tiles += P / M;
-      G += s_c[s] > 0;
-      N += s_c[s];
-    }
-    s_off[S] = off;
-    hdr[kHdrTiles] = (uint32_t)tiles;
-    hdr[kHdrActive] = (uint32_t)G;
-    hdr[kHdrPairs] = (uint32_t)N;
-    hdr[kHdrLastErr] = s_err;
-    hdr[kHdrSticky] = hdr[kHdrSticky] | s_err;
-  }
-  __syncthreads();
-  for (int s = tid; s <= S; s += bd) slot_offsets[s] = s_off[s];
-  for (int s = 0; s < S; s++) {
-    const int c = s_c[s], P = s_off[s + 1] - s_off[s];
-    for (int r = c + tid; r < P; r += bd) row_token[s_off[s] + r] = -1;
-  }
-  if (timing)
-    for (int s = tid; s < S; s += bd) {
-      t0[s] = ~0ull;
-      t1[s] = 0ull;
-    }
+  plan_slots<NW>(s_n, E, S, M, 0u, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
+                 row_token, slot_lo, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
 }
 
-template <int ESIZE>
 __global__ __launch_bounds__(256) void k_scatter(const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S,
-                                                 int H, const int32_t* __restrict__ blk_prefix,
+                                                 const int32_t* __restrict__ blk_prefix,
                                                  const int32_t* __restrict__ local_rank,
                                                  const int32_t* __restrict__ slot_expert,
                                                  const int32_t* __restrict__ slot_lo,
                                                  const int32_t* __restrict__ slot_counts,
                                                  const int32_t* __restrict__ slot_offsets,
-                                                 const uint8_t* __restrict__ x, const float* __restrict__ x_scale,
-                                                 int32_t* __restrict__ pair_row, int32_t* __restrict__ row_token,
-                                                 uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale) {
-  __shared__ int32_t s_se[kMaxS], s_lo[kMaxS], s_c[kMaxS], s_off[kMaxS];
-  __shared__ int32_t s_row[kScatterPairs], s_tok[kScatterPairs];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+                                                 int32_t* __restrict__ pair_row, int32_t* __restrict__ row_token) {
+  __shared__ SlotLds L;
+  const int tid = threadIdx.x;
   for (int s = tid; s < S; s += 256) {
-    s_se[s] = slot_expert[s];
-    s_lo[s] = slot_lo[s];
-    s_c[s] = slot_counts[s];
-    s_off[s] = slot_offsets[s];
+    L.se[s] = slot_expert[s];
+    L.lo[s] = slot_lo[s];
+    L.c[s] = slot_counts[s];
+    L.off[s] = slot_offsets[s];
   }
   __syncthreads();
-  if (tid < kScatterPairs) {
-    const int p = blockIdx.x * kScatterPairs + tid;
-    int row = -1;
-    if (p < P) {
-      if (p < Pv) {
-        const int e = ids[p];
-        if (e >= 0 && e < E) {
-          const int r = blk_prefix[(size_t)(p / kCountChunk) * E + e] + local_rank[p];
-          for (int s = 0; s < S; s++)
-            if (s_se[s] == e && r >= s_lo[s] && r < s_lo[s] + s_c[s]) {
-              row = s_off[s] + (r - s_lo[s]);
-              break;
-            }
-        }
-      }
-      pair_row[p] = row;
-      if (row >= 0) row_token[row] = p / K;
-    }
-    s_row[tid] = row;
-    s_tok[tid] = p / K;
+  const int p = blockIdx.x * 256 + tid;
+  if (p >= P) return;
+  int row = -1;
+  if (p < Pv) {
+    const int e = ids[p];
+    if (e >= 0 && e < E) row = row_of(L, S, e, blk_prefix[(size_t)(p / kCountChunk) * E + e] + local_rank[p]);
   }
-  __syncthreads();
-  // copy the activation rows: one wavefront per placed pair
+  pair_row[p] = row;
+  if (row >= 0) row_token[row] = p / K;
+}
+
+// ---------------------------------------------------------------------------
+// row copy: one wavefront per pair
+// ---------------------------------------------------------------------------
+
+template <int ESIZE>
+__global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair_row, int P, int K, int H,
+                                                const uint8_t* __restrict__ x, const float* __restrict__ x_scale,
+                                                uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale) {
+  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (p >= P) return;
+  const int row = pair_row[p];
+  if (row < 0) return;
+  const int t = p / K;
   const int nch = H * ESIZE / 16;
-  for (int j = w; j < kScatterPairs; j += 4) {
-    const int row = s_row[j];
-    if (row < 0) continue;
-    const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x + (size_t)s_tok[j] * H * ESIZE);
-    uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm + (size_t)row * H * ESIZE);
-    constexpr int U = 8;
-    for (int i0 = lane; i0 < nch; i0 += 64 * U) {
-      uint4 v[U];
+  const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x + (size_t)t * H * ESIZE);
+  uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm + (size_t)row * H * ESIZE);
+  constexpr int U = 8;
+  for (int i0 = lane; i0 < nch; i0 += 64 * U) {
+    uint4 v[U];
 #pragma unroll
-      for (int u = 0; u < U; u++)
-        if (i0 + u * 64 < nch) v[u] = src[i0 + u * 64];
+    for (int u = 0; u < U; u++)
+      if (i0 + u * 64 < nch) v[u] = src[i0 + u * 64];
 #pragma unroll
-      for (int u = 0; u < U; u++)
-        if (i0 + u * 64 < nch) dst[i0 + u * 64] = v[u];
-    }
-    if (ESIZE == 1) {
-      const int ns = H / 128;
-      for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)row * ns + i] = x_scale[(size_t)s_tok[j] * ns + i];
-    }
+    for (int u = 0; u < U; u++)
+      if (i0 + u * 64 < nch) dst[i0 + u * 64] = v[u];
+  }
+  if (ESIZE == 1) {
+    const int ns = H / 128;
+    for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)row * ns + i] = x_scale[(size_t)t * ns + i];
   }
 }
 
@@ -275,23 +433,30 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
-  hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), 5 * s.E * sizeof(int32_t), st, topk_ids, Pv, s.E,
-                     ebits, blk_hist, blk_err, local_rank);
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, st, L.nblk, s.E, s.S, s.m_tile, timing ? 1 : 0, blk_hist,
-                     blk_err, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
-                     out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token, slot_lo,
-                     t0, t1, hdr);
-  const int nb = ceil_div(P, kScatterPairs);
+  const size_t small_lds = (size_t)(17 * s.E + P) * sizeof(int32_t);
+  if (P <= kSmallMaxPairs && small_lds <= 120 * 1024) {
+    hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(1024), small_lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
+                       s.m_tile, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
+                       out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
+                       out.pair_row, hdr, timing ? 1 : 0, t0, t1);
+  } else {
+    hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t),
+                       st, topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);
+    hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, st, L.nblk, s.E, s.S, s.m_tile, timing ? 1 : 0, blk_hist,
+                       blk_err, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
+                       out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token, slot_lo,
+                       t0, t1, hdr);
+    hipLaunchKernelGGL(k_scatter, dim3(ceil_div(P, 256)), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, blk_hist,
+                       local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets, out.pair_row,
+                       out.row_token);
+  }
+  const int nb = ceil_div(P, 4);
   if (s.dtype == TEMPO_BF16)
-    hipLaunchKernelGGL(k_scatter<2>, dim3(nb), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, s.H, blk_hist,
-                       local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets,
-                       static_cast<const uint8_t*>(x), x_scale, out.pair_row, out.row_token,
-                       static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+    hipLaunchKernelGGL(k_gather<2>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
+                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
   else
-    hipLaunchKernelGGL(k_scatter<1>, dim3(nb), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, s.H, blk_hist,
-                       local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets,
-                       static_cast<const uint8_t*>(x), x_scale, out.pair_row, out.row_token,
-                       static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+    hipLaunchKernelGGL(k_gather<1>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
+                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
   return hipGetLastError();
 }
 

@@ -4,29 +4,41 @@
 // (Sec. 2.1: "gate/up, activation, down"; Sec. 2.2: the cost of an activated
 // replica is streaming its weights, every extra M-tile re-uses them.)
 //
-// One persistent kernel per GEMM.  Work items are (M-tile, N-block) pairs; the
-// tile count and the slot of each tile come from the stage-1 results in device
-// memory (slot_offsets / slot_counts / header), so the launch needs no host
-// round trip and has a fixed grid.  Workgroup b runs on XCD b mod 8 (the
-// hardware's round-robin); each XCD owns a contiguous range of N-blocks, so
-// the weight block of an N-block is fetched into one XCD's L2 and shared by
-// every M-tile of the slot that runs there, and the activation tile is shared
-// by the XCD's N-blocks.
+// One persistent kernel per GEMM, one workgroup per CU.  Work items are
+// (M-tile, N-block) pairs; the tile count and the slot of each tile come from
+// the stage-1 results in device memory (slot_offsets / slot_counts / header),
+// so the launch has a fixed grid and needs no host round trip.  Workgroup b
+// runs on XCD b mod 8 (the dispatcher's round-robin); each XCD owns a
+// contiguous range of N-blocks, so an N-block of a slot's weights is fetched
+// into one XCD's L2 and shared by every M-tile of that slot running there.
 //
-// Tile: BM rows x 128 weight rows x 64 of the contraction per step, 256
-// threads as 2 x 2 wavefronts, each wavefront (BM/2) x 64 outputs with
-// v_mfma_f32_32x32x16_bf16 (lane layout verified on gfx950: A row / B column =
-// lane % 32, 8 consecutive k per lane; accumulator element i of lane l is
-// row 8*(i/4) + 4*(l/32) + i%4, column l % 32).  Operand tiles are staged
-// global -> registers -> LDS with two LDS buffers; LDS rows are padded by 16
-// bytes so the 16-byte fragment reads of 8 consecutive rows hit distinct banks.
-// Rows past a slot's real count are never loaded (zero-filled in LDS) nor
-// stored.  The gate/up instance puts gate columns n..n+63 and up columns
-// n..n+63 in one tile so that each lane holds matching g and u values and
-// SwiGLU runs in registers.
+// Weights arrive in the packed layout of tempo_moe_pack_weights: the 128-row
+// x K block of an item is contiguous, one 16 KB swizzled tile per step.
+//
+// Memory pipeline.  In the weight-streaming (flat) regime the kernel must keep
+// ~100 KB per CU in flight to run near HBM bandwidth, so operand tiles go
+// straight from global memory into an LDS ring with global_load_lds_dwordx4
+// (no registers involved): stage k+NS-1 is in flight while stage k is
+// multiplied.  A stage holds only the activation row groups that have real
+// rows plus the weight tile, so the ring depth NS adapts per item (4 stages
+// for a full 128-row tile, 8 for a decode-sized one).  Each wavefront waits only for its own loads of
+// the stage it is about to use (vmcnt), then a plain workgroup barrier makes
+// all wavefronts' data visible.  LDS rows are 128 bytes (64 bf16 of the
+// contraction); the 16-byte chunk c of row r is stored at chunk c ^ (r & 7),
+// so the MFMA fragment reads of 8 consecutive rows hit 8 distinct bank groups.
+// Activation rows past the slot's real count are not loaded (their LDS rows
+// hold stale values that only reach output rows which are never stored).
+//
+// Compute.  BM x 128 output tile (the gate/up instance holds 64 gate and the
+// matching 64 up columns), 2 x 2 wavefronts of (BM/2) x 64, 32x32x16 bf16
+// MFMA (lane layout verified on gfx950: A row / B column = lane % 32, 8
+// consecutive k per lane; accumulator element i of lane l is row
+// 8*(i/4) + 4*(l/32) + i%4, column l % 32).  SwiGLU and the bf16 rounding run
+// on the accumulators.
 //
 // Every output row is produced by the same instruction sequence (same K
-// order) wherever it lands, so results do not depend on the plan's split.
+// order) wherever it lands, so results do not depend on the plan's split or
+// on the M-tile.
 #include "internal.h"
 
 namespace tempo {
@@ -35,9 +47,11 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
-constexpr int BK = 64;
-constexpr int BNW = 128;      // weight rows per tile
-constexpr int LDS_ROW = BK + 8;  // bf16 elements per padded LDS row
+constexpr int BK = 64;           // contraction elements per stage
+constexpr int ROWB = BK * 2;     // bytes per LDS row
+constexpr int BNW = 128;         // weight rows per tile
+constexpr int RING_BYTES = 144 * 1024;  // LDS ring shared by the pipeline stages
+constexpr int NS_MAX = 8;
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -45,23 +59,77 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt[3:0] bits 3:0, vmcnt[5:4] bits 15:14, expcnt 6:4 and lgkmcnt 11:8 at
+// their maximum so they do not wait).
+#define TEMPO_VMCNT_IMM(n) (((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
+__device__ __forceinline__ void wait_vmcnt(int n) {
+  switch (n) {
+#define TEMPO_W(i) \
+  case i:          \
+    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(i)); \
+    break;
+    TEMPO_W(0) TEMPO_W(1) TEMPO_W(2) TEMPO_W(3) TEMPO_W(4) TEMPO_W(5) TEMPO_W(6) TEMPO_W(7)
+    TEMPO_W(8) TEMPO_W(9) TEMPO_W(10) TEMPO_W(11) TEMPO_W(12) TEMPO_W(13) TEMPO_W(14) TEMPO_W(15)
+    TEMPO_W(16) TEMPO_W(17) TEMPO_W(18) TEMPO_W(19) TEMPO_W(20) TEMPO_W(21) TEMPO_W(22) TEMPO_W(23)
+    TEMPO_W(24) TEMPO_W(25) TEMPO_W(26) TEMPO_W(27) TEMPO_W(28) TEMPO_W(29) TEMPO_W(30) TEMPO_W(31)
+    TEMPO_W(32) TEMPO_W(33) TEMPO_W(34) TEMPO_W(35) TEMPO_W(36) TEMPO_W(37) TEMPO_W(38) TEMPO_W(39)
+    TEMPO_W(40) TEMPO_W(41) TEMPO_W(42) TEMPO_W(43) TEMPO_W(44) TEMPO_W(45) TEMPO_W(46) TEMPO_W(47)
+    TEMPO_W(48) TEMPO_W(49) TEMPO_W(50) TEMPO_W(51) TEMPO_W(52) TEMPO_W(53) TEMPO_W(54) TEMPO_W(55)
+    TEMPO_W(56) TEMPO_W(57) TEMPO_W(58) TEMPO_W(59) TEMPO_W(60) TEMPO_W(61) TEMPO_W(62) TEMPO_W(63)
+#undef TEMPO_W
+    default:
+      __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
+  }
+}
+
+// Workgroup barrier without a memory fence (the fence would make the
+// compiler wait for every outstanding load, draining the pipeline); the
+// empty asm statements keep LDS accesses on their side of the barrier.
+__device__ __forceinline__ void barrier_nofence() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// 16 bytes per lane from global memory straight into LDS at
+// lds_base + 16 * lane (global_load_lds_dwordx4; the LDS base goes in M0).
+// Issued from inline assembly so that the compiler does not track it: it
+// would otherwise wait for every such load before each LDS read, since it
+// cannot tell which ring stage a read touches.  The caller waits with
+// wait_vmcnt before using the data.
+__device__ __forceinline__ void lds_dma16(const void* gptr, const void* lds_base) {
+  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
+  asm volatile(
+      "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, off" ::"v"(gptr),
+      "s"(lds)
+      : "memory", "m0");
+}
+
+// Byte offset of 16-byte chunk c of row r in a swizzled tile.
+__device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ (r & 7)) << 4); }
+
 template <int BM, bool GATEUP>
-__global__ __launch_bounds__(256, 2) void k_gemm_bf16(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+__global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
                                                       size_t w_slot_stride, uint16_t* __restrict__ C,
                                                       const int32_t* __restrict__ slot_counts,
                                                       const int32_t* __restrict__ slot_offsets, int S, int Kd,
-                                                      int Nout, int up_off, int max_tiles,
+                                                      int Nout, int max_tiles,
                                                       const uint32_t* __restrict__ hdr, uint64_t* __restrict__ t0,
                                                       uint64_t* __restrict__ t1, int timing) {
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDS_ROW];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BNW * LDS_ROW];
+  constexpr int B_BYTES = BNW * ROWB;
+  __shared__ __attribute__((aligned(1024))) char ring[RING_BYTES];
   __shared__ int32_t s_off[kMaxS + 1];
   __shared__ int32_t s_cnt[kMaxS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  constexpr int MI = BM / 64;  // 32-row blocks per wavefront
+  constexpr int MI = BM / 64;              // 32-row blocks per wavefront
   constexpr int NCOLS = GATEUP ? 64 : 128;  // output columns per tile
+  constexpr int AG = BM / 32;               // A 8-row groups per wavefront
+  constexpr int BG = BNW / 32;              // B 8-row groups per wavefront
 
   for (int s = tid; s <= S; s += 256) s_off[s] = slot_offsets[s];
   for (int s = tid; s < S; s += 256) s_cnt[s] = slot_counts[s];
@@ -75,13 +143,17 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const uint16_t* __restrict
   const int nb_lo = xcd * nbx;
   const int my_nb = max(0, min(NB, nb_lo + nbx) - nb_lo);
   const int items = NT * my_nb;
+  const int KT = Kd / BK;
+
+  // this lane's place in a 1 KB (8-row) load group: row within the group and
+  // the global chunk that lands in its swizzled LDS position
+  const int lrow = lane >> 3, gchunk = (lane & 7) ^ (lane >> 3);
 
   for (int it = j0; it < items; it += wpx) {
     const int tile = it / my_nb;
     const int nb = nb_lo + it % my_nb;
-    // slot of this tile: largest s with s_off[s] <= tile*BM
     const int row0 = tile * BM;
-    int lo = 0, hi = S;  // invariant: s_off[lo] <= row0 < s_off[hi]
+    int lo = 0, hi = S;  // slot of this tile: s_off[lo] <= row0 < s_off[hi]
     while (hi - lo > 1) {
       const int mid = (lo + hi) >> 1;
       if (s_off[mid] <= row0) lo = mid;
@@ -93,38 +165,45 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const uint16_t* __restrict
     if (timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
 
     const uint16_t* __restrict__ Wsl = W + (size_t)slot * w_slot_stride;
-    // global source rows of the B tile
-    auto wrow = [&](int r) -> int {
-      if (GATEUP) return r < 64 ? nb * 64 + r : up_off + nb * 64 + (r - 64);
-      return nb * 128 + r;
-    };
+    // per-lane source pointers at k = 0 for this wavefront's load groups
+    const uint16_t* srcA[AG];
+    const uint16_t* srcB[BG];
+    int nA = 0;  // A groups this wavefront loads (those with a real row)
+#pragma unroll
+    for (int j = 0; j < AG; j++) {
+      const int g = wave + 4 * j, r = g * 8 + lrow;
+      srcA[j] = A + (size_t)(row0 + r) * Kd + gchunk * 8;
+      nA += (g * 8 < nvalid) ? 1 : 0;
+    }
+    // packed weights: the item's tiles are contiguous 16 KB blocks, one per
+    // contraction step; group g of a tile is its g-th KB
+#pragma unroll
+    for (int j = 0; j < BG; j++) {
+      const int g = wave + 4 * j;
+      srcB[j] = Wsl + ((size_t)nb * KT * BNW * BK) + g * 8 * BK + lane * 8;
+    }
+    const int L = BG + nA;  // load instructions per stage for this wavefront
+    // ring geometry of this item: a stage holds the activation groups that
+    // have a real row, then the 16 KB weight tile; the fewer real rows, the
+    // more stages fit and the more weight bytes are in flight
+    const int a_groups = (nvalid + 7) >> 3;
+    const int A_BYTES = a_groups * 8 * ROWB;
+    const int STAGE = A_BYTES + B_BYTES;
+    const int NS = min(NS_MAX, RING_BYTES / STAGE);
+    const int mi_live = (nvalid - wm * (BM / 2) + 31) >> 5;  // this wavefront's 32-row blocks with a real row
 
-    constexpr int ACH = BM * BK / 8 / 256;   // 16-byte chunks per thread (A)
-    constexpr int BCH = BNW * BK / 8 / 256;  // (B)
-    uint4 ra[ACH], rb[BCH];
-    auto gload = [&](int k0) {
+    auto issue = [&](int kt) {
+      char* st = ring + (kt % NS) * STAGE;
 #pragma unroll
-      for (int i = 0; i < ACH; i++) {
-        const int c = tid + 256 * i, r = c >> 3, kc = c & 7;
-        if (r < nvalid) ra[i] = *reinterpret_cast<const uint4*>(A + (size_t)(row0 + r) * Kd + k0 + kc * 8);
-        else ra[i] = make_uint4(0, 0, 0, 0);
+      for (int j = 0; j < AG; j++) {
+        const int g = wave + 4 * j;
+        if (g * 8 < nvalid)
+          lds_dma16(srcA[j] + kt * BK, st + g * 8 * ROWB);
       }
 #pragma unroll
-      for (int i = 0; i < BCH; i++) {
-        const int c = tid + 256 * i, r = c >> 3, kc = c & 7;
-        rb[i] = *reinterpret_cast<const uint4*>(Wsl + (size_t)wrow(r) * Kd + k0 + kc * 8);
-      }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-      for (int i = 0; i < ACH; i++) {
-        const int c = tid + 256 * i, r = c >> 3, kc = c & 7;
-        *reinterpret_cast<uint4*>(&sA[buf][r * LDS_ROW + kc * 8]) = ra[i];
-      }
-#pragma unroll
-      for (int i = 0; i < BCH; i++) {
-        const int c = tid + 256 * i, r = c >> 3, kc = c & 7;
-        *reinterpret_cast<uint4*>(&sB[buf][r * LDS_ROW + kc * 8]) = rb[i];
+      for (int j = 0; j < BG; j++) {
+        const int g = wave + 4 * j;
+        lds_dma16(srcB[j] + (size_t)kt * BNW * BK, st + A_BYTES + g * 8 * ROWB);
       }
     };
 
@@ -136,35 +215,36 @@ __global__ __launch_bounds__(256, 2) void k_gemm_bf16(const uint16_t* __restrict
 #pragma unroll
         for (int i = 0; i < 16; i++) acc[mi][j][i] = 0.f;
 
-    const int KT = Kd / BK;
-    gload(0);
-    __syncthreads();  // previous item's readers are done with buffer 0
-    lstore(0);
-    __syncthreads();
+    barrier_nofence();  // every wavefront is done reading the ring (previous item)
+#pragma unroll
+    for (int s = 0; s < NS - 1; s++)
+      if (s < KT) issue(s);
     for (int kt = 0; kt < KT; kt++) {
-      const int buf = kt & 1;
-      if (kt + 1 < KT) gload((kt + 1) * BK);
+      wait_vmcnt(L * min(NS - 2, KT - 1 - kt));
+      barrier_nofence();
+      if (kt + NS - 1 < KT) issue(kt + NS - 1);
+      const char* st = ring + (kt % NS) * STAGE;
 #pragma unroll
       for (int ks = 0; ks < BK / 16; ks++) {
+        const int c = 2 * ks + (lane >> 5);
         bf16x8 a[MI], b[2];
-        const int kk = ks * 16 + (lane >> 5) * 8;
 #pragma unroll
-        for (int mi = 0; mi < MI; mi++)
-          a[mi] = *reinterpret_cast<const bf16x8*>(
-              &sA[buf][(wm * (BM / 2) + mi * 32 + (lane & 31)) * LDS_ROW + kk]);
+        for (int mi = 0; mi < MI; mi++) {
+          const int r = wm * (BM / 2) + mi * 32 + (lane & 31);
+          if (mi < mi_live) a[mi] = *reinterpret_cast<const bf16x8*>(st + swz(r, c));
+        }
 #pragma unroll
         for (int j = 0; j < 2; j++) {
-          const int brow = GATEUP ? (j * 64 + wn * 32) : (wn * 64 + j * 32);
-          b[j] = *reinterpret_cast<const bf16x8*>(&sB[buf][(brow + (lane & 31)) * LDS_ROW + kk]);
+          const int r = (GATEUP ? (j * 64 + wn * 32) : (wn * 64 + j * 32)) + (lane & 31);
+          b[j] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + swz(r, c));
         }
 #pragma unroll
         for (int mi = 0; mi < MI; mi++)
+          if (mi < mi_live)
 #pragma unroll
-          for (int j = 0; j < 2; j++)
-            acc[mi][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[j], acc[mi][j], 0, 0, 0);
+            for (int j = 0; j < 2; j++)
+              acc[mi][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[j], acc[mi][j], 0, 0, 0);
       }
-      if (kt + 1 < KT) lstore(buf ^ 1);
-      __syncthreads();
     }
 
     // epilogue
@@ -203,16 +283,16 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   uint64_t* t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint16_t* h = reinterpret_cast<uint16_t*>(ws + L.h);
-  const int grid = persistent_grid();
+  const int grid = persistent_grid(1);
   const int max_tiles = L.row_cap / BM;
   hipLaunchKernelGGL((k_gemm_bf16<BM, true>), dim3(grid), dim3(256), 0, st,
                      static_cast<const uint16_t*>(d.x_perm), static_cast<const uint16_t*>(w.w13),
-                     (size_t)2 * s.I * s.H, h, d.slot_counts, d.slot_offsets, s.S, s.H, s.I, s.I, max_tiles, hdr, t0,
-                     t1, timing ? 1 : 0);
+                     (size_t)2 * s.I * s.H, h, d.slot_counts, d.slot_offsets, s.S, s.H, s.I, max_tiles, hdr, t0, t1,
+                     timing ? 1 : 0);
   if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_gemm_bf16<BM, false>), dim3(grid), dim3(256), 0, st, h,
                      static_cast<const uint16_t*>(w.w2), (size_t)s.H * s.I, static_cast<uint16_t*>(y_perm),
-                     d.slot_counts, d.slot_offsets, s.S, s.I, s.H, 0, max_tiles, hdr, t0, t1, timing ? 1 : 0);
+                     d.slot_counts, d.slot_offsets, s.S, s.I, s.H, max_tiles, hdr, t0, t1, timing ? 1 : 0);
   return hipGetLastError();
 }
 

@@ -14,8 +14,6 @@ namespace tempo {
 // the per-block histograms).
 constexpr int kCountChunk = 1024;
 constexpr int kCountThreads = 256;
-// Pairs handled by one block of the scatter/gather kernel.
-constexpr int kScatterPairs = 32;
 
 constexpr int kMaxE = 1024;
 constexpr int kMaxS = 256;
@@ -69,10 +67,14 @@ hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, con
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
                           uint64_t* slot_time_ns, hipStream_t st);
 
+hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& natural,
+                       const tempo_expert_weights& packed, hipStream_t st);
+
 // Whether stage-2 kernels exist for this shape's element type and M-tile.
 bool experts_supported(const tempo_moe_shape& s);
 
-// Number of workgroups of the persistent stage-2 kernels.
-int persistent_grid();
+// Workgroups of a persistent kernel with per_cu resident workgroups per CU
+// (a multiple of 8, the XCD count).
+int persistent_grid(int per_cu);
 
 }  // namespace tempo

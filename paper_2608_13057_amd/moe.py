@@ -155,6 +155,18 @@ class WeightTensors:
         return ExpertWeights(_ptr(self.w13), _ptr(self.w13_scale), _ptr(self.w2), _ptr(self.w2_scale))
 
 
+def pack_weights(shape: MoEShape, natural: WeightTensors, stream=None) -> WeightTensors:
+    """One-time re-layout (tempo_moe_pack_weights): returns new tensors holding
+    w13 / w2 in the packed layout stage 2 reads; scales are shared as is."""
+    _check_weights(shape, natural)
+    packed = WeightTensors(torch.empty_like(natural.w13), torch.empty_like(natural.w2), natural.w13_scale,
+                           natural.w2_scale)
+    sh, nat, pk = shape.c(), natural.c(), packed.c()
+    check(_lib.load().tempo_moe_pack_weights(ctypes.byref(sh), ctypes.byref(nat), ctypes.byref(pk),
+                                             _stream(stream)), "tempo_moe_pack_weights")
+    return packed
+
+
 def _check_inputs(shape, topk_ids, x, x_scale):
     _need(topk_ids, torch.int32, (shape.T, shape.K), "topk_ids")
     _need(x, shape.elem, (shape.T, shape.H), "x")
@@ -206,7 +218,8 @@ def dispatch(shape: MoEShape, plan: PlanTensors, topk_ids, x, x_scale, out: Disp
 
 
 def experts(shape: MoEShape, disp: DispatchBuffers, weights: WeightTensors, y_perm, ws: Workspace, stream=None):
-    """Stage 2 (tempo_moe_experts): writes y_perm [row_cap, H] bf16."""
+    """Stage 2 (tempo_moe_experts): writes y_perm [row_cap, H] bf16.  weights
+    must be packed (pack_weights)."""
     _check_disp(shape, disp, ws.row_cap)
     _check_weights(shape, weights)
     _need(y_perm, torch.int16, (ws.row_cap, shape.H), "y_perm")
@@ -231,7 +244,8 @@ def combine(shape: MoEShape, pair_row, topk_w, y_perm, y, stream=None):
 
 def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, weights: WeightTensors,
             disp: DispatchBuffers, y, ws: Workspace, slot_time_ns=None, stage_events=None, stream=None):
-    """Stages 1-3 (tempo_moe_forward): writes y [T, H] bf16 (int16 bits).
+    """Stages 1-3 (tempo_moe_forward): writes y [T, H] bf16 (int16 bits);
+    weights must be packed (pack_weights).
     stage_events: optional list of 5 torch.cuda.Event (created with
     enable_timing=True) recorded around the stages."""
     _check_inputs(shape, topk_ids, x, x_scale)
@@ -253,6 +267,36 @@ def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, we
                                         _ptr(slot_time_ns), evs, ws.ptr, ws.nbytes, _stream(stream)),
           "tempo_moe_forward")
     return y
+
+
+class PreparedForward:
+    """A validated tempo_moe_forward call whose ctypes arguments are built
+    once; calling it re-issues the same launch sequence on the current (or a
+    given) stream with no per-call Python checks -- for serving loops and
+    graph capture.  The tensors passed in must stay alive and in place."""
+
+    def __init__(self, shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, weights: WeightTensors,
+                 disp: DispatchBuffers, y, ws: Workspace, slot_time_ns=None):
+        _check_inputs(shape, topk_ids, x, x_scale)
+        _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
+        _check_plan(shape, plan)
+        _check_weights(shape, weights)
+        _check_disp(shape, disp, ws.row_cap)
+        _need(y, torch.int16, (shape.T, shape.H), "y")
+        if slot_time_ns is not None:
+            _need(slot_time_ns, torch.int64, (shape.S,), "slot_time_ns")
+        self._keep = (shape.c(), plan.c(), weights.c(), disp.c())
+        sh, pl, w, do = self._keep
+        self._args = [ctypes.byref(sh), ctypes.byref(pl), _ptr(topk_ids), _ptr(topk_w), _ptr(x), _ptr(x_scale),
+                      ctypes.byref(w), ctypes.byref(do), _ptr(y), _ptr(slot_time_ns)]
+        self._tail = [ws.ptr, ws.nbytes]
+        self._fn = _lib.load().tempo_moe_forward
+
+    def __call__(self, stage_events=None, stream=None):
+        evs = None
+        if stage_events is not None:
+            evs = (ctypes.c_void_p * 5)(*[_event_handle(e) for e in stage_events])
+        check(self._fn(*self._args, evs, *self._tail, _stream(stream)), "tempo_moe_forward")
 
 
 def _event_handle(ev) -> int:

@@ -57,9 +57,11 @@ class Case:
                                       to_dev(self.plan.remote_weight, device),
                                       to_dev(self.plan.remote_replicas, device))
         if weights:
-            self.d_weights = moe.WeightTensors(to_dev(self.w13, device), to_dev(self.w2, device),
-                                               None if self.s13 is None else to_dev(self.s13, device),
-                                               None if self.s2 is None else to_dev(self.s2, device))
+            natural = moe.WeightTensors(to_dev(self.w13, device), to_dev(self.w2, device),
+                                        None if self.s13 is None else to_dev(self.s13, device),
+                                        None if self.s2 is None else to_dev(self.s2, device))
+            self.d_weights = moe.pack_weights(self.shape, natural)
+            del natural
         self.ws = moe.Workspace(self.shape, device)
         self.disp = moe.DispatchBuffers.allocate(self.shape, self.ws.row_cap, device)
 

@@ -165,3 +165,39 @@ def test_forward_full_size_sampled(name, plan):
     assert err <= TOL_EXACT[wl.dtype]
     assert np.all(y[none] == 0)
     assert np.all((st > 0) == (d["slot_counts"] > 0))
+
+
+def test_pack_layout():
+    """The packed weight layout: per slot, output block by output block, each
+    128-byte contraction step a 16 KB tile of 128 rows x 8 chunks of 16
+    bytes, chunk c of row r at position c ^ (r & 7); gate/up blocks pair gate
+    rows n..n+63 with up rows I+n..I+n+63."""
+    import torch
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(3)
+    S, H, I = 2, 256, 384
+    shape = moe.MoEShape(T=4, K=1, E=2, S=S, H=H, I=I)
+    w13 = rng.integers(0, 2**16, size=(S, 2 * I, H), dtype=np.uint16)
+    w2 = rng.integers(0, 2**16, size=(S, H, I), dtype=np.uint16)
+    pk = moe.pack_weights(shape, moe.WeightTensors(to_dev(w13), to_dev(w2)))
+    torch.cuda.synchronize()
+
+    def expect(w, rows_of_block, nblk):
+        S_, R, C = w.shape
+        ch = w.reshape(S_, R, C // 8, 8)  # 16-byte chunks of 8 bf16
+        KT = C // 64
+        out = np.empty((S_, nblk, KT, 128, 8, 8), np.uint16)
+        for nb in range(nblk):
+            rows = rows_of_block(nb)
+            for kt in range(KT):
+                for r in range(128):
+                    for p in range(8):
+                        out[:, nb, kt, r, p] = ch[:, rows[r], kt * 8 + (p ^ (r & 7))]
+        return out.reshape(S_, -1)
+
+    e13 = expect(w13, lambda nb: list(range(nb * 64, nb * 64 + 64)) + list(range(I + nb * 64, I + nb * 64 + 64)),
+                 I // 64)
+    e2 = expect(w2, lambda nb: list(range(nb * 128, nb * 128 + 128)), H // 128)
+    assert np.array_equal(to_host(pk.w13).reshape(S, -1), e13)
+    assert np.array_equal(to_host(pk.w2).reshape(S, -1), e2)
