@@ -21,12 +21,14 @@
 // earlier rounds.  No atomics decide positions.
 //
 // Two paths, both free of zero-initialised memory:
-//   small batches (T*K <= 16384): k_dispatch_small -- one 1024-thread block
-//     ranks every pair into LDS, splits, scans and writes every index output;
-//     then k_gather copies the activation rows, one wavefront per pair.
+//   small batches (T*K <= 16384): k_dispatch_fused -- one launch; every
+//     block re-derives the counts and the plan from all ids (cheap at this
+//     size) and places and gathers its own 64 pairs, so no block waits for
+//     another.
 //   large batches: k_count (blocks of 1024 pairs, per-block histograms and
 //     in-block ranks) -> k_plan (one block: per-expert scan over blocks, split,
-//     offsets) -> k_scatter (index outputs) -> k_gather.
+//     offsets) -> k_scatter (index outputs) -> k_gather (one wavefront per
+//     pair).
 #include "internal.h"
 
 namespace tempo {
@@ -113,9 +115,10 @@ struct SlotLds {
 };
 
 // Plan split, padded sizes, offsets, padding-row markers and header.  n_e is
-// read from n (LDS or global); runs on one block of NW wavefronts.
-template <int NW>
-__device__ void plan_slots(const int32_t* n, int E, int S, int M, uint32_t err_in, const int32_t* __restrict__ slot_expert,
+// read from n (LDS or global); runs on one block of NW wavefronts with
+// S <= 64 * NW.  WRITE = false computes the LDS tables only.
+template <int NW, bool WRITE>
+__device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
                            const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                            const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ slot_counts,
                            int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
@@ -146,7 +149,7 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, uint32_t err_i
             nloc_before++;
           }
         }
-      const int rr = remote_replicas[e];
+      const int rr = remote_replicas[e];  // LDS or global
       const uint32_t rw = remote_weight[e];
       const bool has_remote = rw > 0u || rr > 0;
       if (has_remote) W += rw;
@@ -168,14 +171,20 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, uint32_t err_i
     }
     L.c[s] = c;
     L.lo[s] = lo;
-    slot_counts[s] = c;
-    if (slot_lo_out) slot_lo_out[s] = lo;
+    if (WRITE) {
+      slot_counts[s] = c;
+      if (slot_lo_out) slot_lo_out[s] = lo;
+    }
     P = (c + M - 1) / M * M;
   }
   int total = 0;
   const int off = block_exclusive_scan<NW>(P, s_tmp, &total);
   if (tid < S) L.off[tid] = off;
   if (tid == 0) L.off[S] = total;
+  if (!WRITE) {
+    __syncthreads();
+    return;
+  }
   // tiles, G, N
   const int tiles = block_exclusive_scan<NW>(P / M, s_tmp, &total), ntiles = total;
   (void)tiles;
@@ -187,7 +196,7 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, uint32_t err_i
     hdr[kHdrTiles] = (uint32_t)ntiles;
     hdr[kHdrActive] = (uint32_t)G;
     hdr[kHdrPairs] = (uint32_t)N;
-    const uint32_t e = err_in | *s_err;
+    const uint32_t e = *s_err;
     hdr[kHdrLastErr] = e;
     hdr[kHdrSticky] = hdr[kHdrSticky] | e;
   }
@@ -214,59 +223,174 @@ __device__ __forceinline__ int row_of(const SlotLds& L, int S, int e, int r) {
 }
 
 // ---------------------------------------------------------------------------
-// small batches: everything but the row copy in one block
+// small batches: one launch, no grid-wide synchronisation
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(1024) void k_dispatch_small(const int32_t* __restrict__ ids, int P, int Pv, int K, int E,
-                                                         int ebits, int S, int M, const int32_t* __restrict__ slot_expert,
-                                                         const uint32_t* __restrict__ slot_weight,
-                                                         const uint32_t* __restrict__ remote_weight,
-                                                         const int32_t* __restrict__ remote_replicas,
-                                                         int32_t* __restrict__ expert_counts,
-                                                         uint32_t* __restrict__ cum_counts,
-                                                         int32_t* __restrict__ slot_counts,
-                                                         int32_t* __restrict__ slot_offsets,
-                                                         int32_t* __restrict__ row_token, int32_t* __restrict__ pair_row,
-                                                         uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0,
-                                                         uint64_t* __restrict__ t1) {
-  constexpr int NW = 16;
-  extern __shared__ int32_t dyn[];  // run[E], wc[NW][E], rank[P]
-  int32_t* run = dyn;
-  int32_t* wc = dyn + E;
-  int32_t* rank = dyn + E + NW * E;
+// Block b owns pairs [64 b, 64 b + 64).  Every block histograms all valid ids
+// (from L2; 16K pairs at most) -- the total gives n_e, the part before its
+// chunk the rank offset of its pairs -- then recomputes the small plan split
+// and slot offsets itself, places and gathers its own pairs.  Block 0 alone
+// writes the per-expert / per-slot outputs and the header.
+constexpr int kFusedChunk = 64;
+
+template <int ESIZE>
+__global__ __launch_bounds__(256) void k_dispatch_fused(
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int ebits, int S, int M, int H,
+    const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
+    const uint32_t* __restrict__ remote_weight, const int32_t* __restrict__ remote_replicas,
+    int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
+    int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token, int32_t* __restrict__ pair_row,
+    const uint8_t* __restrict__ x, const float* __restrict__ x_scale, uint8_t* __restrict__ x_perm,
+    float* __restrict__ x_perm_scale, uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0,
+    uint64_t* __restrict__ t1) {
+  constexpr int NW = 4;
+  constexpr int IDS_PER_THREAD = kSmallMaxPairs / 256;  // every id of the batch, 64 per thread at most
+  constexpr int BATCH = 16;                              // id loads in flight per thread
+  extern __shared__ int32_t dyn[];  // n_all[E], n_before[E], first_slot[E], rem_w[E], rem_r[E]
+  int32_t* n_all = dyn;
+  int32_t* n_before = dyn + E;
+  int32_t* first_slot = dyn + 2 * E;
+  uint32_t* rem_w = reinterpret_cast<uint32_t*>(dyn + 3 * E);
+  int32_t* rem_r = dyn + 4 * E;
   __shared__ SlotLds L;
   __shared__ uint32_t s_w[kMaxS];
+  __shared__ int32_t s_next[kMaxS];
   __shared__ int s_tmp[64];
   __shared__ uint32_t s_err;
-  const int tid = threadIdx.x;
-  for (int i = tid; i < (NW + 1) * E; i += 1024) dyn[i] = 0;
+  __shared__ int32_t s_rank[kFusedChunk];
+  __shared__ int32_t s_prow[kFusedChunk], s_ptok[kFusedChunk];
+  __shared__ int s_nplaced;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int base = blockIdx.x * kFusedChunk;
+
+  // every global input this block needs is requested before anything waits
+  for (int i = tid; i < E; i += 256) {
+    rem_w[i] = remote_weight[i];
+    rem_r[i] = remote_replicas[i];
+    n_all[i] = 0;
+    n_before[i] = 0;
+    first_slot[i] = 0x7fffffff;
+  }
   if (tid == 0) s_err = 0;
-  __syncthreads();
+
+  // histogram of all valid ids; wavefronts aggregate equal ids with ballots
   int bad = 0;
-  for (int base = 0; base < P; base += 1024) {
-    const int p = base + tid;
-    int e = -1;
-    if (p < Pv) {
-      const int id = ids[p];
+  const int nq = (P + 255) / 256;
+  for (int b0 = 0; b0 < nq; b0 += BATCH) {
+    int idv[BATCH];
+#pragma unroll
+    for (int u = 0; u < BATCH; u++) {
+      const int p = (b0 + u) * 256 + tid;
+      idv[u] = (b0 + u < nq && p < Pv) ? ids[p] : -1;
+    }
+    __syncthreads();  // LDS initialisation done (first batch) / keeps batches in step
+#pragma unroll
+    for (int u = 0; u < BATCH; u++) {
+      if (b0 + u >= nq) break;
+      const int q0 = (b0 + u) * 256;
+      int e = -1;
+      const int id = idv[u];
       if (id >= 0 && id < E) e = id;
       else if (id != -1) bad = 1;
+      uint64_t peers = __ballot(e >= 0);
+      for (int b = 0; b < ebits; b++) {
+        const int bit = (e >> b) & 1;
+        const uint64_t m = __ballot(e >= 0 && bit);
+        peers &= bit ? m : ~m;
+      }
+      // a wavefront's 64 pairs lie wholly before the block's chunk, on it, or after it
+      const int wbase = q0 + w * 64;
+      if (e >= 0) {
+        const int below = __popcll(peers & ((1ull << lane) - 1ull));
+        if (below == 0) {
+          atomicAdd(&n_all[e], __popcll(peers));
+          if (wbase < base) atomicAdd(&n_before[e], __popcll(peers));
+        }
+        if (wbase == base) s_rank[lane] = below;  // in-chunk rank of an own pair
+      }
     }
-    const int rk = rank_round<NW>(e, E, ebits, run, wc);
-    if (p < P) rank[p] = e >= 0 ? rk : -1;
   }
-  if (__syncthreads_or(bad) && tid == 0) s_err = TEMPO_DERR_BAD_ID;
-  for (int e = tid; e < E; e += 1024) {
-    expert_counts[e] = run[e];
-    if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)run[e];
+  (void)IDS_PER_THREAD;
+  // own pairs' ids (L2 hits: just read above)
+  int own_e = -1;
+  if (tid < kFusedChunk && base + tid < Pv) own_e = ids[base + tid];
+  const int any_bad = __syncthreads_or(bad);
+  if (blockIdx.x == 0) {
+    if (tid == 0 && any_bad) s_err = TEMPO_DERR_BAD_ID;
+    for (int e = tid; e < E; e += 256) {
+      expert_counts[e] = n_all[e];
+      if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)n_all[e];
+    }
+  }
+  // plan split and offsets (every block; outputs from block 0 only)
+  if (blockIdx.x == 0) {
+    plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, rem_w, rem_r, slot_counts, slot_offsets,
+                         row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+  } else {
+    plan_slots<NW, false>(n_all, E, S, M, slot_expert, slot_weight, rem_w, rem_r, slot_counts, slot_offsets,
+                          row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+  }
+  // per-expert list of local slots in ascending order: first_slot[e], s_next[s]
+  for (int s = tid; s < S; s += 256) {
+    const int e = L.se[s];
+    int nx = -1;
+    if (e >= 0 && e < E) {
+      atomicMin(&first_slot[e], s);
+      for (int s2 = s + 1; s2 < S; s2++)
+        if (L.se[s2] == e) {
+          nx = s2;
+          break;
+        }
+    }
+    s_next[s] = nx;
   }
   __syncthreads();
-  plan_slots<NW>(run, E, S, M, 0u, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
-                 row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
-  for (int p = tid; p < P; p += 1024) {
+  // own pairs: rank -> slot -> row
+  if (tid < kFusedChunk) {
+    const int p = base + tid;
     int row = -1;
-    if (rank[p] >= 0) row = row_of(L, S, ids[p], rank[p]);
-    pair_row[p] = row;
-    if (row >= 0) row_token[row] = p / K;
+    const int e = own_e;
+    if (e >= 0 && e < E) {
+      const int r = n_before[e] + s_rank[tid];
+      for (int s = first_slot[e]; s >= 0 && s < S; s = s_next[s])
+        if (r >= L.lo[s] && r < L.lo[s] + L.c[s]) {
+          row = L.off[s] + (r - L.lo[s]);
+          break;
+        }
+    }
+    if (p < P) {
+      pair_row[p] = row;
+      if (row >= 0) row_token[row] = p / K;
+    }
+    const uint64_t m = __ballot(row >= 0);
+    if (row >= 0) {
+      const int pos = __popcll(m & ((1ull << lane) - 1ull));
+      s_prow[pos] = row;
+      s_ptok[pos] = p / K;
+    }
+    if (lane == 0) s_nplaced = __popcll(m);
+  }
+  __syncthreads();
+  // gather the placed rows: one wavefront per row, every load of a row in flight
+  const int R = s_nplaced;
+  const int nch = H * ESIZE / 16;
+  for (int j = w; j < R; j += NW) {
+    const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x) + (size_t)s_ptok[j] * nch;
+    uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm) + (size_t)s_prow[j] * nch;
+    constexpr int U = 8;
+    for (int c0 = lane; c0 < nch; c0 += 64 * U) {
+      uint4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; u++) v[u] = src[min(c0 + u * 64, nch - 1)];
+#pragma unroll
+      for (int u = 0; u < U; u++)
+        if (c0 + u * 64 < nch) dst[c0 + u * 64] = v[u];
+    }
+    if (ESIZE == 1) {
+      const int ns = H / 128;
+      for (int i = lane; i < ns; i += 64)
+        x_perm_scale[(size_t)s_prow[j] * ns + i] = x_scale[(size_t)s_ptok[j] * ns + i];
+    }
   }
 }
 
@@ -352,7 +476,7 @@ __global__ __launch_bounds__(1024) void k_plan(int nblk, int E, int S, int M, in
     if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)acc;
   }
   __syncthreads();
-  plan_slots<NW>(s_n, E, S, M, 0u, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
+  plan_slots<NW, true>(s_n, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
                  row_token, slot_lo, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
 }
 
@@ -405,8 +529,7 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair
   for (int i0 = lane; i0 < nch; i0 += 64 * U) {
     uint4 v[U];
 #pragma unroll
-    for (int u = 0; u < U; u++)
-      if (i0 + u * 64 < nch) v[u] = src[i0 + u * 64];
+    for (int u = 0; u < U; u++) v[u] = src[min(i0 + u * 64, nch - 1)];
 #pragma unroll
     for (int u = 0; u < U; u++)
       if (i0 + u * 64 < nch) dst[i0 + u * 64] = v[u];
@@ -433,23 +556,31 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
-  const size_t small_lds = (size_t)(17 * s.E + P) * sizeof(int32_t);
-  if (P <= kSmallMaxPairs && small_lds <= 120 * 1024) {
-    hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(1024), small_lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
-                       s.m_tile, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
-                       out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
-                       out.pair_row, hdr, timing ? 1 : 0, t0, t1);
-  } else {
-    hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t),
-                       st, topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);
-    hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, st, L.nblk, s.E, s.S, s.m_tile, timing ? 1 : 0, blk_hist,
-                       blk_err, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
-                       out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token, slot_lo,
-                       t0, t1, hdr);
-    hipLaunchKernelGGL(k_scatter, dim3(ceil_div(P, 256)), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, blk_hist,
-                       local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets, out.pair_row,
-                       out.row_token);
+  if (P <= kSmallMaxPairs && s.S <= 256) {
+    const size_t lds = (size_t)5 * s.E * sizeof(int32_t);
+    const int nb = ceil_div(P, kFusedChunk);
+    if (s.dtype == TEMPO_BF16)
+      hipLaunchKernelGGL(k_dispatch_fused<2>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
+                         s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
+                         out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
+                         out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
+                         out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
+    else
+      hipLaunchKernelGGL(k_dispatch_fused<1>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
+                         s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
+                         out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
+                         out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
+                         out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
+    return hipGetLastError();
   }
+  hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t), st,
+                     topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);
+  hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, st, L.nblk, s.E, s.S, s.m_tile, timing ? 1 : 0, blk_hist, blk_err,
+                     plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts,
+                     out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token, slot_lo, t0, t1, hdr);
+  hipLaunchKernelGGL(k_scatter, dim3(ceil_div(P, 256)), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, blk_hist,
+                     local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets, out.pair_row,
+                     out.row_token);
   const int nb = ceil_div(P, 4);
   if (s.dtype == TEMPO_BF16)
     hipLaunchKernelGGL(k_gather<2>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
