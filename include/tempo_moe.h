@@ -122,7 +122,10 @@ typedef struct tempo_plan {
  *                 window counts are recovered by wrap-safe differencing
  *   x_perm        [row_cap, H] bf16 or fp8: x_perm[row] = x[row_token[row]]
  *                 on real rows; padding rows are not written
- *   x_perm_scale  [row_cap, H/128] fp32, fp8 only (NULL for bf16)
+ *   x_perm_scale  [H/128, row_cap] fp32, fp8 only (NULL for bf16): the scale
+ *                 of row r and 128-column block b at b * row_cap + r
+ *                 (block-major, so stage 2 reads the scales of one
+ *                 contraction block contiguously); padding rows not written
  */
 typedef struct tempo_dispatch_out {
   int32_t* expert_counts;
@@ -155,8 +158,8 @@ typedef struct tempo_expert_weights {
 
 /*
  * Sizes for a shape.  *workspace_bytes: the workspace every other call needs
- * (one per stream in flight); *row_cap = T*K + S*(m_tile-1), the rows of the
- * permuted buffers.  The workspace must be zero-filled once before its first
+ * (one per stream in flight); *row_cap = T*K + S*(m_tile-1) rounded up to a
+ * multiple of 128, the rows of the permuted buffers.  The workspace must be zero-filled once before its first
  * use (it holds the sticky error word); after that it is reused without
  * clearing.  Returns TEMPO_EINVAL / TEMPO_EUNSUPPORTED for shapes the library
  * rejects.  Either output pointer may be NULL.
@@ -197,8 +200,10 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
  * x_perm_scale) of a stage-1 result from device memory, so no host round
  * trip is needed.  y_perm [row_cap, H] bf16 device: real rows written,
  * padding rows not.  Accumulation is fp32; h is rounded to bf16 (bf16 path)
- * or quantised to e4m3 with 1 x 128 fp32 scales amax/448 (fp8 path); y_perm
- * is rounded to bf16.  The arithmetic of a row does not depend on which slot
+ * or quantised to e4m3 with 1 x 128 fp32 scales amax/448, round to nearest
+ * even, saturating at 448 (fp8 path; the fp8 contraction applies the
+ * activation and weight block scales once per 128-element block); y_perm is
+ * rounded to bf16.  The arithmetic of a row does not depend on which slot
  * or tile it lands in.
  */
 int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* disp,

@@ -17,7 +17,9 @@ Layout make_layout(const tempo_moe_shape& s) {
   Layout L{};
   const size_t P = (size_t)s.T * s.K;
   L.nblk = (int)((P + kCountChunk - 1) / kCountChunk);
-  L.row_cap = (int)(P + (size_t)s.S * (s.m_tile - 1));
+  // rounded up to 128 rows so that every block-major scale column starts on a
+  // 512-byte boundary (stage 2 moves them with 16-byte DMA loads)
+  L.row_cap = (int)((P + (size_t)s.S * (s.m_tile - 1) + 127) / 128 * 128);
   const size_t eh = s.dtype == TEMPO_BF16 ? 2 : 1;
   size_t o = 0;
   L.header = o;
@@ -38,6 +40,8 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + (size_t)L.row_cap * s.I * eh);
   L.h_scale = o;
   o = align_up(o + (s.dtype == TEMPO_BF16 ? 0 : (size_t)L.row_cap * (s.I / 128) * 4));
+  L.h32 = o;
+  o = align_up(o + (s.dtype == TEMPO_BF16 ? 0 : (size_t)L.row_cap * s.I * 4));
   L.y_perm = o;
   o = align_up(o + (size_t)L.row_cap * s.H * 2);
   L.total = o;

@@ -241,8 +241,8 @@ __global__ __launch_bounds__(256) void k_dispatch_fused(
     int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
     int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token, int32_t* __restrict__ pair_row,
     const uint8_t* __restrict__ x, const float* __restrict__ x_scale, uint8_t* __restrict__ x_perm,
-    float* __restrict__ x_perm_scale, uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0,
-    uint64_t* __restrict__ t1) {
+    float* __restrict__ x_perm_scale, int row_cap, uint32_t* __restrict__ hdr, int timing,
+    uint64_t* __restrict__ t0, uint64_t* __restrict__ t1) {
   constexpr int NW = 4;
   constexpr int IDS_PER_THREAD = kSmallMaxPairs / 256;  // every id of the batch, 64 per thread at most
   constexpr int BATCH = 16;                              // id loads in flight per thread
@@ -386,10 +386,10 @@ __global__ __launch_bounds__(256) void k_dispatch_fused(
       for (int u = 0; u < U; u++)
         if (c0 + u * 64 < nch) dst[c0 + u * 64] = v[u];
     }
-    if (ESIZE == 1) {
+    if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
       const int ns = H / 128;
       for (int i = lane; i < ns; i += 64)
-        x_perm_scale[(size_t)s_prow[j] * ns + i] = x_scale[(size_t)s_ptok[j] * ns + i];
+        x_perm_scale[(size_t)i * row_cap + s_prow[j]] = x_scale[(size_t)s_ptok[j] * ns + i];
     }
   }
 }
@@ -515,7 +515,8 @@ __global__ __launch_bounds__(256) void k_scatter(const int32_t* __restrict__ ids
 template <int ESIZE>
 __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair_row, int P, int K, int H,
                                                 const uint8_t* __restrict__ x, const float* __restrict__ x_scale,
-                                                uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale) {
+                                                uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale,
+                                                int row_cap) {
   const int lane = threadIdx.x & 63;
   const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (p >= P) return;
@@ -534,9 +535,9 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair
     for (int u = 0; u < U; u++)
       if (i0 + u * 64 < nch) dst[i0 + u * 64] = v[u];
   }
-  if (ESIZE == 1) {
+  if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
     const int ns = H / 128;
-    for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)row * ns + i] = x_scale[(size_t)t * ns + i];
+    for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)i * row_cap + row] = x_scale[(size_t)t * ns + i];
   }
 }
 
@@ -564,13 +565,13 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
                          s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
                          out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
                          out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
-                         out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
+                         out.x_perm_scale, L.row_cap, hdr, timing ? 1 : 0, t0, t1);
     else
       hipLaunchKernelGGL(k_dispatch_fused<1>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
                          s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
                          out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
                          out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
-                         out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
+                         out.x_perm_scale, L.row_cap, hdr, timing ? 1 : 0, t0, t1);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t), st,
@@ -584,10 +585,12 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   const int nb = ceil_div(P, 4);
   if (s.dtype == TEMPO_BF16)
     hipLaunchKernelGGL(k_gather<2>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
-                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale,
+                       L.row_cap);
   else
     hipLaunchKernelGGL(k_gather<1>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
-                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale,
+                       L.row_cap);
   return hipGetLastError();
 }
 

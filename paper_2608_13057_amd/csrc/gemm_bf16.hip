@@ -41,75 +41,17 @@
 // on the M-tile.
 #include "internal.h"
 
+#include "gemm_common.h"
+
 namespace tempo {
 namespace {
+
+using namespace gemm;
 
 typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
 typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 
-constexpr int BK = 64;           // contraction elements per stage
-constexpr int ROWB = BK * 2;     // bytes per LDS row
-constexpr int BNW = 128;         // weight rows per tile
-constexpr int RING_BYTES = 144 * 1024;  // LDS ring shared by the pipeline stages
-constexpr int NS_MAX = 8;
-
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
-// vmcnt[3:0] bits 3:0, vmcnt[5:4] bits 15:14, expcnt 6:4 and lgkmcnt 11:8 at
-// their maximum so they do not wait).
-#define TEMPO_VMCNT_IMM(n) (((n) & 15) | (((n) >> 4) << 14) | (7 << 4) | (15 << 8))
-__device__ __forceinline__ void wait_vmcnt(int n) {
-  switch (n) {
-#define TEMPO_W(i) \
-  case i:          \
-    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(i)); \
-    break;
-    TEMPO_W(0) TEMPO_W(1) TEMPO_W(2) TEMPO_W(3) TEMPO_W(4) TEMPO_W(5) TEMPO_W(6) TEMPO_W(7)
-    TEMPO_W(8) TEMPO_W(9) TEMPO_W(10) TEMPO_W(11) TEMPO_W(12) TEMPO_W(13) TEMPO_W(14) TEMPO_W(15)
-    TEMPO_W(16) TEMPO_W(17) TEMPO_W(18) TEMPO_W(19) TEMPO_W(20) TEMPO_W(21) TEMPO_W(22) TEMPO_W(23)
-    TEMPO_W(24) TEMPO_W(25) TEMPO_W(26) TEMPO_W(27) TEMPO_W(28) TEMPO_W(29) TEMPO_W(30) TEMPO_W(31)
-    TEMPO_W(32) TEMPO_W(33) TEMPO_W(34) TEMPO_W(35) TEMPO_W(36) TEMPO_W(37) TEMPO_W(38) TEMPO_W(39)
-    TEMPO_W(40) TEMPO_W(41) TEMPO_W(42) TEMPO_W(43) TEMPO_W(44) TEMPO_W(45) TEMPO_W(46) TEMPO_W(47)
-    TEMPO_W(48) TEMPO_W(49) TEMPO_W(50) TEMPO_W(51) TEMPO_W(52) TEMPO_W(53) TEMPO_W(54) TEMPO_W(55)
-    TEMPO_W(56) TEMPO_W(57) TEMPO_W(58) TEMPO_W(59) TEMPO_W(60) TEMPO_W(61) TEMPO_W(62) TEMPO_W(63)
-#undef TEMPO_W
-    default:
-      __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
-  }
-}
-
-// Workgroup barrier without a memory fence (the fence would make the
-// compiler wait for every outstanding load, draining the pipeline); the
-// empty asm statements keep LDS accesses on their side of the barrier.
-__device__ __forceinline__ void barrier_nofence() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
-// 16 bytes per lane from global memory straight into LDS at
-// lds_base + 16 * lane (global_load_lds_dwordx4; the LDS base goes in M0).
-// Issued from inline assembly so that the compiler does not track it: it
-// would otherwise wait for every such load before each LDS read, since it
-// cannot tell which ring stage a read touches.  The caller waits with
-// wait_vmcnt before using the data.
-__device__ __forceinline__ void lds_dma16(const void* gptr, const void* lds_base) {
-  const uint32_t lds = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_base);
-  asm volatile(
-      "s_mov_b32 m0, %1\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %0, off" ::"v"(gptr),
-      "s"(lds)
-      : "memory", "m0");
-}
-
-// Byte offset of 16-byte chunk c of row r in a swizzled tile.
-__device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ (r & 7)) << 4); }
+constexpr int BK = 64;  // bf16 contraction elements per stage (128 bytes)
 
 template <int BM, bool GATEUP>
 __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
@@ -153,13 +95,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
     const int tile = it / my_nb;
     const int nb = nb_lo + it % my_nb;
     const int row0 = tile * BM;
-    int lo = 0, hi = S;  // slot of this tile: s_off[lo] <= row0 < s_off[hi]
-    while (hi - lo > 1) {
-      const int mid = (lo + hi) >> 1;
-      if (s_off[mid] <= row0) lo = mid;
-      else hi = mid;
-    }
-    const int slot = lo;
+    const int slot = slot_of_row(s_off, S, row0);
     const int nvalid = min(BM, s_off[slot] + s_cnt[slot] - row0);
     uint64_t tstart = 0;
     if (timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();

@@ -38,7 +38,8 @@ struct Layout {
   size_t slot_t0;     // [S] uint64 first stage-2 tile start (real-time counter)
   size_t slot_t1;     // [S] uint64 last stage-2 tile end
   size_t h;           // [row_cap, I] bf16 or e4m3
-  size_t h_scale;     // [row_cap, I/128] fp32 (fp8 only)
+  size_t h_scale;     // [I/128, row_cap] fp32 (fp8 only; scale-block-major)
+  size_t h32;         // [row_cap, I] fp32 gate/up output before re-quantisation (fp8 only)
   size_t y_perm;      // [row_cap, H] bf16
   size_t total;
   int nblk;

@@ -121,7 +121,7 @@ class DispatchBuffers:
             row_token=torch.empty(row_cap, **i32),
             pair_row=torch.empty(shape.T, shape.K, **i32),
             x_perm=torch.empty(row_cap, shape.H, dtype=shape.elem, device=device),
-            x_perm_scale=(torch.empty(row_cap, shape.H // 128, dtype=torch.float32, device=device)
+            x_perm_scale=(torch.empty(shape.H // 128, row_cap, dtype=torch.float32, device=device)
                           if shape.dtype == "fp8" else None),
             cum_counts=torch.zeros(shape.E, dtype=torch.int32, device=device) if cum_counts else None,
         )
@@ -200,7 +200,7 @@ def _check_disp(shape, d, row_cap):
     if d.pair_row is not None:
         _need(d.pair_row, torch.int32, (shape.T, shape.K), "pair_row")
     if shape.dtype == "fp8":
-        _need(d.x_perm_scale, torch.float32, (row_cap, shape.H // 128), "x_perm_scale")
+        _need(d.x_perm_scale, torch.float32, (shape.H // 128, row_cap), "x_perm_scale")
     if d.cum_counts is not None:
         _need(d.cum_counts, torch.int32, (shape.E,), "cum_counts")
 

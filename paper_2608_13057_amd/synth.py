@@ -332,6 +332,7 @@ class Workload:
 WORKLOADS = {
     # name: (dtype, T, K, E, H, I, zipf, placement kind, extras, plans)
     "tiny": ("bf16", 96, 2, 6, 256, 512, 1.2, ("local_hot", 6, 2), ("uniform",)),
+    "tiny_fp8": ("fp8", 96, 2, 6, 256, 512, 1.2, ("local_hot", 6, 2), ("uniform",)),
     "qwen3_decode_bf16": ("bf16", 512, 8, 128, 4096, 1536, 1.0, ("remote_hot", 2), ("token_balancing",)),
     "qwen3_decode_fp8": ("fp8", 1024, 8, 128, 4096, 1536, 1.2, ("local_hot_strided", 16, 2),
                          ("uniform", "replica_min")),

@@ -42,12 +42,13 @@ def _local_rows(d_ref, T_valid):
 
 
 @pytest.mark.parametrize("m_tile", [64, 128])
-def test_experts_stage_tiny(m_tile):
+@pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
+def test_experts_stage_tiny(m_tile, name):
     """Stage 2 alone: y_perm real rows against the oracle's per-row FFN."""
     import torch
     from paper_2608_13057_amd import moe, synth
 
-    wl = synth.make_workload("tiny")
+    wl = synth.make_workload(name)
     c = Case(wl, "uniform", m_tile)
     moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
     y_perm = torch.empty(c.ws.row_cap, wl.H, dtype=torch.int16, device="cuda")
@@ -58,10 +59,10 @@ def test_experts_stage_tiny(m_tile):
     real = np.nonzero(rt >= 0)[0]
     slot = np.searchsorted(d["slot_offsets"], real, side="right") - 1
     got = bf16_to_f64(to_host(y_perm)[real])
-    for mode, tol in (("exact", TOL_EXACT["bf16"]), ("mirror", TOL_MIRROR["bf16"])):
-        ref = oracle.ffn_rows(c.x, rt[real], slot, c.w13, c.w2, "bf16", mode)
+    for mode, tol in (("exact", TOL_EXACT[wl.dtype]), ("mirror", TOL_MIRROR[wl.dtype])):
+        ref = oracle.ffn_rows(c.x, rt[real], slot, c.w13, c.w2, wl.dtype, mode, c.xs, c.s13, c.s2)
         err = rel_err_rows(got, ref, np.arange(len(real)))
-        print(f"[experts tiny M={m_tile}] {mode} err={err:.2e}")
+        print(f"[experts {name} M={m_tile}] {mode} err={err:.2e}")
         assert err <= tol
 
 
@@ -90,10 +91,11 @@ def test_combine_stage():
 
 
 @pytest.mark.parametrize("m_tile", [64, 128])
-def test_forward_tiny(m_tile):
+@pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
+def test_forward_tiny(m_tile, name):
     from paper_2608_13057_amd import synth
 
-    wl = synth.make_workload("tiny")
+    wl = synth.make_workload(name)
     c = Case(wl, "uniform", m_tile)
     y, st = _run_forward(c, timing=True)
     d = c.oracle_dispatch()
@@ -102,19 +104,20 @@ def test_forward_tiny(m_tile):
     for mode in ("exact", "mirror"):
         ref = _oracle_y(c, d, mode)
         err = rel_err_rows(got, ref, loc)
-        print(f"[forward tiny M={m_tile}] {mode} err={err:.2e}")
-        assert err <= (TOL_EXACT if mode == "exact" else TOL_MIRROR)["bf16"]
+        print(f"[forward {name} M={m_tile}] {mode} err={err:.2e}")
+        assert err <= (TOL_EXACT if mode == "exact" else TOL_MIRROR)[wl.dtype]
     assert np.all(y[none] == 0)
     sc = d["slot_counts"]
     assert np.all((st > 0) == (sc > 0))
 
 
-def test_forward_split_invariance_bit_exact():
+@pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
+def test_forward_split_invariance_bit_exact(name):
     """The same batch under different splits of the replicated experts over
     their two local slots (and both M-tiles) gives bit-identical y."""
     from paper_2608_13057_amd import synth
 
-    wl = synth.make_workload("tiny")
+    wl = synth.make_workload(name)
     base = wl.plans["uniform"]
     outs = []
     for sw in ([1] * 8, [1, 1, 1, 1, 1, 1, 0, 0], [0, 0, 1, 1, 1, 1, 1, 1], [3, 1, 1, 1, 1, 1, 1, 5]):
@@ -143,7 +146,8 @@ def test_forward_padding_rows_and_empty_batch():
     assert np.all(y0 == 0)
 
 
-@pytest.mark.parametrize("name,plan", [("qwen3_decode_bf16", "token_balancing")])
+@pytest.mark.parametrize("name,plan", [("qwen3_decode_bf16", "token_balancing"), ("qwen3_decode_fp8", "uniform"),
+                                       ("qwen3_decode_fp8", "replica_min"), ("dsv3_decode_fp8", "uniform")])
 def test_forward_full_size_sampled(name, plan):
     """The full-size workload in the benchmark's launch configuration; y is
     checked on a seeded sample of tokens (the oracle computes each one)."""
