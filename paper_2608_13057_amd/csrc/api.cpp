@@ -16,7 +16,7 @@ static size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 Layout make_layout(const tempo_moe_shape& s) {
   Layout L{};
   const size_t P = (size_t)s.T * s.K;
-  L.nblk = (int)((P + kCountChunk - 1) / kCountChunk);
+  L.nblk = (int)((P + kCountThreads - 1) / kCountThreads);
   // rounded up to 128 rows so that every block-major scale column starts on a
   // 512-byte boundary (stage 2 moves them with 16-byte DMA loads)
   L.row_cap = (int)((P + (size_t)s.S * (s.m_tile - 1) + 127) / 128 * 128);
@@ -32,6 +32,7 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + P * 4);
   L.slot_lo = o;
   o = align_up(o + (size_t)s.S * 4);
+
   L.slot_t0 = o;
   o = align_up(o + (size_t)s.S * 8);
   L.slot_t1 = o;
@@ -141,7 +142,7 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
   const Layout L = make_layout(*shape);
   if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
   return dev_status(launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *out, static_cast<char*>(workspace), L,
-                                    false, static_cast<hipStream_t>(stream)));
+                                    false, true, static_cast<hipStream_t>(stream)));
 }
 
 int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* disp,
@@ -157,8 +158,8 @@ int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* di
   char* ws = static_cast<char*>(workspace);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t e = shape->dtype == TEMPO_BF16
-                           ? launch_experts_bf16(*shape, *disp, *weights, y_perm, ws, L, false, nullptr, st)
-                           : launch_experts_fp8(*shape, *disp, *weights, y_perm, ws, L, false, nullptr, st);
+                           ? launch_experts_bf16(*shape, *disp, *weights, nullptr, y_perm, ws, L, false, nullptr, st)
+                           : launch_experts_fp8(*shape, *disp, *weights, nullptr, y_perm, ws, L, false, nullptr, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   return dev_status(e);
 }
@@ -194,10 +195,11 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   auto mark = [&](int i) { return !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!mark(0)) return TEMPO_EDEVICE;
-  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, st);
+  // the gate/up GEMM gathers the activation rows itself; x_perm stays unwritten
+  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, false, st);
   if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
-  e = shape->dtype == TEMPO_BF16 ? launch_experts_bf16(*shape, *disp, *weights, y_perm, ws, L, timing, ev[2], st)
-                                 : launch_experts_fp8(*shape, *disp, *weights, y_perm, ws, L, timing, ev[2], st);
+  e = shape->dtype == TEMPO_BF16 ? launch_experts_bf16(*shape, *disp, *weights, x, y_perm, ws, L, timing, ev[2], st)
+                                 : launch_experts_fp8(*shape, *disp, *weights, x, y_perm, ws, L, timing, ev[2], st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   if (e != hipSuccess || !mark(3)) return TEMPO_EDEVICE;
   e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,

@@ -20,21 +20,27 @@
 // give the offset of earlier wavefronts and a running count the offset of
 // earlier rounds.  No atomics decide positions.
 //
-// Two paths, both free of zero-initialised memory:
-//   small batches (T*K <= 16384): k_dispatch_fused -- one launch; every
-//     block re-derives the counts and the plan from all ids (cheap at this
-//     size) and places and gathers its own 64 pairs, so no block waits for
-//     another.
-//   large batches: k_count (blocks of 1024 pairs, per-block histograms and
-//     in-block ranks) -> k_plan (one block: per-expert scan over blocks, split,
-//     offsets) -> k_scatter (index outputs) -> k_gather (one wavefront per
-//     pair).
+// Two launches, no block ever waits for or signals another (device-scope
+// fences write back L2 on this multi-XCD chip and cost more than the work):
+//   k_count  blocks of 256 pairs: in-block stable ranks and per-block expert
+//            histograms.
+//   k_place  blocks of 64 pairs: each sums the block histograms (n_e and the
+//            prefix of its own count block), recomputes the small plan -- the
+//            split of every expert over its slots, padded sizes, offsets,
+//            per-expert slot lists -- in LDS (block 0 also writes the
+//            per-expert / per-slot outputs and the header), then maps its
+//            pairs rank -> slot -> row and writes the index outputs and
+//            copies the rows, one wavefront per row with every load in
+//            flight (the whole forward skips the copy: its gate/up GEMM reads
+//            the activation rows through row_token directly).
+// Global loads are issued before the values are needed: at one wavefront per
+// SIMD every exposed memory latency (~0.3-0.5 us) adds up.
 #include "internal.h"
 
 namespace tempo {
 namespace {
 
-constexpr int kSmallMaxPairs = 16384;
+constexpr int kPlaceChunk = 64;  // pairs per k_place_gather block
 
 // ---------------------------------------------------------------------------
 // shared pieces
@@ -214,6 +220,107 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t*
     }
 }
 
+// Plan for S <= 64 in one wavefront (lane s = slot s): the same split as
+// plan_slots without block barriers -- per-expert weight sums and the
+// slot-order position come from a readlane loop over the slots, offsets and
+// totals from wavefront scans.  Fills the LDS slot tables (se, lo, c, off and
+// the per-expert slot lists first[E] / next[S]; first must hold INT_MAX on
+// entry) and, when write is set, the global per-slot outputs and the header.
+__device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
+                                const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
+                                const int32_t* __restrict__ remote_replicas, SlotLds& L, int32_t* first,
+                                int32_t* next, bool write, int32_t* __restrict__ slot_counts,
+                                int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
+                                uint32_t* __restrict__ hdr, uint32_t err_in, int timing, uint64_t* __restrict__ t0,
+                                uint64_t* __restrict__ t1) {
+  const int lane = threadIdx.x & 63;
+  const bool live = lane < S;
+  const int e = live ? slot_expert[lane] : -1;
+  const uint32_t w = live ? slot_weight[lane] : 0u;
+  const bool ok = live && e >= 0 && e < E;
+  int rr = 0;
+  uint32_t rw = 0;
+  int ne = 0;
+  if (ok) {
+    rr = remote_replicas[e];
+    rw = remote_weight[e];
+    ne = n[e];
+  }
+  uint32_t err = err_in;
+  if (__ballot(live && !ok)) err |= TEMPO_DERR_BAD_SLOT_EXPERT;
+  uint64_t Wloc = 0, before = 0;
+  int nloc = 0, nbefore = 0, nx = -1;
+  for (int l = 0; l < S; l++) {
+    const int el = __builtin_amdgcn_readlane(e, l);
+    const uint32_t wl = (uint32_t)__builtin_amdgcn_readlane((int)w, l);
+    if (ok && el == e) {
+      Wloc += wl;
+      nloc++;
+      if (l < lane) {
+        before += wl;
+        nbefore++;
+      }
+      if (l > lane && nx < 0) nx = l;
+    }
+  }
+  int c = 0, lo = 0;
+  const bool has_remote = rw > 0u || rr > 0;
+  const uint64_t Wtot = Wloc + (has_remote ? rw : 0u);
+  if (ok) {
+    uint64_t W = Wtot;
+    uint64_t mine = w;
+    const bool uniform = (W == 0) || (W >= (1ull << 32));
+    if (uniform) {
+      W = (uint64_t)nloc + (has_remote && rr > 0 ? (uint64_t)rr : 0ull);
+      before = (uint64_t)nbefore;
+      mine = 1;
+    }
+    const uint64_t blo = (uint64_t)ne * before / W, bhi = (uint64_t)ne * (before + mine) / W;
+    lo = (int)blo;
+    c = (int)(bhi - blo);
+  }
+  if (__ballot(ok && Wtot >= (1ull << 32))) err |= TEMPO_DERR_WEIGHT_OVERFLOW;
+  const int P = (c + M - 1) / M * M;
+  int incl = P, tiles = P / M, g = c > 0, pairs = c;
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const int y = __shfl_up(incl, d);
+    if (lane >= d) incl += y;
+    tiles += __shfl_xor(tiles, d);
+    g += __shfl_xor(g, d);
+    pairs += __shfl_xor(pairs, d);
+  }
+  const int off = incl - P;
+  const int total = __shfl(incl, 63);
+  if (live) {
+    L.se[lane] = e;
+    L.lo[lane] = lo;
+    L.c[lane] = c;
+    L.off[lane] = off;
+    next[lane] = ok ? nx : -1;
+    if (ok && nbefore == 0) first[e] = lane;
+  }
+  if (lane == 0) L.off[S] = total;
+  if (!write) return;
+  if (live) {
+    slot_counts[lane] = c;
+    slot_offsets[lane] = off;
+    for (int r = c; r < P; r++) row_token[off + r] = -1;
+    if (timing) {
+      t0[lane] = ~0ull;
+      t1[lane] = 0ull;
+    }
+  }
+  if (lane == 0) {
+    slot_offsets[S] = total;
+    hdr[kHdrTiles] = (uint32_t)tiles;
+    hdr[kHdrActive] = (uint32_t)g;
+    hdr[kHdrPairs] = (uint32_t)pairs;
+    hdr[kHdrLastErr] = err;
+    hdr[kHdrSticky] = hdr[kHdrSticky] | err;
+  }
+}
+
 // Row of pair p with expert e and rank r (or -1 when the rank falls on the
 // remote share).
 __device__ __forceinline__ int row_of(const SlotLds& L, int S, int e, int r) {
@@ -223,140 +330,143 @@ __device__ __forceinline__ int row_of(const SlotLds& L, int S, int e, int r) {
 }
 
 // ---------------------------------------------------------------------------
-// small batches: one launch, no grid-wide synchronisation
+// launch 1: in-block ranks and block histograms
 // ---------------------------------------------------------------------------
 
-// Block b owns pairs [64 b, 64 b + 64).  Every block histograms all valid ids
-// (from L2; 16K pairs at most) -- the total gives n_e, the part before its
-// chunk the rank offset of its pairs -- then recomputes the small plan split
-// and slot offsets itself, places and gathers its own pairs.  Block 0 alone
-// writes the per-expert / per-slot outputs and the header.
-constexpr int kFusedChunk = 64;
+__global__ __launch_bounds__(kCountThreads) void k_count(const int32_t* __restrict__ ids, int Pv, int E, int ebits,
+                                                          int32_t* __restrict__ blk_hist,
+                                                          uint32_t* __restrict__ blk_err,
+                                                          int32_t* __restrict__ local_rank) {
+  constexpr int NW = kCountThreads / 64;
+  extern __shared__ int32_t sm[];  // run[E], wc[NW][E]
+  int32_t* run = sm;
+  int32_t* wc = sm + E;
+  const int tid = threadIdx.x;
+  const int p = blockIdx.x * kCountThreads + tid;
+  const int id = p < Pv ? ids[p] : -1;
+  for (int i = tid; i < (NW + 1) * E; i += kCountThreads) sm[i] = 0;
+  __syncthreads();
+  int e = -1, bad = 0;
+  if (id >= 0 && id < E) e = id;
+  else if (id != -1) bad = 1;
+  const int rk = rank_round<NW>(e, E, ebits, run, wc);
+  if (e >= 0) local_rank[p] = rk;
+  for (int x = tid; x < E; x += kCountThreads) blk_hist[(size_t)blockIdx.x * E + x] = run[x];
+  const int any_bad = __syncthreads_or(bad);
+  if (tid == 0) blk_err[blockIdx.x] = any_bad ? TEMPO_DERR_BAD_ID : 0u;
+}
+
+// ---------------------------------------------------------------------------
+// launch 2: plan (recomputed per block), rows of the pairs, index outputs,
+// row copies
+// ---------------------------------------------------------------------------
 
 template <int ESIZE>
-__global__ __launch_bounds__(256) void k_dispatch_fused(
-    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int ebits, int S, int M, int H,
-    const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
-    const uint32_t* __restrict__ remote_weight, const int32_t* __restrict__ remote_replicas,
-    int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
-    int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token, int32_t* __restrict__ pair_row,
-    const uint8_t* __restrict__ x, const float* __restrict__ x_scale, uint8_t* __restrict__ x_perm,
-    float* __restrict__ x_perm_scale, int row_cap, uint32_t* __restrict__ hdr, int timing,
+__global__ __launch_bounds__(256) void k_place(
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int H, int row_cap, int nblk,
+    int gather_rows, const int32_t* __restrict__ blk_hist, const uint32_t* __restrict__ blk_err,
+    const int32_t* __restrict__ local_rank, const int32_t* __restrict__ slot_expert,
+    const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
+    const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts,
+    int32_t* __restrict__ slot_counts, int32_t* __restrict__ slot_offsets, int32_t* __restrict__ pair_row,
+    int32_t* __restrict__ row_token, const uint8_t* __restrict__ x, const float* __restrict__ x_scale,
+    uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale, uint32_t* __restrict__ hdr, int timing,
     uint64_t* __restrict__ t0, uint64_t* __restrict__ t1) {
   constexpr int NW = 4;
-  constexpr int IDS_PER_THREAD = kSmallMaxPairs / 256;  // every id of the batch, 64 per thread at most
-  constexpr int BATCH = 16;                              // id loads in flight per thread
-  extern __shared__ int32_t dyn[];  // n_all[E], n_before[E], first_slot[E], rem_w[E], rem_r[E]
+  extern __shared__ int32_t dyn[];  // n_all[E], n_before[E], first[E]
   int32_t* n_all = dyn;
   int32_t* n_before = dyn + E;
-  int32_t* first_slot = dyn + 2 * E;
-  uint32_t* rem_w = reinterpret_cast<uint32_t*>(dyn + 3 * E);
-  int32_t* rem_r = dyn + 4 * E;
+  int32_t* first = dyn + 2 * E;
   __shared__ SlotLds L;
-  __shared__ uint32_t s_w[kMaxS];
   __shared__ int32_t s_next[kMaxS];
+  __shared__ uint32_t s_w[kMaxS];
   __shared__ int s_tmp[64];
   __shared__ uint32_t s_err;
-  __shared__ int32_t s_rank[kFusedChunk];
-  __shared__ int32_t s_prow[kFusedChunk], s_ptok[kFusedChunk];
+  __shared__ int32_t s_prow[kPlaceChunk], s_ptok[kPlaceChunk];
   __shared__ int s_nplaced;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int base = blockIdx.x * kFusedChunk;
-
-  // every global input this block needs is requested before anything waits
-  for (int i = tid; i < E; i += 256) {
-    rem_w[i] = remote_weight[i];
-    rem_r[i] = remote_replicas[i];
-    n_all[i] = 0;
-    n_before[i] = 0;
-    first_slot[i] = 0x7fffffff;
+  const int base = blockIdx.x * kPlaceChunk;
+  const bool writer = blockIdx.x == 0;
+  // own pairs' ids and in-block ranks (issued first)
+  const int p = base + tid;
+  int own_e = -1, own_rk = 0;
+  if (tid < kPlaceChunk && p < Pv) {
+    own_e = ids[p];
+    if (own_e >= 0 && own_e < E) own_rk = local_rank[p];
+    else own_e = -1;
   }
   if (tid == 0) s_err = 0;
-
-  // histogram of all valid ids; wavefronts aggregate equal ids with ballots
-  int bad = 0;
-  const int nq = (P + 255) / 256;
-  for (int b0 = 0; b0 < nq; b0 += BATCH) {
-    int idv[BATCH];
+  // n_e and the prefix of this block's count block, from the block histograms
+  const int cb = base / kCountThreads;
+  for (int ex = tid; ex < E; ex += 256) {
+    int all = 0, bef = 0, b = 0;
+    for (; b + 16 <= nblk; b += 16) {
+      int v[16];
 #pragma unroll
-    for (int u = 0; u < BATCH; u++) {
-      const int p = (b0 + u) * 256 + tid;
-      idv[u] = (b0 + u < nq && p < Pv) ? ids[p] : -1;
-    }
-    __syncthreads();  // LDS initialisation done (first batch) / keeps batches in step
+      for (int u = 0; u < 16; u++) v[u] = blk_hist[(size_t)(b + u) * E + ex];
 #pragma unroll
-    for (int u = 0; u < BATCH; u++) {
-      if (b0 + u >= nq) break;
-      const int q0 = (b0 + u) * 256;
-      int e = -1;
-      const int id = idv[u];
-      if (id >= 0 && id < E) e = id;
-      else if (id != -1) bad = 1;
-      uint64_t peers = __ballot(e >= 0);
-      for (int b = 0; b < ebits; b++) {
-        const int bit = (e >> b) & 1;
-        const uint64_t m = __ballot(e >= 0 && bit);
-        peers &= bit ? m : ~m;
-      }
-      // a wavefront's 64 pairs lie wholly before the block's chunk, on it, or after it
-      const int wbase = q0 + w * 64;
-      if (e >= 0) {
-        const int below = __popcll(peers & ((1ull << lane) - 1ull));
-        if (below == 0) {
-          atomicAdd(&n_all[e], __popcll(peers));
-          if (wbase < base) atomicAdd(&n_before[e], __popcll(peers));
-        }
-        if (wbase == base) s_rank[lane] = below;  // in-chunk rank of an own pair
+      for (int u = 0; u < 16; u++) {
+        bef += (b + u < cb) ? v[u] : 0;
+        all += v[u];
       }
     }
-  }
-  (void)IDS_PER_THREAD;
-  // own pairs' ids (L2 hits: just read above)
-  int own_e = -1;
-  if (tid < kFusedChunk && base + tid < Pv) own_e = ids[base + tid];
-  const int any_bad = __syncthreads_or(bad);
-  if (blockIdx.x == 0) {
-    if (tid == 0 && any_bad) s_err = TEMPO_DERR_BAD_ID;
-    for (int e = tid; e < E; e += 256) {
-      expert_counts[e] = n_all[e];
-      if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)n_all[e];
+    for (; b < nblk; b++) {
+      const int v = blk_hist[(size_t)b * E + ex];
+      bef += (b < cb) ? v : 0;
+      all += v;
+    }
+    n_all[ex] = all;
+    n_before[ex] = bef;
+    first[ex] = 0x7fffffff;
+    if (writer) {
+      expert_counts[ex] = all;
+      if (cum_counts) cum_counts[ex] = cum_counts[ex] + (uint32_t)all;
     }
   }
-  // plan split and offsets (every block; outputs from block 0 only)
-  if (blockIdx.x == 0) {
-    plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, rem_w, rem_r, slot_counts, slot_offsets,
-                         row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+  uint32_t eb = 0;
+  if (writer)
+    for (int b = tid; b < nblk; b += 256) eb |= blk_err[b];
+  __syncthreads();
+  if (eb) atomicOr(&s_err, eb);
+  __syncthreads();
+  // the plan: one wavefront when S <= 64, the block otherwise
+  if (S <= 64) {
+    if (tid < 64)
+      plan_slots_wave(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, L, first, s_next,
+                      writer, slot_counts, slot_offsets, row_token, hdr, s_err, timing, t0, t1);
   } else {
-    plan_slots<NW, false>(n_all, E, S, M, slot_expert, slot_weight, rem_w, rem_r, slot_counts, slot_offsets,
-                          row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
-  }
-  // per-expert list of local slots in ascending order: first_slot[e], s_next[s]
-  for (int s = tid; s < S; s += 256) {
-    const int e = L.se[s];
-    int nx = -1;
-    if (e >= 0 && e < E) {
-      atomicMin(&first_slot[e], s);
-      for (int s2 = s + 1; s2 < S; s2++)
-        if (L.se[s2] == e) {
-          nx = s2;
-          break;
-        }
+    if (writer)
+      plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
+                           slot_offsets, row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+    else
+      plan_slots<NW, false>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
+                            slot_offsets, row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+    for (int s2 = tid; s2 < S; s2 += 256) {
+      const int ex = L.se[s2];
+      int nx = -1;
+      if (ex >= 0 && ex < E) {
+        atomicMin(&first[ex], s2);
+        for (int s3 = s2 + 1; s3 < S; s3++)
+          if (L.se[s3] == ex) {
+            nx = s3;
+            break;
+          }
+      }
+      s_next[s2] = nx;
     }
-    s_next[s] = nx;
   }
   __syncthreads();
   // own pairs: rank -> slot -> row
-  if (tid < kFusedChunk) {
-    const int p = base + tid;
+  if (tid < kPlaceChunk) {
     int row = -1;
-    const int e = own_e;
-    if (e >= 0 && e < E) {
-      const int r = n_before[e] + s_rank[tid];
-      for (int s = first_slot[e]; s >= 0 && s < S; s = s_next[s])
-        if (r >= L.lo[s] && r < L.lo[s] + L.c[s]) {
-          row = L.off[s] + (r - L.lo[s]);
+    if (own_e >= 0) {
+      const int r = n_before[own_e] + own_rk;
+      for (int s2 = first[own_e]; s2 >= 0 && s2 < S; s2 = s_next[s2])
+        if (r >= L.lo[s2] && r < L.lo[s2] + L.c[s2]) {
+          row = L.off[s2] + (r - L.lo[s2]);
           break;
         }
+      if (row >= row_cap) row = -1;  // defensive: never index past the buffers
     }
     if (p < P) {
       pair_row[p] = row;
@@ -371,10 +481,15 @@ __global__ __launch_bounds__(256) void k_dispatch_fused(
     if (lane == 0) s_nplaced = __popcll(m);
   }
   __syncthreads();
-  // gather the placed rows: one wavefront per row, every load of a row in flight
   const int R = s_nplaced;
   const int nch = H * ESIZE / 16;
-  for (int j = w; j < R; j += NW) {
+  for (int j = w; j < R; j += 4) {
+    if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
+      const int ns = H / 128;
+      for (int i = lane; i < ns; i += 64)
+        x_perm_scale[(size_t)i * row_cap + s_prow[j]] = x_scale[(size_t)s_ptok[j] * ns + i];
+    }
+    if (!gather_rows) continue;
     const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x) + (size_t)s_ptok[j] * nch;
     uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm) + (size_t)s_prow[j] * nch;
     constexpr int U = 8;
@@ -386,158 +501,6 @@ __global__ __launch_bounds__(256) void k_dispatch_fused(
       for (int u = 0; u < U; u++)
         if (c0 + u * 64 < nch) dst[c0 + u * 64] = v[u];
     }
-    if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
-      const int ns = H / 128;
-      for (int i = lane; i < ns; i += 64)
-        x_perm_scale[(size_t)i * row_cap + s_prow[j]] = x_scale[(size_t)s_ptok[j] * ns + i];
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// large batches
-// ---------------------------------------------------------------------------
-
-__global__ __launch_bounds__(kCountThreads) void k_count(const int32_t* __restrict__ ids, int Pv, int E, int ebits,
-                                                          int32_t* __restrict__ blk_hist,
-                                                          uint32_t* __restrict__ blk_err,
-                                                          int32_t* __restrict__ local_rank) {
-  constexpr int NW = kCountThreads / 64;
-  extern __shared__ int32_t sm[];  // run[E] then wc[NW][E]
-  int32_t* run = sm;
-  int32_t* wc = sm + E;
-  const int tid = threadIdx.x;
-  for (int i = tid; i < (NW + 1) * E; i += kCountThreads) sm[i] = 0;
-  __syncthreads();
-  int bad = 0;
-  const int base = blockIdx.x * kCountChunk;
-  for (int r = 0; r < kCountChunk / kCountThreads; r++) {
-    const int p = base + r * kCountThreads + tid;
-    int e = -1;
-    if (p < Pv) {
-      const int id = ids[p];
-      if (id >= 0 && id < E) e = id;
-      else if (id != -1) bad = 1;
-    }
-    const int rk = rank_round<NW>(e, E, ebits, run, wc);
-    if (e >= 0) local_rank[p] = rk;
-  }
-  for (int x = tid; x < E; x += kCountThreads) blk_hist[(size_t)blockIdx.x * E + x] = run[x];
-  const int any_bad = __syncthreads_or(bad);
-  if (tid == 0) blk_err[blockIdx.x] = any_bad ? TEMPO_DERR_BAD_ID : 0u;
-}
-
-__global__ __launch_bounds__(1024) void k_plan(int nblk, int E, int S, int M, int timing, int32_t* __restrict__ blk_hist,
-                                               const uint32_t* __restrict__ blk_err,
-                                               const int32_t* __restrict__ slot_expert,
-                                               const uint32_t* __restrict__ slot_weight,
-                                               const uint32_t* __restrict__ remote_weight,
-                                               const int32_t* __restrict__ remote_replicas,
-                                               int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts,
-                                               int32_t* __restrict__ slot_counts, int32_t* __restrict__ slot_offsets,
-                                               int32_t* __restrict__ row_token, int32_t* __restrict__ slot_lo,
-                                               uint64_t* __restrict__ t0, uint64_t* __restrict__ t1,
-                                               uint32_t* __restrict__ hdr) {
-  constexpr int NW = 16;
-  __shared__ int32_t s_n[kMaxE];
-  __shared__ SlotLds L;
-  __shared__ uint32_t s_w[kMaxS];
-  __shared__ int s_tmp[64];
-  __shared__ uint32_t s_err;
-  const int tid = threadIdx.x;
-  if (tid == 0) s_err = 0;
-  __syncthreads();
-  uint32_t eb = 0;
-  for (int b = tid; b < nblk; b += 1024) eb |= blk_err[b];
-  if (eb) atomicOr(&s_err, eb);
-  // n_e and the exclusive prefix of the block counts, in place; the loads of
-  // one expert's column are independent and issued back to back
-  for (int e = tid; e < E; e += 1024) {
-    int acc = 0;
-    int b = 0;
-    for (; b + 8 <= nblk; b += 8) {
-      int v[8];
-#pragma unroll
-      for (int u = 0; u < 8; u++) v[u] = blk_hist[(size_t)(b + u) * E + e];
-#pragma unroll
-      for (int u = 0; u < 8; u++) {
-        blk_hist[(size_t)(b + u) * E + e] = acc;
-        acc += v[u];
-      }
-    }
-    for (; b < nblk; b++) {
-      const size_t i = (size_t)b * E + e;
-      const int v = blk_hist[i];
-      blk_hist[i] = acc;
-      acc += v;
-    }
-    s_n[e] = acc;
-    expert_counts[e] = acc;
-    if (cum_counts) cum_counts[e] = cum_counts[e] + (uint32_t)acc;
-  }
-  __syncthreads();
-  plan_slots<NW, true>(s_n, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts, slot_offsets,
-                 row_token, slot_lo, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
-}
-
-__global__ __launch_bounds__(256) void k_scatter(const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S,
-                                                 const int32_t* __restrict__ blk_prefix,
-                                                 const int32_t* __restrict__ local_rank,
-                                                 const int32_t* __restrict__ slot_expert,
-                                                 const int32_t* __restrict__ slot_lo,
-                                                 const int32_t* __restrict__ slot_counts,
-                                                 const int32_t* __restrict__ slot_offsets,
-                                                 int32_t* __restrict__ pair_row, int32_t* __restrict__ row_token) {
-  __shared__ SlotLds L;
-  const int tid = threadIdx.x;
-  for (int s = tid; s < S; s += 256) {
-    L.se[s] = slot_expert[s];
-    L.lo[s] = slot_lo[s];
-    L.c[s] = slot_counts[s];
-    L.off[s] = slot_offsets[s];
-  }
-  __syncthreads();
-  const int p = blockIdx.x * 256 + tid;
-  if (p >= P) return;
-  int row = -1;
-  if (p < Pv) {
-    const int e = ids[p];
-    if (e >= 0 && e < E) row = row_of(L, S, e, blk_prefix[(size_t)(p / kCountChunk) * E + e] + local_rank[p]);
-  }
-  pair_row[p] = row;
-  if (row >= 0) row_token[row] = p / K;
-}
-
-// ---------------------------------------------------------------------------
-// row copy: one wavefront per pair
-// ---------------------------------------------------------------------------
-
-template <int ESIZE>
-__global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair_row, int P, int K, int H,
-                                                const uint8_t* __restrict__ x, const float* __restrict__ x_scale,
-                                                uint8_t* __restrict__ x_perm, float* __restrict__ x_perm_scale,
-                                                int row_cap) {
-  const int lane = threadIdx.x & 63;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (p >= P) return;
-  const int row = pair_row[p];
-  if (row < 0) return;
-  const int t = p / K;
-  const int nch = H * ESIZE / 16;
-  const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x + (size_t)t * H * ESIZE);
-  uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm + (size_t)row * H * ESIZE);
-  constexpr int U = 8;
-  for (int i0 = lane; i0 < nch; i0 += 64 * U) {
-    uint4 v[U];
-#pragma unroll
-    for (int u = 0; u < U; u++) v[u] = src[min(i0 + u * 64, nch - 1)];
-#pragma unroll
-    for (int u = 0; u < U; u++)
-      if (i0 + u * 64 < nch) dst[i0 + u * 64] = v[u];
-  }
-  if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
-    const int ns = H / 128;
-    for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)i * row_cap + row] = x_scale[(size_t)t * ns + i];
   }
 }
 
@@ -545,52 +508,33 @@ __global__ __launch_bounds__(256) void k_gather(const int32_t* __restrict__ pair
 
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids, const void* x,
                            const float* x_scale, const tempo_dispatch_out& out, char* ws, const Layout& L,
-                           bool timing, hipStream_t st) {
+                           bool timing, bool gather_rows, hipStream_t st) {
   const int P = s.T * s.K, Pv = s.T_valid * s.K;
   int ebits = 0;
   while ((1 << ebits) < s.E) ebits++;
   int32_t* blk_hist = reinterpret_cast<int32_t*>(ws + L.blk_hist);
   uint32_t* blk_err = reinterpret_cast<uint32_t*>(ws + L.blk_err);
   int32_t* local_rank = reinterpret_cast<int32_t*>(ws + L.local_rank);
-  int32_t* slot_lo = reinterpret_cast<int32_t*>(ws + L.slot_lo);
   uint64_t* t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
-  if (P <= kSmallMaxPairs && s.S <= 256) {
-    const size_t lds = (size_t)5 * s.E * sizeof(int32_t);
-    const int nb = ceil_div(P, kFusedChunk);
-    if (s.dtype == TEMPO_BF16)
-      hipLaunchKernelGGL(k_dispatch_fused<2>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
-                         s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
-                         out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
-                         out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
-                         out.x_perm_scale, L.row_cap, hdr, timing ? 1 : 0, t0, t1);
-    else
-      hipLaunchKernelGGL(k_dispatch_fused<1>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, ebits, s.S,
-                         s.m_tile, s.H, plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas,
-                         out.expert_counts, out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token,
-                         out.pair_row, static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm),
-                         out.x_perm_scale, L.row_cap, hdr, timing ? 1 : 0, t0, t1);
-    return hipGetLastError();
-  }
   hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t), st,
                      topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(1024), 0, st, L.nblk, s.E, s.S, s.m_tile, timing ? 1 : 0, blk_hist, blk_err,
-                     plan.slot_expert, plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts,
-                     out.cum_counts, out.slot_counts, out.slot_offsets, out.row_token, slot_lo, t0, t1, hdr);
-  hipLaunchKernelGGL(k_scatter, dim3(ceil_div(P, 256)), dim3(256), 0, st, topk_ids, P, Pv, s.K, s.E, s.S, blk_hist,
-                     local_rank, plan.slot_expert, slot_lo, out.slot_counts, out.slot_offsets, out.pair_row,
-                     out.row_token);
-  const int nb = ceil_div(P, 4);
+  const int nb = ceil_div(P, kPlaceChunk);
+  const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
   if (s.dtype == TEMPO_BF16)
-    hipLaunchKernelGGL(k_gather<2>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
-                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale,
-                       L.row_cap);
+    hipLaunchKernelGGL(k_place<2>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H,
+                       L.row_cap, L.nblk, gather_rows ? 1 : 0, blk_hist, blk_err, local_rank, plan.slot_expert,
+                       plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
+                       out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),
+                       x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
   else
-    hipLaunchKernelGGL(k_gather<1>, dim3(nb), dim3(256), 0, st, out.pair_row, P, s.K, s.H,
-                       static_cast<const uint8_t*>(x), x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale,
-                       L.row_cap);
+    hipLaunchKernelGGL(k_place<1>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H,
+                       L.row_cap, L.nblk, gather_rows ? 1 : 0, blk_hist, blk_err, local_rank, plan.slot_expert,
+                       plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
+                       out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),
+                       x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
   return hipGetLastError();
 }
 

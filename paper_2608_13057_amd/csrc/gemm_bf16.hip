@@ -57,7 +57,8 @@ template <int BM, bool GATEUP>
 __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
                                                       size_t w_slot_stride, uint16_t* __restrict__ C,
                                                       const int32_t* __restrict__ slot_counts,
-                                                      const int32_t* __restrict__ slot_offsets, int S, int Kd,
+                                                      const int32_t* __restrict__ slot_offsets,
+                                                      const int32_t* __restrict__ row_src, int S, int Kd,
                                                       int Nout, int max_tiles,
                                                       const uint32_t* __restrict__ hdr, uint64_t* __restrict__ t0,
                                                       uint64_t* __restrict__ t1, int timing) {
@@ -108,7 +109,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
 #pragma unroll
     for (int j = 0; j < AG; j++) {
       const int g = wave + 4 * j, r = g * 8 + lrow;
-      srcA[j] = A + (size_t)(row0 + r) * Kd + gchunk * 8;
+      // A row: the permuted row itself, or the source row it was routed from
+      int ar = row0 + r;
+      if (row_src) ar = (g * 8 < nvalid) ? max(row_src[row0 + min(r, nvalid - 1)], 0) : 0;
+      srcA[j] = A + (size_t)ar * Kd + gchunk * 8;
       nA += (g * 8 < nvalid) ? 1 : 0;
     }
     // packed weights: the item's tiles are contiguous 16 KB blocks, one per
@@ -214,7 +218,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
 
 template <int BM>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                     void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid, hipStream_t st) {
+                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                     hipStream_t st) {
   const uint32_t* hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
   uint64_t* t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
@@ -222,22 +227,23 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   const int grid = persistent_grid(1);
   const int max_tiles = L.row_cap / BM;
   hipLaunchKernelGGL((k_gemm_bf16<BM, true>), dim3(grid), dim3(256), 0, st,
-                     static_cast<const uint16_t*>(d.x_perm), static_cast<const uint16_t*>(w.w13),
-                     (size_t)2 * s.I * s.H, h, d.slot_counts, d.slot_offsets, s.S, s.H, s.I, max_tiles, hdr, t0, t1,
-                     timing ? 1 : 0);
+                     static_cast<const uint16_t*>(x_rows ? x_rows : d.x_perm), static_cast<const uint16_t*>(w.w13),
+                     (size_t)2 * s.I * s.H, h, d.slot_counts, d.slot_offsets, x_rows ? d.row_token : nullptr, s.S, s.H,
+                     s.I, max_tiles, hdr, t0, t1, timing ? 1 : 0);
   if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_gemm_bf16<BM, false>), dim3(grid), dim3(256), 0, st, h,
                      static_cast<const uint16_t*>(w.w2), (size_t)s.H * s.I, static_cast<uint16_t*>(y_perm),
-                     d.slot_counts, d.slot_offsets, s.S, s.I, s.H, max_tiles, hdr, t0, t1, timing ? 1 : 0);
+                     d.slot_counts, d.slot_offsets, nullptr, s.S, s.I, s.H, max_tiles, hdr, t0, t1, timing ? 1 : 0);
   return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                               void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid, hipStream_t st) {
-  if (s.m_tile == 128) return launch_bm<128>(s, d, w, y_perm, ws, L, timing, mid, st);
-  if (s.m_tile == 64) return launch_bm<64>(s, d, w, y_perm, ws, L, timing, mid, st);
+                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                               hipStream_t st) {
+  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
+  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
   return hipErrorInvalidValue;
 }
 

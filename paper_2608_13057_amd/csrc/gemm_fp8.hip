@@ -34,7 +34,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(const uint8_t* __restrict__
                                                      size_t w_slot_stride, const float* __restrict__ Ws,
                                                      int ws_rows, float* __restrict__ Cf, uint16_t* __restrict__ Cb,
                                                      const int32_t* __restrict__ slot_counts,
-                                                     const int32_t* __restrict__ slot_offsets, int S, int Kd,
+                                                     const int32_t* __restrict__ slot_offsets,
+                                                     const int32_t* __restrict__ row_src, int S, int Kd,
                                                      int Nout, int max_tiles, const uint32_t* __restrict__ hdr,
                                                      uint64_t* __restrict__ t0, uint64_t* __restrict__ t1,
                                                      int timing) {
@@ -82,7 +83,10 @@ __global__ __launch_bounds__(256, 1) void k_gemm_fp8(const uint8_t* __restrict__
 #pragma unroll
     for (int j = 0; j < AG; j++) {
       const int g = wave + 4 * j, r = g * 8 + lrow;
-      srcA[j] = A + (size_t)(row0 + r) * Kd + gchunk * 16;
+      // A row: the permuted row itself, or the source row it was routed from
+      int ar = row0 + r;
+      if (row_src) ar = (g * 8 < nvalid) ? max(row_src[row0 + min(r, nvalid - 1)], 0) : 0;
+      srcA[j] = A + (size_t)ar * Kd + gchunk * 16;
       nA += (g * 8 < nvalid) ? 1 : 0;
     }
 #pragma unroll
@@ -249,7 +253,8 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
 
 template <int BM>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                     void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid, hipStream_t st) {
+                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                     hipStream_t st) {
   const uint32_t* hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
   uint64_t* t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
@@ -258,17 +263,18 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   float* hs = reinterpret_cast<float*>(ws + L.h_scale);
   const int grid = persistent_grid(1);
   const int max_tiles = L.row_cap / BM;
-  hipLaunchKernelGGL((k_gemm_fp8<BM, true>), dim3(grid), dim3(256), 0, st, static_cast<const uint8_t*>(d.x_perm),
-                     d.x_perm_scale, L.row_cap, static_cast<const uint8_t*>(w.w13), (size_t)2 * s.I * s.H,
-                     w.w13_scale, 2 * s.I / 128, h32, nullptr, d.slot_counts, d.slot_offsets, s.S, s.H, s.I,
-                     max_tiles, hdr, t0, t1, timing ? 1 : 0);
+  hipLaunchKernelGGL((k_gemm_fp8<BM, true>), dim3(grid), dim3(256), 0, st,
+                     static_cast<const uint8_t*>(x_rows ? x_rows : d.x_perm), d.x_perm_scale, L.row_cap,
+                     static_cast<const uint8_t*>(w.w13), (size_t)2 * s.I * s.H, w.w13_scale, 2 * s.I / 128, h32,
+                     nullptr, d.slot_counts, d.slot_offsets, x_rows ? d.row_token : nullptr, s.S, s.H, s.I, max_tiles,
+                     hdr, t0, t1, timing ? 1 : 0);
   hipLaunchKernelGGL(k_quant_h, dim3(ceil_div(L.row_cap, 4)), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
   if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_gemm_fp8<BM, false>), dim3(grid), dim3(256), 0, st, h8, hs, L.row_cap,
                      static_cast<const uint8_t*>(w.w2), (size_t)s.H * s.I, w.w2_scale, s.H / 128, nullptr,
-                     static_cast<uint16_t*>(y_perm), d.slot_counts, d.slot_offsets, s.S, s.I, s.H, max_tiles, hdr, t0,
-                     t1, timing ? 1 : 0);
+                     static_cast<uint16_t*>(y_perm), d.slot_counts, d.slot_offsets, nullptr, s.S, s.I, s.H, max_tiles,
+                     hdr, t0, t1, timing ? 1 : 0);
   return hipGetLastError();
 }
 
@@ -280,9 +286,10 @@ bool experts_supported(const tempo_moe_shape& s) {
 }
 
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid, hipStream_t st) {
-  if (s.m_tile == 128) return launch_bm<128>(s, d, w, y_perm, ws, L, timing, mid, st);
-  if (s.m_tile == 64) return launch_bm<64>(s, d, w, y_perm, ws, L, timing, mid, st);
+                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                              hipStream_t st) {
+  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
+  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
   return hipErrorInvalidValue;
 }
 

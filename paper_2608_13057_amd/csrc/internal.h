@@ -10,9 +10,8 @@
 
 namespace tempo {
 
-// Pairs handled by one block of the counting kernel (and the granularity of
-// the per-block histograms).
-constexpr int kCountChunk = 1024;
+// Pairs handled by one block of the counting kernel (one pair per thread; the
+// granularity of the per-block histograms).
 constexpr int kCountThreads = 256;
 
 constexpr int kMaxE = 1024;
@@ -51,18 +50,22 @@ Layout make_layout(const tempo_moe_shape& s);
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---- launchers (stream-ordered, no synchronisation) ----
+// gather_rows = false leaves x_perm unwritten (stage 2 then gathers through
+// row_token; x_perm_scale is still written for fp8).
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids,
                            const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
-                           const Layout& L, bool timing, hipStream_t st);
+                           const Layout& L, bool timing, bool gather_rows, hipStream_t st);
 
 // mid_event (nullable) is recorded between the gate/up and the down GEMM.
+// x_rows: null -> the gate/up GEMM reads d.x_perm; otherwise it reads the
+// activation rows x_rows[row_token[row]] (x_rows = the unpermuted x).
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                               void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid_event,
-                               hipStream_t st);
+                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                               hipEvent_t mid_event, hipStream_t st);
 
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid_event,
-                              hipStream_t st);
+                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                              hipEvent_t mid_event, hipStream_t st);
 
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
