@@ -96,8 +96,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
     const int tile = it / my_nb;
     const int nb = nb_lo + it % my_nb;
     const int row0 = tile * BM;
-    const int slot = slot_of_row(s_off, S, row0);
-    const int nvalid = min(BM, s_off[slot] + s_cnt[slot] - row0);
+    // per-item control values are wave-uniform: keep them in scalar registers
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, S, row0));
+    const int nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
     uint64_t tstart = 0;
     if (timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
 
@@ -122,7 +123,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
       const int g = wave + 4 * j;
       srcB[j] = Wsl + ((size_t)nb * KT * BNW * BK) + g * 8 * BK + lane * 8;
     }
-    const int L = BG + nA;  // load instructions per stage for this wavefront
+    const int L = __builtin_amdgcn_readfirstlane(BG + nA);  // load instructions per stage for this wavefront
     // ring geometry of this item: a stage holds the activation groups that
     // have a real row, then the 16 KB weight tile; the fewer real rows, the
     // more stages fit and the more weight bytes are in flight
@@ -130,7 +131,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
     const int A_BYTES = a_groups * 8 * ROWB;
     const int STAGE = A_BYTES + B_BYTES;
     const int NS = min(NS_MAX, RING_BYTES / STAGE);
-    const int mi_live = (nvalid - wm * (BM / 2) + 31) >> 5;  // this wavefront's 32-row blocks with a real row
+    // this wavefront's 32-row blocks with a real row
+    const int mi_live = __builtin_amdgcn_readfirstlane((nvalid - wm * (BM / 2) + 31) >> 5);
 
     auto issue = [&](int kt) {
       char* st = ring + (kt % NS) * STAGE;
@@ -164,27 +166,31 @@ __global__ __launch_bounds__(256, 1) void k_gemm_bf16(const uint16_t* __restrict
       barrier_nofence();
       if (kt + NS - 1 < KT) issue(kt + NS - 1);
       const char* st = ring + (kt % NS) * STAGE;
+      // every fragment of the stage is requested before the first MFMA
+      constexpr int KS = BK / 16;
+      bf16x8 a[KS][MI], b[KS][2];
 #pragma unroll
-      for (int ks = 0; ks < BK / 16; ks++) {
+      for (int ks = 0; ks < KS; ks++) {
         const int c = 2 * ks + (lane >> 5);
-        bf16x8 a[MI], b[2];
-#pragma unroll
-        for (int mi = 0; mi < MI; mi++) {
-          const int r = wm * (BM / 2) + mi * 32 + (lane & 31);
-          if (mi < mi_live) a[mi] = *reinterpret_cast<const bf16x8*>(st + swz(r, c));
-        }
 #pragma unroll
         for (int j = 0; j < 2; j++) {
           const int r = (GATEUP ? (j * 64 + wn * 32) : (wn * 64 + j * 32)) + (lane & 31);
-          b[j] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + swz(r, c));
+          b[ks][j] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + swz(r, c));
         }
+#pragma unroll
+        for (int mi = 0; mi < MI; mi++) {
+          const int r = wm * (BM / 2) + mi * 32 + (lane & 31);
+          if (mi < mi_live) a[ks][mi] = *reinterpret_cast<const bf16x8*>(st + swz(r, c));
+        }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ks++)
 #pragma unroll
         for (int mi = 0; mi < MI; mi++)
           if (mi < mi_live)
 #pragma unroll
             for (int j = 0; j < 2; j++)
-              acc[mi][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi], b[j], acc[mi][j], 0, 0, 0);
-      }
+              acc[mi][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][mi], b[ks][j], acc[mi][j], 0, 0, 0);
     }
 
     // epilogue
