@@ -145,9 +145,14 @@ typedef struct tempo_dispatch_out {
  *   w13_scale [S, 2I/128, H/128] fp32, fp8 only
  *   w2        [S, H, I]   down projection
  *   w2_scale  [S, H/128, I/128] fp32, fp8 only
- * tempo_moe_experts / tempo_moe_forward take w13 and w2 in the packed layout
- * written by tempo_moe_pack_weights (same sizes; the scales keep the natural
- * layout).
+ * tempo_moe_experts / tempo_moe_forward take the packed layout written by
+ * tempo_moe_pack_weights: w13 and w2 of the same sizes, and (fp8) packed
+ * scales of 4 fp32 words per (output block, 128-element contraction step):
+ *   w13_scale packed [S, I/64, H/128, 4]: {gate-row block scale, up-row block
+ *             scale, 0, 0} of the output block pairing gate rows 64n..64n+63
+ *             with up rows I+64n..I+64n+63
+ *   w2_scale  packed [S, H/128, I/128, 4]: {block scale, 0, 0, 0}
+ * All device buffers must be 16-byte aligned.
  */
 typedef struct tempo_expert_weights {
   const void* w13;
@@ -174,9 +179,12 @@ int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32
  * every (output block of 128 weight rows, contraction step of 128 bytes)
  * tile of a slot is one contiguous 16 KB block and the tiles of an output
  * block follow each other along the contraction, so stage 2 streams each
- * activated slot's weights front to back.  For w13 an output block holds 64
- * gate rows and the same 64 up rows.  Scale pointers are ignored.  Returns
- * TEMPO_EINVAL for null or aliasing buffers.
+ * activated slot's weights front to back.  For w13 output block n holds gate
+ * rows 64n..64n+63 and the same up rows, interleaved in groups of 16 rows
+ * (gate 64n..64n+15, up I+64n..I+64n+15, gate 64n+16.., ...).  fp8: packed->w13_scale / w2_scale are
+ * caller buffers of the packed scale sizes above that receive the packed
+ * scales (bf16: scale pointers are ignored).  Returns TEMPO_EINVAL for null
+ * or aliasing buffers.
  */
 int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weights* natural,
                            const tempo_expert_weights* packed, void* stream);

@@ -23,6 +23,9 @@ FLAGS = [
     "-fPIC",
     # no packed-fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in VGPRs: the stage-2 GEMMs add chunk accumulators
+    # with VALU, and the AGPR form would copy them back and forth every step
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-result",
 ]
 

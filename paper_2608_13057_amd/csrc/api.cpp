@@ -30,8 +30,6 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + (size_t)L.nblk * 4);
   L.local_rank = o;
   o = align_up(o + P * 4);
-  L.slot_lo = o;
-  o = align_up(o + (size_t)s.S * 4);
 
   L.slot_t0 = o;
   o = align_up(o + (size_t)s.S * 8);
@@ -45,6 +43,12 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + (s.dtype == TEMPO_BF16 ? 0 : (size_t)L.row_cap * s.I * 4));
   L.y_perm = o;
   o = align_up(o + (size_t)L.row_cap * s.H * 2);
+  // stage-2 partial tiles: per workgroup of the persistent grid, 8 tiles of
+  // m_tile x 128 fp32 (the running sum and the chunks of split work items)
+  L.part = o;
+  o = align_up(o + (size_t)persistent_grid(1) * 8 * s.m_tile * 128 * 4);
+  L.fix = o;  // per workgroup: the split work item it completes (12 int32)
+  o = align_up(o + (size_t)persistent_grid(1) * 12 * 4);
   L.total = o;
   return L;
 }
@@ -119,6 +123,9 @@ int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weig
   int rc = check_shape(shape);
   if (rc) return rc;
   if (!natural || !packed || !natural->w13 || !natural->w2 || !packed->w13 || !packed->w2) return TEMPO_EINVAL;
+  if (shape->dtype == TEMPO_FP8_E4M3 &&
+      (!natural->w13_scale || !natural->w2_scale || !packed->w13_scale || !packed->w2_scale))
+    return TEMPO_EINVAL;
   const size_t es = shape->dtype == TEMPO_BF16 ? 2 : 1;
   const size_t b13 = (size_t)shape->S * 2 * shape->I * shape->H * es, b2 = (size_t)shape->S * shape->H * shape->I * es;
   auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
@@ -129,6 +136,19 @@ int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weig
       overlap(natural->w13, b13, packed->w2, b2) || overlap(natural->w2, b2, packed->w13, b13) ||
       overlap(packed->w13, b13, packed->w2, b2))
     return TEMPO_EINVAL;
+  if (shape->dtype == TEMPO_FP8_E4M3) {
+    const size_t kb = shape->H / 128, ib = shape->I / 128;
+    const size_t n13 = (size_t)shape->S * 2 * ib * kb * 4, n2 = (size_t)shape->S * kb * ib * 4;
+    const size_t p13 = (size_t)shape->S * (shape->I / 64) * kb * 16, p2 = (size_t)shape->S * kb * ib * 16;
+    const void* ns[2] = {natural->w13_scale, natural->w2_scale};
+    const size_t nn[2] = {n13, n2};
+    const void* ps[2] = {packed->w13_scale, packed->w2_scale};
+    const size_t pn[2] = {p13, p2};
+    if (overlap(ps[0], pn[0], ps[1], pn[1])) return TEMPO_EINVAL;
+    for (int i = 0; i < 2; i++)
+      for (int j = 0; j < 2; j++)
+        if (overlap(ps[i], pn[i], ns[j], nn[j])) return TEMPO_EINVAL;
+  }
   return dev_status(launch_pack(*shape, *natural, *packed, static_cast<hipStream_t>(stream)));
 }
 
@@ -195,11 +215,15 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   auto mark = [&](int i) { return !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!mark(0)) return TEMPO_EDEVICE;
-  // the gate/up GEMM gathers the activation rows itself; x_perm stays unwritten
-  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, false, st);
+  // decode-sized batches: the gate/up GEMM gathers the activation rows itself
+  // and x_perm stays unwritten; otherwise stage 1 permutes them into x_perm
+  const bool gemm_gathers = experts_gather_rows(*shape, L);
+  const void* x_rows = gemm_gathers ? x : nullptr;
+  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, !gemm_gathers, st);
   if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
-  e = shape->dtype == TEMPO_BF16 ? launch_experts_bf16(*shape, *disp, *weights, x, y_perm, ws, L, timing, ev[2], st)
-                                 : launch_experts_fp8(*shape, *disp, *weights, x, y_perm, ws, L, timing, ev[2], st);
+  e = shape->dtype == TEMPO_BF16
+          ? launch_experts_bf16(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev[2], st)
+          : launch_experts_fp8(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev[2], st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   if (e != hipSuccess || !mark(3)) return TEMPO_EDEVICE;
   e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,

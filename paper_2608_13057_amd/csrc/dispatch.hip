@@ -128,7 +128,7 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t*
                            const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                            const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ slot_counts,
                            int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
-                           int32_t* __restrict__ slot_lo_out, uint32_t* __restrict__ hdr, SlotLds& L, uint32_t* s_err,
+                           uint32_t* __restrict__ hdr, SlotLds& L, uint32_t* s_err,
                            uint32_t* s_w, int* s_tmp, int timing, uint64_t* __restrict__ t0,
                            uint64_t* __restrict__ t1) {
   const int tid = threadIdx.x, bd = NW * 64;
@@ -177,10 +177,7 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t*
     }
     L.c[s] = c;
     L.lo[s] = lo;
-    if (WRITE) {
-      slot_counts[s] = c;
-      if (slot_lo_out) slot_lo_out[s] = lo;
-    }
+    if (WRITE) slot_counts[s] = c;
     P = (c + M - 1) / M * M;
   }
   int total = 0;
@@ -437,10 +434,10 @@ __global__ __launch_bounds__(256) void k_place(
   } else {
     if (writer)
       plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
-                           slot_offsets, row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+                           slot_offsets, row_token, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
     else
       plan_slots<NW, false>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
-                            slot_offsets, row_token, nullptr, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
+                            slot_offsets, row_token, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
     for (int s2 = tid; s2 < S; s2 += 256) {
       const int ex = L.se[s2];
       int nx = -1;

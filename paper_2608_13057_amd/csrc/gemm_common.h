@@ -71,6 +71,26 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, const void* lds_base
       : "memory", "m0");
 }
 
+// The same DMA with a uniform 64-bit base in scalar registers and a 32-bit
+// per-lane byte offset (global address = sbase + voff): the base of a stream
+// advances with two scalar adds per step instead of a 64-bit add per lane.
+__device__ __forceinline__ void lds_dma16s(const void* sbase, uint32_t voff, uint32_t lds_addr) {
+  const uint64_t b = (uint64_t)(uintptr_t)sbase;
+  const uint64_t bu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32) |
+                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
+  asm volatile(
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %0, %1" ::"v"(voff),
+      "s"(bu), "s"(l)
+      : "memory", "m0");
+}
+
+// LDS byte address of a shared-memory pointer (the low 32 bits of its
+// generic address).
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
 // Byte offset of 16-byte chunk c of row r in a swizzled tile (chunk c of a
 // row is stored at position c ^ (r & 7), so 8 consecutive rows read at the
 // same chunk hit 8 distinct bank groups).

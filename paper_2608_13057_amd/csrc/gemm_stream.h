@@ -1,0 +1,642 @@
+// Stage 2 grouped GEMM (bf16 and fp8 e4m3), the expert FFN of the activated
+// slots over their M-tile-padded row groups (Sec. 2.1 gate/up, activation,
+// down; Sec. 2.2: an activated replica costs the streaming of its weights,
+// each further M-tile of rows re-uses them).
+//
+//   gate/up:  h = silu(A W_gate^T) * (A W_up^T)       A = the slot's rows of x
+//   down:     y_perm = h W2^T
+//
+// Work decomposition (stream-K over fixed contraction chunks).  A work item
+// is one (M-tile, output block of 128 weight rows) pair; its contraction of
+// KT steps (128 bytes of every row per step) is cut into C <= 8 fixed chunks
+// of SPC steps (the last may be shorter).  The chunks of all items, item by
+// item, form one sequence that is split into equal contiguous ranges, one per
+// workgroup (one workgroup per CU), so every CU streams the same number of
+// weight bytes whatever the tile and slot counts are.  When the output blocks
+// divide by 8, workgroup b (dispatched to XCD b mod 8) only takes items of
+// the b mod 8 eighth of the output blocks, so one XCD's L2 holds each weight
+// block that several M-tiles of a slot read.
+//
+// Arithmetic is fixed per row: chunk i of an item is accumulated by MFMA from
+// zero in step order (c_i), and the result is ((c_0 + c_1) + c_2) + ... in
+// fp32.  A workgroup that holds an item from chunk 0 keeps that running sum in
+// registers; if its range ends inside the item it writes the running sum to a
+// partial tile, and the workgroups holding the next chunks write each c_i to
+// a partial tile of their own.  A fixup kernel then adds the chunks in order
+// and applies the epilogue.  Results therefore do not depend on where the
+// range boundaries fall, on the plan, or on the tile a row lands in.
+//
+// Memory pipeline.  Operand tiles go from global memory straight into an LDS
+// ring with global_load_lds_dwordx4 (no registers involved).  The pipeline
+// never drains between work items: a stage holds the activation row groups
+// of its item that have a real row, the 16 KB weight tile, and (fp8) the
+// step's activation and weight scales, so stages differ in size; they are
+// placed back to back in the ring (a stage that would straddle the end starts
+// at offset 0) and up to 7 are in flight ahead of the one being multiplied,
+// as many as the ring holds.  The issuing side records, per stage, where it
+// lies and what it closes (a chunk, a piece of an item) in a small descriptor
+// ring in LDS, and per wavefront how many loads it had issued; each
+// wavefront waits only until its own loads of the stage are done (vmcnt),
+// then a workgroup barrier makes everyone's data visible and frees the
+// previous stage.  When stage 1 left the rows in token order (the gate/up
+// GEMM then gathers rows itself), the source rows of the M-tiles of the range
+// (their row tables) are loaded into LDS before the stream starts.
+//
+// Compute.  BM x 128 tile per item; wavefront w multiplies all real row
+// blocks of 32 by the item's weight rows 32w..32w+31, so the MFMA work is
+// spread over the four SIMDs even for a decode tile of a few rows.  For
+// gate/up the packed layout interleaves 16 gate rows and the same 16 up rows
+// in every 32, so a wavefront holds matching gate and up columns (lanes l and
+// l + 16) for SwiGLU.  bf16: 32x32x16 MFMA, 4 per stage and row block;
+// fp8: two 32x32x64 f8f6f4 MFMA per stage into a stage partial p that is
+// added as acc += p * (sA[row] * sW).  Lane layout of the 32x32 MFMA family
+// on gfx950: A row / B column = lane % 32, consecutive contraction elements
+// per lane; accumulator element i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
+// column l % 32.
+#pragma once
+
+#include <type_traits>
+
+#include "gemm_common.h"
+
+namespace tempo {
+namespace gemm {
+
+constexpr int NQ = 8;           // ring slots at most (the one being multiplied + the ones in flight)
+constexpr int NROWT = 16;       // row tables (M-tiles) per workgroup range for the in-GEMM gather
+constexpr int CMAX = 8;         // contraction chunks per work item (at most)
+constexpr int PART_TILE = 128;  // columns of a partial tile (the 128 weight rows of an item)
+// fixup record of a GEMM workgroup: source count (-1: nothing to complete),
+// row0, output block, real rows, then the partial tiles (global tile index)
+// holding chunks q1.. of the item in chunk order
+constexpr int FIX_WORDS = 4 + CMAX;
+
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(8 * sizeof(int)))) int i32x8;
+typedef __attribute__((__vector_size__(4 * sizeof(int)))) int i32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+
+struct GemmArgs {
+  const char* A;            // activation rows (row_src == null: permuted rows; else token rows)
+  const int32_t* row_src;   // null, or [row_cap] token of each permuted row (-1 = padding)
+  const float* As;          // fp8: activation scales, block-major [Kd/128][as_ld]
+  int as_ld;
+  const char* W;            // packed weights (tempo_moe_pack_weights)
+  size_t w_slot_bytes;
+  const float* Wsp;         // fp8: packed weight scales [slot][block][step][4]
+  size_t ws_slot_floats;
+  void* C;                  // output rows [row_cap][Nout]: bf16, or fp32 (fp8 gate/up)
+  float* part;              // partial tiles [grid][CMAX][BM][128] fp32
+  int32_t* fix;             // per workgroup: the split item whose chunk 0 it holds (FIX_WORDS int32)
+  const int32_t* slot_counts;
+  const int32_t* slot_offsets;
+  int S, Kd, Nout, max_tiles;
+  const uint32_t* hdr;
+  uint64_t* t0;
+  uint64_t* t1;
+  int timing;
+};
+
+// Work geometry; identical in the GEMM and in its fixup kernel.
+struct Geo {
+  int KT, SPC, C, SL;  // steps per item, per chunk, chunks, steps of the last chunk
+  int groups, grp, j0, wpx, my_nb, nb_lo, items;
+  int q0, q1;          // this workgroup's chunk range [q0, q1)
+};
+
+__host__ __device__ __forceinline__ int geo_groups(int NB, int grid) { return (NB % 8 == 0 && grid % 8 == 0) ? 8 : 1; }
+
+// Ranges balance estimated time, not chunk counts: a chunk of an M-tile with
+// m row blocks of 32 real rows costs W_BASE + m (a step's fixed work plus its
+// MFMA and activation traffic per row block).  s_sw[s] holds the summed tile
+// weights of slots before s (s_sw[S] = all tiles).
+constexpr int W_BASE = 2;
+
+template <int BM>
+__device__ __forceinline__ int tile_weight(int rows) { return W_BASE + ((rows + 31) >> 5); }
+
+// All threads of the block; ends with a barrier.  s_off / s_cnt must be ready.
+template <int BM>
+__device__ void build_slot_weights(const int32_t* s_off, const int32_t* s_cnt, int32_t* s_sw, int S) {
+  const int tid = threadIdx.x;
+  for (int s = tid; s < S; s += blockDim.x) {
+    const int nt = (s_off[s + 1] - s_off[s]) / BM;
+    s_sw[s + 1] = nt > 0 ? (nt - 1) * tile_weight<BM>(BM) + tile_weight<BM>(s_cnt[s] - (nt - 1) * BM) : 0;
+  }
+  if (tid == 0) s_sw[0] = 0;
+  __syncthreads();
+  // inclusive scan of s_sw[1..S] (Hillis-Steele, S <= kMaxS)
+  for (int d = 1; d < S; d <<= 1) {
+    int v = 0;
+    for (int s = tid; s < S; s += blockDim.x) v = s >= d ? s_sw[s + 1 - d] : 0;
+    __syncthreads();
+    for (int s = tid; s < S; s += blockDim.x)
+      if (s >= d) s_sw[s + 1] += v;
+    __syncthreads();
+  }
+}
+
+// First chunk of workgroup j of a group: the smallest chunk q whose weight
+// prefix reaches j / wpx of the total.
+template <int BM>
+__device__ int range_lo(const Geo& g, int j, const int32_t* s_off, const int32_t* s_cnt, const int32_t* s_sw, int S) {
+  const int U = g.items * g.C;
+  if (j <= 0) return 0;
+  if (j >= g.wpx) return U;
+  const long long unit = (long long)g.my_nb * g.C;  // chunks per M-tile
+  const long long T = unit * s_sw[S] * j / g.wpx;   // target weight
+  // the first slot whose end lies beyond T
+  int lo = 0, hi = S;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (unit * s_sw[mid + 1] > T) hi = mid;
+    else lo = mid + 1;
+  }
+  if (lo == S) return U;
+  const int nt = (s_off[lo + 1] - s_off[lo]) / BM;  // >= 1
+  const long long wf = unit * tile_weight<BM>(BM);
+  const long long rem = T - unit * s_sw[lo];
+  const long long tf = min(rem / wf, (long long)(nt - 1));  // whole tiles of the slot before the target
+  const int wt = tf < nt - 1 ? tile_weight<BM>(BM) : tile_weight<BM>(s_cnt[lo] - (nt - 1) * BM);
+  const long long r = min((rem - tf * wf + wt - 1) / wt, unit);
+  const long long q = (long long)(s_off[lo] / BM + tf) * unit + r;
+  return (int)min(q, (long long)U);
+}
+
+template <int BM>
+__device__ __forceinline__ Geo make_geo(int KT, int NB, int NT, int b, int grid, const int32_t* s_off,
+                                        const int32_t* s_cnt, const int32_t* s_sw, int S) {
+  Geo g;
+  g.KT = KT;
+  g.SPC = (KT + CMAX - 1) / CMAX;
+  g.C = (KT + g.SPC - 1) / g.SPC;
+  g.SL = KT - (g.C - 1) * g.SPC;
+  g.groups = geo_groups(NB, grid);
+  g.grp = b % g.groups;
+  g.j0 = b / g.groups;
+  g.wpx = grid / g.groups;
+  g.my_nb = NB / g.groups;
+  g.nb_lo = g.grp * g.my_nb;
+  g.items = NT * g.my_nb;
+  g.q0 = range_lo<BM>(g, g.j0, s_off, s_cnt, s_sw, S);
+  g.q1 = range_lo<BM>(g, g.j0 + 1, s_off, s_cnt, s_sw, S);
+  return g;
+}
+
+__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+
+// Partial tiles are stored lane-native: the 16 accumulator values of lane l
+// of wavefront w for row block mi are 16 consecutive floats at
+// ((mi * 4 + w) * 64 + l) * 16, i.e. four 16-byte stores per lane.  (Stores
+// count in the same vmcnt as the ring's loads and may complete out of order
+// with them, so the waits do not account for them: each store instruction
+// issued makes the next waits conservative, and fewer is better.)
+__device__ __forceinline__ int part_index(int mi, int w, int l, int i) { return ((mi * 4 + w) * 64 + l) * 16 + i; }
+
+// One step of the contraction on a resident ring slot: acc[mi] += A_mi W^T for
+// the MIL row blocks with a real row (compile-time count, straight-line code).
+template <bool FP8, bool GATEUP, int BM, int MIL, typename Between>
+__device__ __forceinline__ void step_mma(const char* st, int A_BYTES, int lane, int wave, f32x16 (&acc)[MIL],
+                                         Between&& between) {
+  // Fragment reads are requested first, then the caller's work (the DMAs of
+  // a later step) runs while they land, then the MFMAs; the scheduling
+  // barriers keep that order.  A slot holds A_BYTES of activation rows, then
+  // the weight tile, then (fp8) the scales.
+  const int bcol = wave * 32 + (lane & 31);  // weight row of the tile multiplied by this lane
+  if (!FP8) {
+    constexpr int KS = 4;                    // 16-element MFMA steps per 64-element stage
+    constexpr int KA = MIL <= 2 ? KS : 2;    // sub-steps read ahead (all, or two for a full tile)
+    bf16x8 a[KS][MIL], b[KS];
+    auto load = [&](int ks) {
+      const int c = 2 * ks + (lane >> 5);
+      b[ks] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + swz(bcol, c));
+#pragma unroll
+      for (int mi = 0; mi < MIL; mi++) a[ks][mi] = *reinterpret_cast<const bf16x8*>(st + swz(mi * 32 + (lane & 31), c));
+    };
+#pragma unroll
+    for (int ks = 0; ks < KA; ks++) load(ks);
+    __builtin_amdgcn_sched_barrier(0);
+    between();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int ks = 0; ks < KS; ks++) {
+      if (ks + KA < KS) load(ks + KA);
+#pragma unroll
+      for (int mi = 0; mi < MIL; mi++) acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][mi], b[ks], acc[mi], 0, 0, 0);
+    }
+  } else {
+    const float* sa_lds = reinterpret_cast<const float*>(st + A_BYTES + B_BYTES);
+    const float* sw_lds = sa_lds + 128;
+    i32x8 b[2], a[MIL][2];
+    float4 sa4[MIL][4];
+#pragma unroll
+    for (int h = 0; h < 2; h++) {
+      const int c = 4 * h + 2 * (lane >> 5);
+      const i32x4 lo = *reinterpret_cast<const i32x4*>(st + A_BYTES + swz(bcol, c));
+      const i32x4 hi = *reinterpret_cast<const i32x4*>(st + A_BYTES + swz(bcol, c + 1));
+      b[h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+#pragma unroll
+    for (int mi = 0; mi < MIL; mi++) {
+      const int r = mi * 32 + (lane & 31);
+#pragma unroll
+      for (int h = 0; h < 2; h++) {
+        const int c = 4 * h + 2 * (lane >> 5);
+        const i32x4 lo = *reinterpret_cast<const i32x4*>(st + swz(r, c));
+        const i32x4 hi = *reinterpret_cast<const i32x4*>(st + swz(r, c + 1));
+        a[mi][h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      }
+#pragma unroll
+      for (int q = 0; q < 4; q++)
+        sa4[mi][q] = *reinterpret_cast<const float4*>(sa_lds + mi * 32 + 8 * q + 4 * (lane >> 5));
+    }
+    // gate/up: lanes with bit 4 clear hold gate columns, the others up columns
+    const float sw = GATEUP ? sw_lds[(lane >> 4) & 1] : sw_lds[0];
+    __builtin_amdgcn_sched_barrier(0);
+    between();
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int mi = 0; mi < MIL; mi++) {
+      f32x16 pp = {};
+      pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[mi][0], b[0], pp, 0, 0, 0, 127, 0, 127);
+      pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[mi][1], b[1], pp, 0, 0, 0, 127, 0, 127);
+      const float sa[16] = {sa4[mi][0].x, sa4[mi][0].y, sa4[mi][0].z, sa4[mi][0].w, sa4[mi][1].x, sa4[mi][1].y,
+                            sa4[mi][1].z, sa4[mi][1].w, sa4[mi][2].x, sa4[mi][2].y, sa4[mi][2].z, sa4[mi][2].w,
+                            sa4[mi][3].x, sa4[mi][3].y, sa4[mi][3].z, sa4[mi][3].w};
+#pragma unroll
+      for (int i = 0; i < 16; i++) acc[mi][i] += pp[i] * (sa[i] * sw);
+    }
+  }
+}
+
+template <bool FP8, int BM, bool GATEUP>
+__global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
+  constexpr int MI = BM / 32;               // row blocks of 32
+  constexpr int AG = BM / 32;               // activation 8-row groups per wavefront
+  constexpr int BG = BNW / 32;              // weight 8-row groups per wavefront
+  constexpr int EXTRA = FP8 ? 1024 : 0;     // fp8: BM activation scales (<= 512 B), then 4 weight-scale words
+  constexpr int NCOLS = GATEUP ? 64 : 128;  // output columns per item
+  constexpr int BK = FP8 ? 128 : 64;        // contraction elements per step
+
+  __shared__ __attribute__((aligned(1024))) char ring[RING_BYTES];
+  __shared__ __attribute__((aligned(16))) int32_t s_rows[NROWT][BM];
+  __shared__ int32_t s_cum[4][NQ];                                   // per wavefront: loads issued through a step
+  __shared__ int32_t s_off[kMaxS + 1];
+  __shared__ int32_t s_cnt[kMaxS];
+  __shared__ int32_t s_sw[kMaxS + 1];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+
+  for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
+  for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
+  __syncthreads();
+  build_slot_weights<BM>(s_off, s_cnt, s_sw, p.S);
+
+  int NT = (int)p.hdr[kHdrTiles];
+  NT = NT < p.max_tiles ? NT : p.max_tiles;
+  const Geo g = make_geo<BM>(p.Kd / BK, p.Nout / NCOLS, NT, blockIdx.x, gridDim.x, s_off, s_cnt, s_sw, p.S);
+  if (g.q0 >= g.q1) {  // uniform: the whole workgroup leaves
+    if (tid == 0) p.fix[(size_t)blockIdx.x * FIX_WORDS] = -1;
+    return;
+  }
+  const int first_item = g.q0 / g.C;
+  const int first_c = g.q0 - first_item * g.C;
+  const int last_item = (g.q1 - 1) / g.C;
+  const bool gather = p.row_src != nullptr;
+  const uint32_t a_row_bytes = (uint32_t)p.Kd * (FP8 ? 1 : 2);
+  const int lrow = lane >> 3, gchunk = (lane & 7) ^ (lane >> 3);
+  const uint32_t ring_lds = lds_addr(ring);
+
+  // row tables of the range's M-tiles (tiles past NROWT read row_src directly)
+  const int tile_lo = first_item / g.my_nb;
+  if (gather) {
+    const int nt = min(last_item / g.my_nb - tile_lo + 1, NROWT);
+    for (int t = wave; t < nt; t += 4)
+      if (lane < BM / 4) lds_dma16(p.row_src + (size_t)(tile_lo + t) * BM + lane * 4, &s_rows[t][0]);
+    wait_vmcnt(0);
+  }
+  barrier_nofence();
+
+  // Ring geometry of this range: a slot holds the activation row groups of
+  // the range's largest M-tile, so ranges of decode-sized tiles get more
+  // slots (more weight bytes in flight) than ranges with full tiles.
+  int amax = 0;
+  for (int t = tile_lo + lane; t <= last_item / g.my_nb; t += 64) {
+    const int sl = slot_of_row(s_off, p.S, t * BM);
+    const int rows = min(BM, s_off[sl] + s_cnt[sl] - t * BM);
+    amax = max(amax, rows);
+  }
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) amax = max(amax, __shfl_xor(amax, d));
+  const int A_BYTES = __builtin_amdgcn_readfirstlane(((amax + 7) >> 3) * 1024);
+  const int SLOT = A_BYTES + B_BYTES + EXTRA;
+  const int NS = __builtin_amdgcn_readfirstlane(min(NQ, RING_BYTES / SLOT));
+
+  // total steps of the range: SPC per chunk, SL for an item's last chunk
+  const int F = (g.q1 - g.q0) * g.SPC - (g.q1 / g.C - g.q0 / g.C) * (g.SPC - g.SL);
+
+  // ---- issue side: step iss of the range goes to ring slot iss % NS ----
+  int is_item = first_item, is_kt = first_c * g.SPC;
+  int is_kt_end = min(g.KT, (g.q1 - is_item * g.C) * g.SPC);
+  int is_nvalid = 0, is_L = 0;
+  bool is_new = true;
+  const char* a_base = p.A;
+  const char* b_base = p.W;
+  const char* as_base = nullptr;
+  const char* ws_base = nullptr;
+  uint32_t a_voff[AG];
+  uint32_t b_voff[BG];
+#pragma unroll
+  for (int j = 0; j < BG; j++) b_voff[j] = (wave + 4 * j) * 1024 + lane * 16;
+  int iss = 0, cum = 0, is_slot = 0;
+
+  auto setup_item = [&]() {
+    const int tile = is_item / g.my_nb;
+    const int nb = g.nb_lo + is_item - tile * g.my_nb;
+    const int row0 = tile * BM;
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
+    is_nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
+    b_base = p.W + (size_t)slot * p.w_slot_bytes + (size_t)nb * g.KT * B_BYTES;
+    a_base = gather ? p.A : p.A + (size_t)row0 * a_row_bytes;
+    int nA = 0;
+    const int tt = tile - tile_lo;
+#pragma unroll
+    for (int j = 0; j < AG; j++) {
+      const int gi = wave + 4 * j;
+      const int r = min(gi * 8 + lrow, is_nvalid - 1);
+      uint32_t row = r;
+      if (gather) {
+        // (separate loads: one through a pointer that may be LDS or global
+        // would be a generic load, whose wait drains the whole DMA stream)
+        int v;
+        if (tt < NROWT) {
+          v = s_rows[tt][r];
+        } else {  // not reached when the host chose gathering: a plain load that waits for everything
+          asm volatile("global_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)"
+                       : "=v"(v)
+                       : "v"(p.row_src + row0 + r)
+                       : "memory");
+        }
+        row = max(v, 0);
+      }
+      a_voff[j] = row * a_row_bytes + gchunk * 16;
+      nA += gi * 8 < is_nvalid ? 1 : 0;
+    }
+    is_L = nA + BG + (FP8 && (wave == 3 || wave == 2) ? 1 : 0);
+    if (FP8) {
+      as_base = reinterpret_cast<const char*>(p.As + row0);
+      ws_base = reinterpret_cast<const char*>(p.Wsp + (size_t)slot * p.ws_slot_floats + (size_t)nb * g.KT * 4);
+    }
+    is_new = false;
+  };
+
+  auto issue = [&]() {
+    if (is_new) setup_item();
+    const uint32_t sl = ring_lds + is_slot * SLOT;
+    const char* ab = a_base + is_kt * ROWB;
+#pragma unroll
+    for (int j = 0; j < AG; j++) {
+      const int gi = wave + 4 * j;
+      if (gi * 8 < is_nvalid) lds_dma16s(ab, a_voff[j], sl + gi * 1024);
+    }
+    const char* bb = b_base + (size_t)is_kt * B_BYTES;
+#pragma unroll
+    for (int j = 0; j < BG; j++) lds_dma16s(bb, b_voff[j], sl + A_BYTES + (wave + 4 * j) * 1024);
+    if (FP8) {
+      if (wave == 3) {
+        if (lane < BM / 4) lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES + B_BYTES);
+      } else if (wave == 2) {
+        if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + B_BYTES + 512);
+      }
+    }
+    cum += is_L;
+    if (lane == 0) s_cum[wave][iss % NQ] = cum;
+    iss++;
+    if (++is_slot == NS) is_slot = 0;
+    if (++is_kt == is_kt_end) {
+      is_item++;
+      is_kt = 0;
+      is_kt_end = min(g.KT, (g.q1 - is_item * g.C) * g.SPC);
+      is_new = true;
+    }
+  };
+
+  // ---- consume side ----
+  // The lane index is laundered where the stores happen, so that the
+  // compiler does not keep every address live across the main loop.
+  auto store_tile = [&](float* dst, const auto& v) {
+    constexpr int NV = sizeof(v) / sizeof(v[0]);
+    int ln = lane;
+    asm volatile("" : "+v"(ln));
+#pragma unroll
+    for (int mi = 0; mi < NV; mi++)
+#pragma unroll
+      for (int q = 0; q < 4; q++)
+        *reinterpret_cast<float4*>(dst + part_index(mi, wave, ln, 4 * q)) =
+            make_float4(v[mi][4 * q], v[mi][4 * q + 1], v[mi][4 * q + 2], v[mi][4 * q + 3]);
+  };
+
+#pragma unroll 1
+  for (int s = 0; s < NS - 1 && s < F; s++) issue();
+
+  // One piece of an item (the steps of one item inside this range), with the
+  // number of row blocks holding a real row fixed at compile time.
+  int k = 0, uc_slot = 0;
+  uint64_t tstart = 0;
+  int ck_next = 0;  // loads this wavefront had issued through step k
+  if (F > 0) ck_next = __builtin_amdgcn_readfirstlane(s_cum[wave][0]);
+  auto run_piece = [&](auto mil, int ord) {
+    constexpr int MIL = decltype(mil)::value;
+    const int item = first_item + ord;
+    const int tile = item / g.my_nb;
+    const int nb = g.nb_lo + item - tile * g.my_nb;
+    const int row0 = tile * BM;
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
+    const int nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
+    const int c0 = ord == 0 ? first_c : 0;  // first chunk of the piece
+    const int kt_end = min(g.KT, (g.q1 - item * g.C) * g.SPC);
+    const int n = kt_end - c0 * g.SPC;
+    if (p.timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
+    float* const part_mine = p.part + (size_t)blockIdx.x * CMAX * BM * PART_TILE;
+    // running sum of the chunks of a piece that starts at chunk 0
+    f32x16 R[MIL];
+#pragma unroll
+    for (int mi = 0; mi < MIL; mi++)
+#pragma unroll
+      for (int i = 0; i < 16; i++) R[mi][i] = 0.f;
+    // a piece is whole chunks: an outer loop over them, a branch-free inner
+    // loop over a chunk's steps (the accumulator stays in place)
+#pragma unroll 1
+    for (int c = c0, t = 0; t < n; c++) {
+      const int steps = c == g.C - 1 ? g.SL : g.SPC;
+      f32x16 acc[MIL];
+#pragma unroll
+      for (int mi = 0; mi < MIL; mi++)
+#pragma unroll
+        for (int i = 0; i < 16; i++) acc[mi][i] = 0.f;
+#pragma unroll 1
+      for (int u = 0; u < steps; u++, t++, k++) {
+        wait_vmcnt(__builtin_amdgcn_readfirstlane(min(63, cum - ck_next)));
+        wait_lgkm0();  // this wavefront's LDS records are complete before the barrier
+        barrier_nofence();
+        const char* st = ring + uc_slot * SLOT;
+        if (++uc_slot == NS) uc_slot = 0;
+        step_mma<FP8, GATEUP, BM, MIL>(st, A_BYTES, lane, wave, acc, [&]() {
+          if (iss < F) issue();  // step k + NS - 1 into the slot step k - 1 left
+        });
+        // loads this wavefront had issued through step k + 1 (recorded when
+        // that step was issued, an iteration or more ago)
+        ck_next = __builtin_amdgcn_readfirstlane(s_cum[wave][(k + 1) % NQ]);
+      }
+      // end of a chunk: fold it into the running sum, or hand it to the fixup
+      const bool piece_end = t == n;
+      if (c0 > 0) {
+        store_tile(part_mine + (size_t)(1 + c - c0) * BM * PART_TILE, acc);
+      } else {
+        if (c == 0) {
+#pragma unroll
+          for (int mi = 0; mi < MIL; mi++) R[mi] = acc[mi];
+        } else {
+#pragma unroll
+          for (int mi = 0; mi < MIL; mi++) R[mi] += acc[mi];
+        }
+        if (piece_end) {
+          if (c == g.C - 1) {
+            // the whole item is here: epilogue
+            int ln = lane;
+            asm volatile("" : "+v"(ln));
+            const int rb = 4 * (ln >> 5);
+            char* const cbase = static_cast<char*>(p.C) + (size_t)row0 * p.Nout * (GATEUP && FP8 ? 4 : 2);
+#pragma unroll
+            for (int mi = 0; mi < MIL; mi++)
+#pragma unroll
+              for (int i = 0; i < 16; i++) {
+                const int r = rb + mi * 32 + 8 * (i >> 2) + (i & 3);
+                if (GATEUP) {
+                  // lanes l and l ^ 16 hold the gate and the up value of one column
+                  const float up = __shfl_xor(R[mi][i], 16);
+                  if (r < nvalid && (ln & 16) == 0) {
+                    const float h = silu_mul(R[mi][i], up);
+                    const int o = r * p.Nout + nb * 64 + wave * 16 + (ln & 15);
+                    if (FP8) reinterpret_cast<float*>(cbase)[o] = h;
+                    else reinterpret_cast<uint16_t*>(cbase)[o] = f32_to_bf16_rne(h);
+                  }
+                } else if (r < nvalid) {
+                  const int o = r * p.Nout + nb * 128 + wave * 32 + (ln & 31);
+                  reinterpret_cast<uint16_t*>(cbase)[o] = f32_to_bf16_rne(R[mi][i]);
+                }
+              }
+          } else {
+            store_tile(part_mine, R);  // running sum of chunks 0..c
+          }
+        }
+      }
+    }
+    if (p.timing && tid == 0) {
+      const uint64_t tend = __builtin_amdgcn_s_memrealtime();
+      atomicMin(reinterpret_cast<unsigned long long*>(&p.t0[slot]), (unsigned long long)tstart);
+      atomicMax(reinterpret_cast<unsigned long long*>(&p.t1[slot]), (unsigned long long)tend);
+    }
+  };
+
+#pragma unroll 1
+  for (int ord = 0; k < F; ord++) {
+    const int item = first_item + ord;
+    const int row0 = (item / g.my_nb) * BM;
+    const int slot = slot_of_row(s_off, p.S, row0);
+    const int live = __builtin_amdgcn_readfirstlane((min(BM, s_off[slot] + s_cnt[slot] - row0) + 31) >> 5);
+    // row blocks multiplied: 1, 2 or all (a tile with 3 live blocks of 4 runs the
+    // full path; the extra block's rows are never stored)
+    if (live <= 1) run_piece(std::integral_constant<int, 1>{}, ord);
+    else if (MI > 2 && live == 2) run_piece(std::integral_constant<int, 2>{}, ord);
+    else run_piece(std::integral_constant<int, MI>{}, ord);
+  }
+
+  // fixup record: if the last item of the range started here (chunk 0) and
+  // continues past it, list where the later chunks' partial tiles are
+  if (tid == 0) {
+    int32_t* rec = p.fix + (size_t)blockIdx.x * FIX_WORDS;
+    const int cf = last_item * g.C;
+    if (cf >= g.q0 && g.q1 < cf + g.C) {
+      const int tile = last_item / g.my_nb;
+      const int row0 = tile * BM;
+      const int slot = slot_of_row(s_off, p.S, row0);
+      int n = 0, q = g.q1;
+      for (int j = g.j0 + 1; j < g.wpx && q < cf + g.C; j++) {
+        const int lo = range_lo<BM>(g, j, s_off, s_cnt, s_sw, p.S), hi = range_lo<BM>(g, j + 1, s_off, s_cnt, s_sw, p.S);
+        for (; q < hi && q < cf + g.C; q++) rec[4 + n++] = (j * g.groups + g.grp) * CMAX + 1 + q - lo;
+      }
+      rec[1] = row0;
+      rec[2] = g.nb_lo + last_item - tile * g.my_nb;
+      rec[3] = min(BM, s_off[slot] + s_cnt[slot] - row0);
+      rec[0] = n;
+    } else {
+      rec[0] = -1;
+    }
+  }
+}
+
+// Completes the items whose chunks were spread over several workgroups.  The
+// GEMM workgroup b whose range holds chunk 0 of such an item left a record
+// (row0, output block, real rows, the partial tiles of the later chunks in
+// chunk order).  Workgroup b + gemm_grid * (4 mi + w) of this grid (grid =
+// gemm_grid * BM / 8) takes what wavefront w held for row block mi: thread
+// (l, q) adds float4 q of lane l of the running sum b stored and of every
+// later chunk, in chunk order (all loads issued before the first add), then
+// applies the epilogue of the GEMM to its 4 rows.  For gate/up the gate lane
+// l (bit 4 clear) also reads the up lane l + 16; up lanes are idle.
+template <bool FP8, int BM, bool GATEUP>
+__global__ __launch_bounds__(256) void k_fixup(const GemmArgs p, int gemm_grid) {
+  const int b = blockIdx.x % gemm_grid, mw = blockIdx.x / gemm_grid;
+  const int mi = mw >> 2, w = mw & 3;
+  const int32_t* rec = p.fix + (size_t)b * FIX_WORDS;
+  const int nsrc = rec[0];
+  if (nsrc < 0) return;
+  const int row0 = rec[1], nb = rec[2], nvalid = rec[3];
+  if (mi * 32 >= nvalid) return;
+  const int l = threadIdx.x >> 2, q = threadIdx.x & 3;
+  if (GATEUP && (l & 16)) return;
+  const int rfirst = mi * 32 + 8 * q + 4 * (l >> 5);  // rows rfirst .. rfirst + 3
+  if (rfirst >= nvalid) return;
+  const size_t tile_elems = (size_t)BM * PART_TILE;
+  const int og = part_index(mi, w, l, 4 * q), ou = part_index(mi, w, l + 16, 4 * q);
+  const float* head = p.part + (size_t)b * CMAX * tile_elems;
+  float4 xg[CMAX], xu[CMAX];
+  xg[0] = *reinterpret_cast<const float4*>(head + og);
+  if (GATEUP) xu[0] = *reinterpret_cast<const float4*>(head + ou);
+#pragma unroll
+  for (int i = 0; i < CMAX - 1; i++) {
+    if (i < nsrc) {
+      const float* t = p.part + (size_t)rec[4 + i] * tile_elems;
+      xg[i + 1] = *reinterpret_cast<const float4*>(t + og);
+      if (GATEUP) xu[i + 1] = *reinterpret_cast<const float4*>(t + ou);
+    }
+  }
+  float4 g = xg[0], u = GATEUP ? xu[0] : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int i = 1; i < CMAX; i++) {
+    if (i <= nsrc) {
+      g.x += xg[i].x, g.y += xg[i].y, g.z += xg[i].z, g.w += xg[i].w;
+      if (GATEUP) u.x += xu[i].x, u.y += xu[i].y, u.z += xu[i].z, u.w += xu[i].w;
+    }
+  }
+  const float gv[4] = {g.x, g.y, g.z, g.w}, uv[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int e = 0; e < 4; e++) {
+    const int r = rfirst + e;
+    if (r >= nvalid) break;
+    const size_t orow = (size_t)(row0 + r) * p.Nout;
+    if (GATEUP) {
+      const float h = silu_mul(gv[e], uv[e]);
+      const int col = nb * 64 + w * 16 + (l & 15);
+      if (FP8) static_cast<float*>(p.C)[orow + col] = h;
+      else static_cast<uint16_t*>(p.C)[orow + col] = f32_to_bf16_rne(h);
+    } else {
+      static_cast<uint16_t*>(p.C)[orow + nb * 128 + w * 32 + (l & 31)] = f32_to_bf16_rne(gv[e]);
+    }
+  }
+}
+
+}  // namespace gemm
+}  // namespace tempo

@@ -33,13 +33,14 @@ struct Layout {
   size_t blk_hist;    // [nblk][E] int32 per-block counts, then per-block prefixes
   size_t blk_err;     // [nblk] uint32
   size_t local_rank;  // [T*K] int32 stable rank of a pair within its block and expert
-  size_t slot_lo;     // [S] int32 first rank (within its expert) taken by slot s
   size_t slot_t0;     // [S] uint64 first stage-2 tile start (real-time counter)
   size_t slot_t1;     // [S] uint64 last stage-2 tile end
   size_t h;           // [row_cap, I] bf16 or e4m3
   size_t h_scale;     // [I/128, row_cap] fp32 (fp8 only; scale-block-major)
   size_t h32;         // [row_cap, I] fp32 gate/up output before re-quantisation (fp8 only)
   size_t y_perm;      // [row_cap, H] bf16
+  size_t part;        // [grid][8][m_tile][128] fp32 stage-2 partial tiles
+  size_t fix;         // [grid][12] int32 stage-2 fixup records
   size_t total;
   int nblk;
   int row_cap;
@@ -73,6 +74,12 @@ hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, con
 
 hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& natural,
                        const tempo_expert_weights& packed, hipStream_t st);
+
+// Whether the gate/up GEMM gathers the activation rows itself (through
+// row_token, with the row tables of a workgroup's M-tiles in LDS) rather than
+// reading rows that stage 1 permuted into x_perm: true when every
+// workgroup's range spans few enough M-tiles.
+bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L);
 
 // Whether stage-2 kernels exist for this shape's element type and M-tile.
 bool experts_supported(const tempo_moe_shape& s);

@@ -8,7 +8,14 @@
 // of 8 rows is then one contiguous 1 KB that lands in LDS already swizzled,
 // and a work item streams its 128 rows x K weights as one contiguous block.
 // For the gate/up matrix an output block pairs gate rows n..n+63 with up rows
-// I+n..I+n+63 so SwiGLU sees matching columns.
+// I+n..I+n+63, interleaved in groups of 16 (gate n..n+15, up I+n..I+n+15,
+// gate n+16.., ...), so a 32-row slice multiplied by one wavefront holds
+// matching gate and up columns for SwiGLU.
+//
+// fp8 weight scales are packed per (output block, contraction step) as four
+// words, so that a step's scales travel with the step in one 16-byte load:
+// gate/up {scale of the gate rows' 128-block, scale of the up rows' block,
+// 0, 0}; down {scale of the block, 0, 0, 0}.
 #include "internal.h"
 
 namespace tempo {
@@ -30,10 +37,33 @@ __global__ __launch_bounds__(256) void k_pack(const uint4* __restrict__ src, uin
     const int kt = (int)(q % KT);
     const int nb = (int)(q / KT);
     int row;
-    if (gateup) row = r < 64 ? nb * 64 + r : half_rows + nb * 64 + (r - 64);
+    // gate/up: 16-row groups alternate gate and up: group 2w holds gate rows
+    // 64nb+16w.., group 2w+1 the matching up rows
+    if (gateup) row = ((r >> 4) & 1 ? half_rows : 0) + nb * 64 + (r >> 5) * 16 + (r & 15);
     else row = nb * 128 + r;
     const int c = p ^ (r & 7);
     dst[o] = src[s * per_slot + (size_t)row * row_chunks + kt * 8 + c];
+  }
+}
+
+// one thread per packed 4-word entry [slot][block][step]
+__global__ __launch_bounds__(256) void k_pack_scales(const float* __restrict__ nat, float4* __restrict__ dst, int S,
+                                                     int nblk, int KT, int nat_rows, int gateup, int half_blocks) {
+  const size_t total = (size_t)S * nblk * KT;
+  for (size_t o = (size_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (size_t)gridDim.x * 256) {
+    const int kt = (int)(o % KT);
+    const size_t q = o / KT;
+    const int nb = (int)(q % nblk);
+    const size_t s = q / nblk;
+    const float* ns = nat + s * nat_rows * KT;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (gateup) {
+      v.x = ns[(size_t)(nb / 2) * KT + kt];
+      v.y = ns[(size_t)(half_blocks + nb / 2) * KT + kt];
+    } else {
+      v.x = ns[(size_t)nb * KT + kt];
+    }
+    dst[o] = v;
   }
 }
 
@@ -51,6 +81,16 @@ hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& nat
                      static_cast<uint4*>(const_cast<void*>(pk.w13)), s.S, 2 * s.I, rc13, 1, s.I);
   hipLaunchKernelGGL(k_pack, dim3(g2), dim3(256), 0, st, static_cast<const uint4*>(nat.w2),
                      static_cast<uint4*>(const_cast<void*>(pk.w2)), s.S, s.H, rc2, 0, 0);
+  if (s.dtype == TEMPO_FP8_E4M3) {
+    // gate/up: I/64 output blocks x H/128 steps; down: H/128 blocks x I/128 steps
+    const size_t m13 = (size_t)s.S * (s.I / 64) * (s.H / 128), m2 = (size_t)s.S * (s.H / 128) * (s.I / 128);
+    hipLaunchKernelGGL(k_pack_scales, dim3((int)((m13 + 255) / 256 < 65536 ? (m13 + 255) / 256 : 65536)), dim3(256), 0,
+                       st, nat.w13_scale, reinterpret_cast<float4*>(const_cast<float*>(pk.w13_scale)), s.S, s.I / 64,
+                       s.H / 128, 2 * s.I / 128, 1, s.I / 128);
+    hipLaunchKernelGGL(k_pack_scales, dim3((int)((m2 + 255) / 256 < 65536 ? (m2 + 255) / 256 : 65536)), dim3(256), 0,
+                       st, nat.w2_scale, reinterpret_cast<float4*>(const_cast<float*>(pk.w2_scale)), s.S, s.H / 128,
+                       s.I / 128, s.H / 128, 0, 0);
+  }
   return hipGetLastError();
 }
 

@@ -157,10 +157,15 @@ class WeightTensors:
 
 def pack_weights(shape: MoEShape, natural: WeightTensors, stream=None) -> WeightTensors:
     """One-time re-layout (tempo_moe_pack_weights): returns new tensors holding
-    w13 / w2 in the packed layout stage 2 reads; scales are shared as is."""
+    w13 / w2 in the packed layout stage 2 reads and, for fp8, the packed
+    scales ([S, I/64, H/128, 4] and [S, H/128, I/128, 4] fp32)."""
     _check_weights(shape, natural)
-    packed = WeightTensors(torch.empty_like(natural.w13), torch.empty_like(natural.w2), natural.w13_scale,
-                           natural.w2_scale)
+    s13 = s2 = None
+    if shape.dtype == "fp8":
+        dev = natural.w13.device
+        s13 = torch.empty(shape.S, shape.I // 64, shape.H // 128, 4, dtype=torch.float32, device=dev)
+        s2 = torch.empty(shape.S, shape.H // 128, shape.I // 128, 4, dtype=torch.float32, device=dev)
+    packed = WeightTensors(torch.empty_like(natural.w13), torch.empty_like(natural.w2), s13, s2)
     sh, nat, pk = shape.c(), natural.c(), packed.c()
     check(_lib.load().tempo_moe_pack_weights(ctypes.byref(sh), ctypes.byref(nat), ctypes.byref(pk),
                                              _stream(stream)), "tempo_moe_pack_weights")
@@ -181,12 +186,16 @@ def _check_plan(shape, plan):
     _need(plan.remote_replicas, torch.int32, (shape.E,), "remote_replicas")
 
 
-def _check_weights(shape, w):
+def _check_weights(shape, w, packed=False):
     _need(w.w13, shape.elem, (shape.S, 2 * shape.I, shape.H), "w13")
     _need(w.w2, shape.elem, (shape.S, shape.H, shape.I), "w2")
     if shape.dtype == "fp8":
-        _need(w.w13_scale, torch.float32, (shape.S, 2 * shape.I // 128, shape.H // 128), "w13_scale")
-        _need(w.w2_scale, torch.float32, (shape.S, shape.H // 128, shape.I // 128), "w2_scale")
+        if packed:
+            _need(w.w13_scale, torch.float32, (shape.S, shape.I // 64, shape.H // 128, 4), "packed w13_scale")
+            _need(w.w2_scale, torch.float32, (shape.S, shape.H // 128, shape.I // 128, 4), "packed w2_scale")
+        else:
+            _need(w.w13_scale, torch.float32, (shape.S, 2 * shape.I // 128, shape.H // 128), "w13_scale")
+            _need(w.w2_scale, torch.float32, (shape.S, shape.H // 128, shape.I // 128), "w2_scale")
 
 
 def _check_disp(shape, d, row_cap):
@@ -221,7 +230,7 @@ def experts(shape: MoEShape, disp: DispatchBuffers, weights: WeightTensors, y_pe
     """Stage 2 (tempo_moe_experts): writes y_perm [row_cap, H] bf16.  weights
     must be packed (pack_weights)."""
     _check_disp(shape, disp, ws.row_cap)
-    _check_weights(shape, weights)
+    _check_weights(shape, weights, packed=True)
     _need(y_perm, torch.int16, (ws.row_cap, shape.H), "y_perm")
     sh, do, w = shape.c(), disp.c(), weights.c()
     check(_lib.load().tempo_moe_experts(ctypes.byref(sh), ctypes.byref(do), ctypes.byref(w), _ptr(y_perm), ws.ptr,
@@ -251,7 +260,7 @@ def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, we
     _check_inputs(shape, topk_ids, x, x_scale)
     _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
     _check_plan(shape, plan)
-    _check_weights(shape, weights)
+    _check_weights(shape, weights, packed=True)
     _check_disp(shape, disp, ws.row_cap)
     _need(y, torch.int16, (shape.T, shape.H), "y")
     if slot_time_ns is not None:
@@ -280,7 +289,7 @@ class PreparedForward:
         _check_inputs(shape, topk_ids, x, x_scale)
         _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
         _check_plan(shape, plan)
-        _check_weights(shape, weights)
+        _check_weights(shape, weights, packed=True)
         _check_disp(shape, disp, ws.row_cap)
         _need(y, torch.int16, (shape.T, shape.H), "y")
         if slot_time_ns is not None:

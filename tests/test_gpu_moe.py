@@ -175,7 +175,7 @@ def test_pack_layout():
     """The packed weight layout: per slot, output block by output block, each
     128-byte contraction step a 16 KB tile of 128 rows x 8 chunks of 16
     bytes, chunk c of row r at position c ^ (r & 7); gate/up blocks pair gate
-    rows n..n+63 with up rows I+n..I+n+63."""
+    rows n..n+63 with up rows I+n..I+n+63, interleaved in groups of 16."""
     import torch
     from paper_2608_13057_amd import moe
 
@@ -200,8 +200,36 @@ def test_pack_layout():
                         out[:, nb, kt, r, p] = ch[:, rows[r], kt * 8 + (p ^ (r & 7))]
         return out.reshape(S_, -1)
 
-    e13 = expect(w13, lambda nb: list(range(nb * 64, nb * 64 + 64)) + list(range(I + nb * 64, I + nb * 64 + 64)),
-                 I // 64)
+    def gu_rows(nb):  # 16-row groups alternate gate and the matching up rows
+        return [(I if (r // 16) % 2 else 0) + nb * 64 + (r // 32) * 16 + r % 16 for r in range(128)]
+
+    e13 = expect(w13, gu_rows, I // 64)
     e2 = expect(w2, lambda nb: list(range(nb * 128, nb * 128 + 128)), H // 128)
     assert np.array_equal(to_host(pk.w13).reshape(S, -1), e13)
     assert np.array_equal(to_host(pk.w2).reshape(S, -1), e2)
+
+
+def test_pack_fp8_scales():
+    """Packed fp8 weight scales: 4 words per (output block, contraction step);
+    gate/up {gate-row block scale, up-row block scale, 0, 0} for the block
+    pairing gate rows 64n.. with up rows I+64n..; down {block scale, 0, 0, 0}."""
+    import torch
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(4)
+    S, H, I = 3, 384, 640
+    shape = moe.MoEShape(T=4, K=1, E=3, S=S, H=H, I=I, dtype="fp8")
+    w13 = rng.integers(0, 256, size=(S, 2 * I, H), dtype=np.uint8)
+    w2 = rng.integers(0, 256, size=(S, H, I), dtype=np.uint8)
+    s13 = rng.random((S, 2 * I // 128, H // 128)).astype(np.float32)
+    s2 = rng.random((S, H // 128, I // 128)).astype(np.float32)
+    pk = moe.pack_weights(shape, moe.WeightTensors(to_dev(w13), to_dev(w2), to_dev(s13), to_dev(s2)))
+    torch.cuda.synchronize()
+    e13 = np.zeros((S, I // 64, H // 128, 4), np.float32)
+    for nb in range(I // 64):
+        e13[:, nb, :, 0] = s13[:, nb // 2, :]
+        e13[:, nb, :, 1] = s13[:, I // 128 + nb // 2, :]
+    e2 = np.zeros((S, H // 128, I // 128, 4), np.float32)
+    e2[..., 0] = s2
+    assert np.array_equal(to_host(pk.w13_scale), e13)
+    assert np.array_equal(to_host(pk.w2_scale), e2)
