@@ -29,13 +29,11 @@ __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int 
                                                  const uint64_t* __restrict__ t0, const uint64_t* __restrict__ t1,
                                                  uint64_t* __restrict__ slot_time_ns) {
   const int lane = threadIdx.x & 63;
-  const int segs = H / 512;  // 512-column segments per token (H is a multiple of 128)
   const int nseg = (H + 511) / 512;
   const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (slot_time_ns && blockIdx.x == 0)
     for (int s = threadIdx.x; s < S; s += 256)
       slot_time_ns[s] = slot_counts[s] > 0 ? (t1[s] - t0[s]) * 10ull : 0ull;  // 100 MHz counter
-  (void)segs;
   const int t = wid / nseg, seg = wid - t * nseg;
   if (t >= T) return;
   const int c = seg * 64 + lane;  // this lane's 16-byte chunk (8 columns)

@@ -40,7 +40,7 @@
 namespace tempo {
 namespace {
 
-constexpr int kPlaceChunk = 64;  // pairs per k_place_gather block
+constexpr int kPlaceChunk = 64;  // pairs per k_place block
 
 // ---------------------------------------------------------------------------
 // shared pieces

@@ -10,11 +10,13 @@
 // is one (M-tile, output block of 128 weight rows) pair; its contraction of
 // KT steps (128 bytes of every row per step) is cut into C <= 8 fixed chunks
 // of SPC steps (the last may be shorter).  The chunks of all items, item by
-// item, form one sequence that is split into equal contiguous ranges, one per
-// workgroup (one workgroup per CU), so every CU streams the same number of
-// weight bytes whatever the tile and slot counts are.  When the output blocks
-// divide by 8, workgroup b (dispatched to XCD b mod 8) only takes items of
-// the b mod 8 eighth of the output blocks, so one XCD's L2 holds each weight
+// item, form one sequence that is split into contiguous ranges, one per
+// workgroup (one workgroup per CU).  Range boundaries balance estimated time
+// rather than chunk counts: a chunk of an M-tile with m live row blocks of 32
+// weighs W_BASE + m (weight streaming plus MFMA work), taken from per-slot
+// prefix sums in LDS.  When the output blocks divide by 8, workgroup b
+// (dispatched to XCD b mod 8) only takes items of the b mod 8 eighth of the
+// output blocks, so one XCD's L2 holds each weight
 // block that several M-tiles of a slot read.
 //
 // Arithmetic is fixed per row: chunk i of an item is accumulated by MFMA from
@@ -28,15 +30,15 @@
 //
 // Memory pipeline.  Operand tiles go from global memory straight into an LDS
 // ring with global_load_lds_dwordx4 (no registers involved).  The pipeline
-// never drains between work items: a stage holds the activation row groups
-// of its item that have a real row, the 16 KB weight tile, and (fp8) the
-// step's activation and weight scales, so stages differ in size; they are
-// placed back to back in the ring (a stage that would straddle the end starts
-// at offset 0) and up to 7 are in flight ahead of the one being multiplied,
-// as many as the ring holds.  The issuing side records, per stage, where it
-// lies and what it closes (a chunk, a piece of an item) in a small descriptor
-// ring in LDS, and per wavefront how many loads it had issued; each
-// wavefront waits only until its own loads of the stage are done (vmcnt),
+// never drains between work items.  The ring is cut into NS equal slots,
+// each sized for the largest M-tile of the workgroup's range (its live
+// activation row groups, the 16 KB weight tile and, for fp8, the step's
+// scales), so a range of decode-sized tiles keeps up to 7 steps in flight
+// ahead of the one being multiplied and a range of full tiles 3.  The issuing
+// side records per wavefront and step how many loads it had issued so far
+// (s_cum); each wavefront waits only until its own loads of the step are
+// done (vmcnt; stores are never counted as allowed outstanding: they share
+// the counter with loads and may complete out of order),
 // then a workgroup barrier makes everyone's data visible and frees the
 // previous stage.  When stage 1 left the rows in token order (the gate/up
 // GEMM then gathers rows itself), the source rows of the M-tiles of the range
