@@ -179,7 +179,10 @@ int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32
  * every (output block of 128 weight rows, contraction step of 128 bytes)
  * tile of a slot is one contiguous 16 KB block and the tiles of an output
  * block follow each other along the contraction, so stage 2 streams each
- * activated slot's weights front to back.  For w13 output block n holds gate
+ * activated slot's weights front to back.  Inside a tile, rows 32w..32w+31
+ * form the 4 KB piece w, stored as four 1 KB loads in MFMA operand order:
+ * load j, lane l (0..63) holds the 16-byte chunk c of row 32w + l%32, with
+ * c = 2j + l/32 (bf16) or c = 4(j/2) + 2(l/32) + j%2 (fp8).  For w13 output block n holds gate
  * rows 64n..64n+63 and the same up rows, interleaved in groups of 16 rows
  * (gate 64n..64n+15, up I+64n..I+64n+15, gate 64n+16.., ...).  fp8: packed->w13_scale / w2_scale are
  * caller buffers of the packed scale sizes above that receive the packed

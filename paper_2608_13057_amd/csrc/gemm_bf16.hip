@@ -36,7 +36,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.C = h;
   gu.Kd = s.H;
   gu.Nout = s.I;
-  hipLaunchKernelGGL((k_gemm<false, BM, true>), dim3(grid), dim3(256), 0, st, gu);
+  hipLaunchKernelGGL((k_gemm<false, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
   hipLaunchKernelGGL((k_fixup<false, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
   if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
 
@@ -48,7 +48,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.C = y_perm;
   dn.Kd = s.I;
   dn.Nout = s.H;
-  hipLaunchKernelGGL((k_gemm<false, BM, false>), dim3(grid), dim3(256), 0, st, dn);
+  hipLaunchKernelGGL((k_gemm<false, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
   hipLaunchKernelGGL((k_fixup<false, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }
@@ -59,17 +59,13 @@ bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L) {
   // upper bound of the M-tiles one workgroup range of the gate/up GEMM spans
   const int grid = persistent_grid(1);
   const int NB = s.I / 64;
-  const long long groups = geo_groups(NB, grid), wpx = grid / groups, my_nb = NB / groups;
-  const int KT = s.H / (s.dtype == TEMPO_BF16 ? 64 : 128);
-  const int SPC = (KT + CMAX - 1) / CMAX, C = (KT + SPC - 1) / SPC;
+  const long long groups = geo_groups(NB, grid), wpx = grid / groups;
   // ranges balance weighted chunks; a range holds at most 1/wpx of the total
   // weight, which is largest when every tile is full, and its tiles weigh at
   // least W_BASE + 1 each
   const long long max_tiles = L.row_cap / s.m_tile;
   const long long wfull = W_BASE + s.m_tile / 32, wmin = W_BASE + 1;
   const long long tiles = (max_tiles * wfull + wpx * wmin - 1) / (wpx * wmin) + 2;
-  (void)my_nb;
-  (void)C;
   return tiles <= NROWT;
 }
 

@@ -71,7 +71,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.C = h32;
   gu.Kd = s.H;
   gu.Nout = s.I;
-  hipLaunchKernelGGL((k_gemm<true, BM, true>), dim3(grid), dim3(256), 0, st, gu);
+  hipLaunchKernelGGL((k_gemm<true, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
   hipLaunchKernelGGL((k_fixup<true, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
   hipLaunchKernelGGL(k_quant_h, dim3(ceil_div(L.row_cap, 4)), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
@@ -88,7 +88,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.C = y_perm;
   dn.Kd = s.I;
   dn.Nout = s.H;
-  hipLaunchKernelGGL((k_gemm<true, BM, false>), dim3(grid), dim3(256), 0, st, dn);
+  hipLaunchKernelGGL((k_gemm<true, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
   hipLaunchKernelGGL((k_fixup<true, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }

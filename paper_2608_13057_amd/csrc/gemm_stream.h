@@ -9,15 +9,16 @@
 // Work decomposition (stream-K over fixed contraction chunks).  A work item
 // is one (M-tile, output block of 128 weight rows) pair; its contraction of
 // KT steps (128 bytes of every row per step) is cut into C <= 8 fixed chunks
-// of SPC steps (the last may be shorter).  The chunks of all items, item by
-// item, form one sequence that is split into contiguous ranges, one per
-// workgroup (one workgroup per CU).  Range boundaries balance estimated time
-// rather than chunk counts: a chunk of an M-tile with m live row blocks of 32
-// weighs W_BASE + m (weight streaming plus MFMA work), taken from per-slot
-// prefix sums in LDS.  When the output blocks divide by 8, workgroup b
-// (dispatched to XCD b mod 8) only takes items of the b mod 8 eighth of the
-// output blocks, so one XCD's L2 holds each weight
-// block that several M-tiles of a slot read.
+// of SPC steps, SPC a multiple of the pipeline depth DR (the last chunk is
+// padded with empty steps to a multiple of DR).  The chunks of all items,
+// item by item, form one sequence that is split into contiguous ranges, one
+// per workgroup (one workgroup per CU).  Range boundaries balance estimated
+// time rather than chunk counts: a chunk of an M-tile with m live row blocks
+// of 32 weighs W_BASE + m (the fixed cost of a step plus its MFMA work), taken
+// from per-slot prefix sums in LDS.  When the output blocks divide by 8,
+// workgroup b (dispatched to XCD b mod 8) only takes items of the b mod 8
+// eighth of the output blocks, so one XCD's L2 holds each weight block that
+// several M-tiles of a slot read.
 //
 // Arithmetic is fixed per row: chunk i of an item is accumulated by MFMA from
 // zero in step order (c_i), and the result is ((c_0 + c_1) + c_2) + ... in
@@ -28,33 +29,36 @@
 // and applies the epilogue.  Results therefore do not depend on where the
 // range boundaries fall, on the plan, or on the tile a row lands in.
 //
-// Memory pipeline.  Operand tiles go from global memory straight into an LDS
-// ring with global_load_lds_dwordx4 (no registers involved).  The pipeline
-// never drains between work items.  The ring is cut into NS equal slots,
-// each sized for the largest M-tile of the workgroup's range (its live
-// activation row groups, the 16 KB weight tile and, for fp8, the step's
-// scales), so a range of decode-sized tiles keeps up to 7 steps in flight
-// ahead of the one being multiplied and a range of full tiles 3.  The issuing
-// side records per wavefront and step how many loads it had issued so far
-// (s_cum); each wavefront waits only until its own loads of the step are
-// done (vmcnt; stores are never counted as allowed outstanding: they share
-// the counter with loads and may complete out of order),
-// then a workgroup barrier makes everyone's data visible and frees the
-// previous stage.  When stage 1 left the rows in token order (the gate/up
-// GEMM then gathers rows itself), the source rows of the M-tiles of the range
-// (their row tables) are loaded into LDS before the stream starts.
+// Memory pipeline.  A weight row block is used by exactly one wavefront
+// (wavefront w multiplies the item's rows 32w..32w+31), so weights skip LDS:
+// each wavefront loads its 4 KB of a step straight into registers with four
+// 1 KB loads (the packed layout stores them in MFMA operand order), DR steps
+// ahead, into a register ring indexed by step mod DR (the step loop is
+// unrolled DR times so that the index is a compile-time constant).  The
+// activation rows of a step are shared by the four wavefronts and go through
+// an LDS ring of DR + 1 slots with global_load_lds_dwordx4 (DMA, no
+// registers), issued just before the step's weight loads.  Loads complete in
+// order and every step issues four weight loads, so "at most 4 (DR - 1)
+// loads outstanding" means that this step's loads have landed; a barrier
+// then makes every wavefront's activation rows visible.  The weight loads of
+// a register set are issued on every step, also for the empty steps at the
+// end, so that the compiler's own wait counts stay static.  When stage 1 left
+// the rows in token order (the gate/up GEMM then gathers rows itself), the
+// source rows of the M-tiles of the range (their row tables) are loaded into
+// LDS before the stream starts.
 //
-// Compute.  BM x 128 tile per item; wavefront w multiplies all real row
+// Compute.  BM x 128 tile per item; wavefront w multiplies all live row
 // blocks of 32 by the item's weight rows 32w..32w+31, so the MFMA work is
 // spread over the four SIMDs even for a decode tile of a few rows.  For
 // gate/up the packed layout interleaves 16 gate rows and the same 16 up rows
 // in every 32, so a wavefront holds matching gate and up columns (lanes l and
-// l + 16) for SwiGLU.  bf16: 32x32x16 MFMA, 4 per stage and row block;
-// fp8: two 32x32x64 f8f6f4 MFMA per stage into a stage partial p that is
-// added as acc += p * (sA[row] * sW).  Lane layout of the 32x32 MFMA family
-// on gfx950: A row / B column = lane % 32, consecutive contraction elements
-// per lane; accumulator element i of lane l is row 8*(i/4) + 4*(l/32) + i%4,
-// column l % 32.
+// l + 16) for SwiGLU.  bf16: 32x32x16 MFMA, 4 per step and row block; fp8:
+// two 32x32x64 f8f6f4 MFMA per step into a step partial p that is added as
+// acc += p * (sA[row] * sW).  Lane layout of the 32x32 MFMA family on gfx950:
+// A row / B column = lane % 32, consecutive contraction elements per lane;
+// accumulator element i of lane l is row 8*(i/4) + 4*(l/32) + i%4, column
+// l % 32.  Finished output rows are staged in LDS and leave as whole rows,
+// 16 bytes per lane.
 #pragma once
 
 #include <type_traits>
@@ -99,9 +103,24 @@ struct GemmArgs {
   int timing;
 };
 
-// Work geometry; identical in the GEMM and in its fixup kernel.
+// Steps in flight per wavefront (DR): the weight slices of DR steps sit in
+// registers (four 16-byte loads per lane and step), the activation rows of
+// DR + 1 steps in the LDS ring.  Small M-tiles afford a deeper pipeline.
+#ifndef TEMPO_DR64
+#define TEMPO_DR64 8
+#endif
+#ifndef TEMPO_DR128
+#define TEMPO_DR128 4
+#endif
+__host__ __device__ constexpr int gemm_dr(int bm) { return bm == 64 ? TEMPO_DR64 : TEMPO_DR128; }
+
+// Work geometry; identical in the GEMM and in its fixup kernel.  Chunks are
+// whole multiples of DR steps (the register ring is indexed by step mod DR at
+// compile time); an item whose step count is not a multiple of DR ends in a
+// few empty steps that load and multiply nothing.
 struct Geo {
-  int KT, SPC, C, SL;  // steps per item, per chunk, chunks, steps of the last chunk
+  int KT, SPC, C, SL;  // real steps per item; steps per chunk; chunks; steps of the last chunk (padded)
+  int KTV;             // steps per item including the padding: (C - 1) * SPC + SL
   int groups, grp, j0, wpx, my_nb, nb_lo, items;
   int q0, q1;          // this workgroup's chunk range [q0, q1)
 };
@@ -112,30 +131,43 @@ __host__ __device__ __forceinline__ int geo_groups(int NB, int grid) { return (N
 // m row blocks of 32 real rows costs W_BASE + m (a step's fixed work plus its
 // MFMA and activation traffic per row block).  s_sw[s] holds the summed tile
 // weights of slots before s (s_sw[S] = all tiles).
-constexpr int W_BASE = 2;
+constexpr int W_BASE = 5;
 
 template <int BM>
 __device__ __forceinline__ int tile_weight(int rows) { return W_BASE + ((rows + 31) >> 5); }
 
 // All threads of the block; ends with a barrier.  s_off / s_cnt must be ready.
+// Wavefront 0 scans: lane l sums slots 4l..4l+3, then a shuffle scan.
 template <int BM>
 __device__ void build_slot_weights(const int32_t* s_off, const int32_t* s_cnt, int32_t* s_sw, int S) {
-  const int tid = threadIdx.x;
-  for (int s = tid; s < S; s += blockDim.x) {
-    const int nt = (s_off[s + 1] - s_off[s]) / BM;
-    s_sw[s + 1] = nt > 0 ? (nt - 1) * tile_weight<BM>(BM) + tile_weight<BM>(s_cnt[s] - (nt - 1) * BM) : 0;
+  static_assert(kMaxS <= 256, "four slots per lane");
+  if (threadIdx.x < 64) {
+    const int l = threadIdx.x;
+    int w[4], run = 0;
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+      const int s = 4 * l + i;
+      int v = 0;
+      if (s < S) {
+        const int nt = (s_off[s + 1] - s_off[s]) / BM;
+        v = nt > 0 ? (nt - 1) * tile_weight<BM>(BM) + tile_weight<BM>(s_cnt[s] - (nt - 1) * BM) : 0;
+      }
+      run += v;
+      w[i] = run;
+    }
+    int incl = run;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int o = __shfl_up(incl, d);
+      if (l >= d) incl += o;
+    }
+    const int excl = incl - run;
+#pragma unroll
+    for (int i = 0; i < 4; i++)
+      if (4 * l + i < S) s_sw[4 * l + i + 1] = excl + w[i];
+    if (l == 0) s_sw[0] = 0;
   }
-  if (tid == 0) s_sw[0] = 0;
   __syncthreads();
-  // inclusive scan of s_sw[1..S] (Hillis-Steele, S <= kMaxS)
-  for (int d = 1; d < S; d <<= 1) {
-    int v = 0;
-    for (int s = tid; s < S; s += blockDim.x) v = s >= d ? s_sw[s + 1 - d] : 0;
-    __syncthreads();
-    for (int s = tid; s < S; s += blockDim.x)
-      if (s >= d) s_sw[s + 1] += v;
-    __syncthreads();
-  }
 }
 
 // First chunk of workgroup j of a group: the smallest chunk q whose weight
@@ -169,10 +201,12 @@ template <int BM>
 __device__ __forceinline__ Geo make_geo(int KT, int NB, int NT, int b, int grid, const int32_t* s_off,
                                         const int32_t* s_cnt, const int32_t* s_sw, int S) {
   Geo g;
+  constexpr int DR = gemm_dr(BM);
   g.KT = KT;
-  g.SPC = (KT + CMAX - 1) / CMAX;
+  g.SPC = ((KT + CMAX - 1) / CMAX + DR - 1) / DR * DR;
   g.C = (KT + g.SPC - 1) / g.SPC;
-  g.SL = KT - (g.C - 1) * g.SPC;
+  g.SL = (KT - (g.C - 1) * g.SPC + DR - 1) / DR * DR;
+  g.KTV = (g.C - 1) * g.SPC + g.SL;
   g.groups = geo_groups(NB, grid);
   g.grp = b % g.groups;
   g.j0 = b / g.groups;
@@ -195,94 +229,35 @@ __device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f +
 // issued makes the next waits conservative, and fewer is better.)
 __device__ __forceinline__ int part_index(int mi, int w, int l, int i) { return ((mi * 4 + w) * 64 + l) * 16 + i; }
 
-// One step of the contraction on a resident ring slot: acc[mi] += A_mi W^T for
-// the MIL row blocks with a real row (compile-time count, straight-line code).
-template <bool FP8, bool GATEUP, int BM, int MIL, typename Between>
-__device__ __forceinline__ void step_mma(const char* st, int A_BYTES, int lane, int wave, f32x16 (&acc)[MIL],
-                                         Between&& between) {
-  // Fragment reads are requested first, then the caller's work (the DMAs of
-  // a later step) runs while they land, then the MFMAs; the scheduling
-  // barriers keep that order.  A slot holds A_BYTES of activation rows, then
-  // the weight tile, then (fp8) the scales.
-  const int bcol = wave * 32 + (lane & 31);  // weight row of the tile multiplied by this lane
-  if (!FP8) {
-    constexpr int KS = 4;                    // 16-element MFMA steps per 64-element stage
-    constexpr int KA = MIL <= 2 ? KS : 2;    // sub-steps read ahead (all, or two for a full tile)
-    bf16x8 a[KS][MIL], b[KS];
-    auto load = [&](int ks) {
-      const int c = 2 * ks + (lane >> 5);
-      b[ks] = *reinterpret_cast<const bf16x8*>(st + A_BYTES + swz(bcol, c));
-#pragma unroll
-      for (int mi = 0; mi < MIL; mi++) a[ks][mi] = *reinterpret_cast<const bf16x8*>(st + swz(mi * 32 + (lane & 31), c));
-    };
-#pragma unroll
-    for (int ks = 0; ks < KA; ks++) load(ks);
-    __builtin_amdgcn_sched_barrier(0);
-    between();
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int ks = 0; ks < KS; ks++) {
-      if (ks + KA < KS) load(ks + KA);
-#pragma unroll
-      for (int mi = 0; mi < MIL; mi++) acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks][mi], b[ks], acc[mi], 0, 0, 0);
-    }
-  } else {
-    const float* sa_lds = reinterpret_cast<const float*>(st + A_BYTES + B_BYTES);
-    const float* sw_lds = sa_lds + 128;
-    i32x8 b[2], a[MIL][2];
-    float4 sa4[MIL][4];
-#pragma unroll
-    for (int h = 0; h < 2; h++) {
-      const int c = 4 * h + 2 * (lane >> 5);
-      const i32x4 lo = *reinterpret_cast<const i32x4*>(st + A_BYTES + swz(bcol, c));
-      const i32x4 hi = *reinterpret_cast<const i32x4*>(st + A_BYTES + swz(bcol, c + 1));
-      b[h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
-#pragma unroll
-    for (int mi = 0; mi < MIL; mi++) {
-      const int r = mi * 32 + (lane & 31);
-#pragma unroll
-      for (int h = 0; h < 2; h++) {
-        const int c = 4 * h + 2 * (lane >> 5);
-        const i32x4 lo = *reinterpret_cast<const i32x4*>(st + swz(r, c));
-        const i32x4 hi = *reinterpret_cast<const i32x4*>(st + swz(r, c + 1));
-        a[mi][h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      }
-#pragma unroll
-      for (int q = 0; q < 4; q++)
-        sa4[mi][q] = *reinterpret_cast<const float4*>(sa_lds + mi * 32 + 8 * q + 4 * (lane >> 5));
-    }
-    // gate/up: lanes with bit 4 clear hold gate columns, the others up columns
-    const float sw = GATEUP ? sw_lds[(lane >> 4) & 1] : sw_lds[0];
-    __builtin_amdgcn_sched_barrier(0);
-    between();
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int mi = 0; mi < MIL; mi++) {
-      f32x16 pp = {};
-      pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[mi][0], b[0], pp, 0, 0, 0, 127, 0, 127);
-      pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[mi][1], b[1], pp, 0, 0, 0, 127, 0, 127);
-      const float sa[16] = {sa4[mi][0].x, sa4[mi][0].y, sa4[mi][0].z, sa4[mi][0].w, sa4[mi][1].x, sa4[mi][1].y,
-                            sa4[mi][1].z, sa4[mi][1].w, sa4[mi][2].x, sa4[mi][2].y, sa4[mi][2].z, sa4[mi][2].w,
-                            sa4[mi][3].x, sa4[mi][3].y, sa4[mi][3].z, sa4[mi][3].w};
-#pragma unroll
-      for (int i = 0; i < 16; i++) acc[mi][i] += pp[i] * (sa[i] * sw);
-    }
-  }
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(integral_constant<int, 0>), ..., f(integral_constant<int, N - 1>)
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+constexpr int GEMM_THREADS = 256;
+
 template <bool FP8, int BM, bool GATEUP>
-__global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
+__global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   constexpr int MI = BM / 32;               // row blocks of 32
   constexpr int AG = BM / 32;               // activation 8-row groups per wavefront
-  constexpr int BG = BNW / 32;              // weight 8-row groups per wavefront
-  constexpr int EXTRA = FP8 ? 1024 : 0;     // fp8: BM activation scales (<= 512 B), then 4 weight-scale words
+  constexpr int DR = gemm_dr(BM);
+  constexpr int EXTRA = FP8 ? 640 : 0;      // fp8: BM activation scales (<= 512 B), then 4 weight-scale words
   constexpr int NCOLS = GATEUP ? 64 : 128;  // output columns per item
   constexpr int BK = FP8 ? 128 : 64;        // contraction elements per step
+  constexpr int NSL = DR + 1;               // activation ring slots
+  constexpr int SLOT_MAX = BM * ROWB + EXTRA;
+  constexpr int OUT_ES = GATEUP && FP8 ? 4 : 2;    // bytes per output element
+  constexpr int ROW_OUT = NCOLS * OUT_ES;           // bytes of an item's output row: 128 or 256
+  constexpr int STG_BYTES = BM * ROW_OUT;           // an item's output rows, staged for coalesced stores
 
-  __shared__ __attribute__((aligned(1024))) char ring[RING_BYTES];
+  __shared__ __attribute__((aligned(1024))) char ring[NSL * SLOT_MAX];
+  __shared__ __attribute__((aligned(16))) char stg[STG_BYTES];
   __shared__ __attribute__((aligned(16))) int32_t s_rows[NROWT][BM];
-  __shared__ int32_t s_cum[4][NQ];                                   // per wavefront: loads issued through a step
   __shared__ int32_t s_off[kMaxS + 1];
   __shared__ int32_t s_cnt[kMaxS];
   __shared__ int32_t s_sw[kMaxS + 1];
@@ -290,13 +265,14 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
-  for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
+  // the independent loads of the set-up first, together
+  const int nt_hdr = (int)p.hdr[kHdrTiles];
+  for (int s = tid; s <= p.S; s += GEMM_THREADS) s_off[s] = p.slot_offsets[s];
+  for (int s = tid; s < p.S; s += GEMM_THREADS) s_cnt[s] = p.slot_counts[s];
   __syncthreads();
   build_slot_weights<BM>(s_off, s_cnt, s_sw, p.S);
 
-  int NT = (int)p.hdr[kHdrTiles];
-  NT = NT < p.max_tiles ? NT : p.max_tiles;
+  const int NT = __builtin_amdgcn_readfirstlane(min(nt_hdr, p.max_tiles));
   const Geo g = make_geo<BM>(p.Kd / BK, p.Nout / NCOLS, NT, blockIdx.x, gridDim.x, s_off, s_cnt, s_sw, p.S);
   if (g.q0 >= g.q1) {  // uniform: the whole workgroup leaves
     if (tid == 0) p.fix[(size_t)blockIdx.x * FIX_WORDS] = -1;
@@ -316,13 +292,12 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
     const int nt = min(last_item / g.my_nb - tile_lo + 1, NROWT);
     for (int t = wave; t < nt; t += 4)
       if (lane < BM / 4) lds_dma16(p.row_src + (size_t)(tile_lo + t) * BM + lane * 4, &s_rows[t][0]);
-    wait_vmcnt(0);
+    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
   }
   barrier_nofence();
 
-  // Ring geometry of this range: a slot holds the activation row groups of
-  // the range's largest M-tile, so ranges of decode-sized tiles get more
-  // slots (more weight bytes in flight) than ranges with full tiles.
+  // A ring slot holds the activation row groups of the range's largest M-tile
+  // (and the step's scales for fp8).
   int amax = 0;
   for (int t = tile_lo + lane; t <= last_item / g.my_nb; t += 64) {
     const int sl = slot_of_row(s_off, p.S, t * BM);
@@ -332,26 +307,24 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
 #pragma unroll
   for (int d = 32; d >= 1; d >>= 1) amax = max(amax, __shfl_xor(amax, d));
   const int A_BYTES = __builtin_amdgcn_readfirstlane(((amax + 7) >> 3) * 1024);
-  const int SLOT = A_BYTES + B_BYTES + EXTRA;
-  const int NS = __builtin_amdgcn_readfirstlane(min(NQ, RING_BYTES / SLOT));
+  const int SLOT = A_BYTES + EXTRA;
 
-  // total steps of the range: SPC per chunk, SL for an item's last chunk
+  // steps of the range: SPC per chunk, SL for an item's last chunk
   const int F = (g.q1 - g.q0) * g.SPC - (g.q1 / g.C - g.q0 / g.C) * (g.SPC - g.SL);
 
-  // ---- issue side: step iss of the range goes to ring slot iss % NS ----
+  // ---- issue side: step iss of the range; its activation rows go to ring
+  // slot iss % NSL, its weight slice to register set iss % DR ----
   int is_item = first_item, is_kt = first_c * g.SPC;
-  int is_kt_end = min(g.KT, (g.q1 - is_item * g.C) * g.SPC);
-  int is_nvalid = 0, is_L = 0;
+  int is_kt_end = min(g.KTV, (g.q1 - is_item * g.C) * g.SPC);
+  int is_nvalid = 0;
   bool is_new = true;
   const char* a_base = p.A;
-  const char* b_base = p.W;
+  const char* w_base = p.W;
   const char* as_base = nullptr;
   const char* ws_base = nullptr;
   uint32_t a_voff[AG];
-  uint32_t b_voff[BG];
-#pragma unroll
-  for (int j = 0; j < BG; j++) b_voff[j] = (wave + 4 * j) * 1024 + lane * 16;
-  int iss = 0, cum = 0, is_slot = 0;
+  int iss = 0, is_slot = 0;
+  i32x4 wr[DR][4];   // weight operands of the steps in flight
 
   auto setup_item = [&]() {
     const int tile = is_item / g.my_nb;
@@ -359,9 +332,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
     const int row0 = tile * BM;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     is_nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
-    b_base = p.W + (size_t)slot * p.w_slot_bytes + (size_t)nb * g.KT * B_BYTES;
+    w_base = p.W + (size_t)slot * p.w_slot_bytes + (size_t)nb * g.KT * B_BYTES + wave * (B_BYTES / 4) + lane * 16;
     a_base = gather ? p.A : p.A + (size_t)row0 * a_row_bytes;
-    int nA = 0;
     const int tt = tile - tile_lo;
 #pragma unroll
     for (int j = 0; j < AG; j++) {
@@ -370,7 +342,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
       uint32_t row = r;
       if (gather) {
         // (separate loads: one through a pointer that may be LDS or global
-        // would be a generic load, whose wait drains the whole DMA stream)
+        // would be a generic load, whose wait drains the whole stream)
         int v;
         if (tt < NROWT) {
           v = s_rows[tt][r];
@@ -383,9 +355,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
         row = max(v, 0);
       }
       a_voff[j] = row * a_row_bytes + gchunk * 16;
-      nA += gi * 8 < is_nvalid ? 1 : 0;
     }
-    is_L = nA + BG + (FP8 && (wave == 3 || wave == 2) ? 1 : 0);
     if (FP8) {
       as_base = reinterpret_cast<const char*>(p.As + row0);
       ws_base = reinterpret_cast<const char*>(p.Wsp + (size_t)slot * p.ws_slot_floats + (size_t)nb * g.KT * 4);
@@ -393,144 +363,234 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
     is_new = false;
   };
 
-  auto issue = [&]() {
-    if (is_new) setup_item();
-    const uint32_t sl = ring_lds + is_slot * SLOT;
-    const char* ab = a_base + is_kt * ROWB;
+  // The four weight loads of a register set are issued on every call, also
+  // past the end of the range and for the empty steps that pad an item (then
+  // from one fixed 4 KB that stays in cache): the compiler counts the loads
+  // issued after each set to place its waits, and a load skipped on some path
+  // would make it wait for everything.
+  const i32x4* const w_idle = reinterpret_cast<const i32x4*>(p.W) + lane;
+  auto issue = [&](auto dd) {
+    constexpr int d = decltype(dd)::value;
+    const i32x4* wp = w_idle;
+    if (iss < F) {
+      if (is_new) setup_item();
+      if (is_kt < g.KT) {
+        const uint32_t sl = ring_lds + is_slot * SLOT;
+        const char* ab = a_base + is_kt * ROWB;
 #pragma unroll
-    for (int j = 0; j < AG; j++) {
-      const int gi = wave + 4 * j;
-      if (gi * 8 < is_nvalid) lds_dma16s(ab, a_voff[j], sl + gi * 1024);
-    }
-    const char* bb = b_base + (size_t)is_kt * B_BYTES;
-#pragma unroll
-    for (int j = 0; j < BG; j++) lds_dma16s(bb, b_voff[j], sl + A_BYTES + (wave + 4 * j) * 1024);
-    if (FP8) {
-      if (wave == 3) {
-        if (lane < BM / 4) lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES + B_BYTES);
-      } else if (wave == 2) {
-        if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + B_BYTES + 512);
+        for (int j = 0; j < AG; j++) {
+          const int gi = wave + 4 * j;
+          if (gi * 8 < is_nvalid) lds_dma16s(ab, a_voff[j], sl + gi * 1024);
+        }
+        if (FP8) {
+          if (wave == 3) {
+            if (lane < BM / 4) lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES);
+          } else if (wave == 2) {
+            if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + 512);
+          }
+        }
+        wp = reinterpret_cast<const i32x4*>(w_base + (size_t)is_kt * B_BYTES);
+      }
+      iss++;
+      if (++is_slot == NSL) is_slot = 0;
+      if (++is_kt == is_kt_end) {
+        is_item++;
+        is_kt = 0;
+        is_kt_end = min(g.KTV, (g.q1 - is_item * g.C) * g.SPC);
+        is_new = true;
       }
     }
-    cum += is_L;
-    if (lane == 0) s_cum[wave][iss % NQ] = cum;
-    iss++;
-    if (++is_slot == NS) is_slot = 0;
-    if (++is_kt == is_kt_end) {
-      is_item++;
-      is_kt = 0;
-      is_kt_end = min(g.KT, (g.q1 - is_item * g.C) * g.SPC);
-      is_new = true;
-    }
+#pragma unroll
+    for (int j = 0; j < 4; j++) wr[d][j] = __builtin_nontemporal_load(wp + j * 64);
   };
 
   // ---- consume side ----
-  // The lane index is laundered where the stores happen, so that the
-  // compiler does not keep every address live across the main loop.
-  auto store_tile = [&](float* dst, const auto& v) {
-    constexpr int NV = sizeof(v) / sizeof(v[0]);
+  // A partial tile goes out lane-native (16-byte stores of 1 KB per
+  // instruction); the lane index is laundered so that the compiler does not
+  // keep every address live across the main loop.
+  auto store_tile = [&](float* dst, const f32x16 (&v)[MI], int live) {
     int ln = lane;
     asm volatile("" : "+v"(ln));
 #pragma unroll
-    for (int mi = 0; mi < NV; mi++)
+    for (int mi = 0; mi < MI; mi++)
+      if (mi < live)
 #pragma unroll
-      for (int q = 0; q < 4; q++)
-        *reinterpret_cast<float4*>(dst + part_index(mi, wave, ln, 4 * q)) =
-            make_float4(v[mi][4 * q], v[mi][4 * q + 1], v[mi][4 * q + 2], v[mi][4 * q + 3]);
+        for (int q = 0; q < 4; q++)
+          *reinterpret_cast<float4*>(dst + part_index(mi, wave, ln, 4 * q)) =
+              make_float4(v[mi][4 * q], v[mi][4 * q + 1], v[mi][4 * q + 2], v[mi][4 * q + 3]);
+  };
+  // Output rows staged in LDS (stg[r][NCOLS]) go out as whole rows, 16
+  // bytes per lane, after a barrier (every wavefront staged its columns).
+  auto flush_rows = [&](char* dst, size_t dst_stride, int nrows) {
+    wait_lgkm0();
+    barrier_nofence();
+    constexpr int PER = ROW_OUT / 16;  // 16-byte pieces per row
+    int t0 = tid;
+    asm volatile("" : "+v"(t0));
+#pragma unroll 2
+    for (int idx = t0; idx < nrows * PER; idx += 256) {
+      const int r = idx / PER, c = idx % PER;
+      *reinterpret_cast<i32x4*>(dst + r * dst_stride + c * 16) = *reinterpret_cast<const i32x4*>(stg + r * ROW_OUT + c * 16);
+    }
   };
 
-#pragma unroll 1
-  for (int s = 0; s < NS - 1 && s < F; s++) issue();
+  // the first DR steps (F is a multiple of DR)
+  static_for<DR>([&](auto dd) { issue(dd); });
 
-  // One piece of an item (the steps of one item inside this range), with the
-  // number of row blocks holding a real row fixed at compile time.
+  // One step on ring slot st with weight set d: acc[mi] += A_mi W^T for the
+  // live row blocks (mi < live; block 0 always is).
+  auto compute = [&](auto dd, const char* st, f32x16(&acc)[MI], int live) {
+    constexpr int d = decltype(dd)::value;
+    const int bcol = lane & 31;
+    if (!FP8) {
+      // every fragment read of the step first, then the MFMAs (the scheduling
+      // barrier keeps the reads from being spread between the MFMAs, which
+      // would expose the LDS latency once per read)
+      bf16x8 a[MI][4];
+#pragma unroll
+      for (int mi = 0; mi < MI; mi++)
+        if (mi < live)
+#pragma unroll
+          for (int ks = 0; ks < 4; ks++)
+            a[mi][ks] = *reinterpret_cast<const bf16x8*>(st + swz(mi * 32 + bcol, 2 * ks + (lane >> 5)));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mi = 0; mi < MI; mi++)
+        if (mi < live)
+#pragma unroll
+          for (int ks = 0; ks < 4; ks++)
+            acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][ks], reinterpret_cast<const bf16x8&>(wr[d][ks]),
+                                                             acc[mi], 0, 0, 0);
+    } else {
+      const float* sa_lds = reinterpret_cast<const float*>(st + A_BYTES);
+      const float* sw_lds = sa_lds + 128;
+      // gate/up: lanes with bit 4 clear hold gate columns, the others up columns
+      const float sw = GATEUP ? sw_lds[(lane >> 4) & 1] : sw_lds[0];
+      const i32x8 b0 = (i32x8){wr[d][0][0], wr[d][0][1], wr[d][0][2], wr[d][0][3],
+                               wr[d][1][0], wr[d][1][1], wr[d][1][2], wr[d][1][3]};
+      const i32x8 b1 = (i32x8){wr[d][2][0], wr[d][2][1], wr[d][2][2], wr[d][2][3],
+                               wr[d][3][0], wr[d][3][1], wr[d][3][2], wr[d][3][3]};
+#pragma unroll
+      for (int mi = 0; mi < MI; mi++) {
+        if (mi < live) {
+          const int r = mi * 32 + bcol;
+          i32x8 a[2];
+#pragma unroll
+          for (int h = 0; h < 2; h++) {
+            const int c = 4 * h + 2 * (lane >> 5);
+            const i32x4 lo = *reinterpret_cast<const i32x4*>(st + swz(r, c));
+            const i32x4 hi = *reinterpret_cast<const i32x4*>(st + swz(r, c + 1));
+            a[h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          }
+          float4 sa4[4];
+#pragma unroll
+          for (int q = 0; q < 4; q++) sa4[q] = *reinterpret_cast<const float4*>(sa_lds + mi * 32 + 8 * q + 4 * (lane >> 5));
+          f32x16 pp = {};
+          pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[0], b0, pp, 0, 0, 0, 127, 0, 127);
+          pp = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[1], b1, pp, 0, 0, 0, 127, 0, 127);
+          const float sa[16] = {sa4[0].x, sa4[0].y, sa4[0].z, sa4[0].w, sa4[1].x, sa4[1].y, sa4[1].z, sa4[1].w,
+                                sa4[2].x, sa4[2].y, sa4[2].z, sa4[2].w, sa4[3].x, sa4[3].y, sa4[3].z, sa4[3].w};
+#pragma unroll
+          for (int i = 0; i < 16; i++) acc[mi][i] += pp[i] * (sa[i] * sw);
+        }
+      }
+    }
+  };
+
   int k = 0, uc_slot = 0;
   uint64_t tstart = 0;
-  int ck_next = 0;  // loads this wavefront had issued through step k
-  if (F > 0) ck_next = __builtin_amdgcn_readfirstlane(s_cum[wave][0]);
-  auto run_piece = [&](auto mil, int ord) {
-    constexpr int MIL = decltype(mil)::value;
+  // One piece of an item: the steps of one item inside this range.
+#pragma unroll 1
+  for (int ord = 0; k < F; ord++) {
     const int item = first_item + ord;
     const int tile = item / g.my_nb;
     const int nb = g.nb_lo + item - tile * g.my_nb;
     const int row0 = tile * BM;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     const int nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
+    const int live = (nvalid + 31) >> 5;
     const int c0 = ord == 0 ? first_c : 0;  // first chunk of the piece
-    const int kt_end = min(g.KT, (g.q1 - item * g.C) * g.SPC);
+    const int kt_end = min(g.KTV, (g.q1 - item * g.C) * g.SPC);
     const int n = kt_end - c0 * g.SPC;
     if (p.timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
     float* const part_mine = p.part + (size_t)blockIdx.x * CMAX * BM * PART_TILE;
     // running sum of the chunks of a piece that starts at chunk 0
-    f32x16 R[MIL];
+    f32x16 R[MI];
 #pragma unroll
-    for (int mi = 0; mi < MIL; mi++)
+    for (int mi = 0; mi < MI; mi++)
 #pragma unroll
       for (int i = 0; i < 16; i++) R[mi][i] = 0.f;
-    // a piece is whole chunks: an outer loop over them, a branch-free inner
-    // loop over a chunk's steps (the accumulator stays in place)
 #pragma unroll 1
     for (int c = c0, t = 0; t < n; c++) {
       const int steps = c == g.C - 1 ? g.SL : g.SPC;
-      f32x16 acc[MIL];
+      const int kt0 = c * g.SPC;
+      f32x16 acc[MI];
 #pragma unroll
-      for (int mi = 0; mi < MIL; mi++)
+      for (int mi = 0; mi < MI; mi++)
 #pragma unroll
         for (int i = 0; i < 16; i++) acc[mi][i] = 0.f;
 #pragma unroll 1
-      for (int u = 0; u < steps; u++, t++, k++) {
-        wait_vmcnt(__builtin_amdgcn_readfirstlane(min(63, cum - ck_next)));
-        wait_lgkm0();  // this wavefront's LDS records are complete before the barrier
-        barrier_nofence();
-        const char* st = ring + uc_slot * SLOT;
-        if (++uc_slot == NS) uc_slot = 0;
-        step_mma<FP8, GATEUP, BM, MIL>(st, A_BYTES, lane, wave, acc, [&]() {
-          if (iss < F) issue();  // step k + NS - 1 into the slot step k - 1 left
+      for (int u = 0; u < steps; u += DR) {
+        static_for<DR>([&](auto dd) {
+          constexpr int d = decltype(dd)::value;
+          // This step's loads are done once at most 4 (DR - 1) loads are
+          // outstanding: every step issues its activation DMAs before its
+          // four weight loads, each later step issues four weight loads,
+          // and loads complete in order.  Then everyone's rows are in LDS.
+          __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(4 * (DR - 1)));
+          barrier_nofence();
+          if (kt0 + u + d < g.KT) compute(dd, ring + uc_slot * SLOT, acc, live);
+          if (++uc_slot == NSL) uc_slot = 0;
+          // the next step for this register set, into the ring slot the
+          // previous step left
+          __builtin_amdgcn_sched_barrier(0);
+          issue(dd);
+          __builtin_amdgcn_sched_barrier(0);
         });
-        // loads this wavefront had issued through step k + 1 (recorded when
-        // that step was issued, an iteration or more ago)
-        ck_next = __builtin_amdgcn_readfirstlane(s_cum[wave][(k + 1) % NQ]);
       }
+      t += steps;
+      k += steps;
       // end of a chunk: fold it into the running sum, or hand it to the fixup
       const bool piece_end = t == n;
       if (c0 > 0) {
-        store_tile(part_mine + (size_t)(1 + c - c0) * BM * PART_TILE, acc);
+        store_tile(part_mine + (size_t)(1 + c - c0) * BM * PART_TILE, acc, live);
       } else {
         if (c == 0) {
 #pragma unroll
-          for (int mi = 0; mi < MIL; mi++) R[mi] = acc[mi];
+          for (int mi = 0; mi < MI; mi++) R[mi] = acc[mi];
         } else {
 #pragma unroll
-          for (int mi = 0; mi < MIL; mi++) R[mi] += acc[mi];
+          for (int mi = 0; mi < MI; mi++)
+            if (mi < live) R[mi] += acc[mi];
         }
         if (piece_end) {
           if (c == g.C - 1) {
-            // the whole item is here: epilogue
-            int ln = lane;
-            asm volatile("" : "+v"(ln));
-            const int rb = 4 * (ln >> 5);
-            char* const cbase = static_cast<char*>(p.C) + (size_t)row0 * p.Nout * (GATEUP && FP8 ? 4 : 2);
+            // the whole item is here: epilogue, rows [r][NCOLS] into the staging area
+            const int rb = 4 * (lane >> 5);
 #pragma unroll
-            for (int mi = 0; mi < MIL; mi++)
+            for (int mi = 0; mi < MI; mi++) {
+              if (mi >= live) break;
 #pragma unroll
               for (int i = 0; i < 16; i++) {
                 const int r = rb + mi * 32 + 8 * (i >> 2) + (i & 3);
                 if (GATEUP) {
                   // lanes l and l ^ 16 hold the gate and the up value of one column
                   const float up = __shfl_xor(R[mi][i], 16);
-                  if (r < nvalid && (ln & 16) == 0) {
+                  if ((lane & 16) == 0) {
                     const float h = silu_mul(R[mi][i], up);
-                    const int o = r * p.Nout + nb * 64 + wave * 16 + (ln & 15);
-                    if (FP8) reinterpret_cast<float*>(cbase)[o] = h;
-                    else reinterpret_cast<uint16_t*>(cbase)[o] = f32_to_bf16_rne(h);
+                    const int o = r * NCOLS + wave * 16 + (lane & 15);
+                    if (FP8) reinterpret_cast<float*>(stg)[o] = h;
+                    else reinterpret_cast<uint16_t*>(stg)[o] = f32_to_bf16_rne(h);
                   }
-                } else if (r < nvalid) {
-                  const int o = r * p.Nout + nb * 128 + wave * 32 + (ln & 31);
-                  reinterpret_cast<uint16_t*>(cbase)[o] = f32_to_bf16_rne(R[mi][i]);
+                } else {
+                  reinterpret_cast<uint16_t*>(stg)[r * NCOLS + wave * 32 + (lane & 31)] = f32_to_bf16_rne(R[mi][i]);
                 }
               }
+            }
+            flush_rows(static_cast<char*>(p.C) + ((size_t)row0 * p.Nout + (size_t)nb * NCOLS) * OUT_ES,
+                       (size_t)p.Nout * OUT_ES, nvalid);
           } else {
-            store_tile(part_mine, R);  // running sum of chunks 0..c
+            store_tile(part_mine, R, live);  // running sum of chunks 0..c
           }
         }
       }
@@ -540,20 +600,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm(const GemmArgs p) {
       atomicMin(reinterpret_cast<unsigned long long*>(&p.t0[slot]), (unsigned long long)tstart);
       atomicMax(reinterpret_cast<unsigned long long*>(&p.t1[slot]), (unsigned long long)tend);
     }
-  };
-
-#pragma unroll 1
-  for (int ord = 0; k < F; ord++) {
-    const int item = first_item + ord;
-    const int row0 = (item / g.my_nb) * BM;
-    const int slot = slot_of_row(s_off, p.S, row0);
-    const int live = __builtin_amdgcn_readfirstlane((min(BM, s_off[slot] + s_cnt[slot] - row0) + 31) >> 5);
-    // row blocks multiplied: 1, 2 or all (a tile with 3 live blocks of 4 runs the
-    // full path; the extra block's rows are never stored)
-    if (live <= 1) run_piece(std::integral_constant<int, 1>{}, ord);
-    else if (MI > 2 && live == 2) run_piece(std::integral_constant<int, 2>{}, ord);
-    else run_piece(std::integral_constant<int, MI>{}, ord);
   }
+
 
   // fixup record: if the last item of the range started here (chunk 0) and
   // continues past it, list where the later chunks' partial tiles are

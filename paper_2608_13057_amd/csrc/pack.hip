@@ -1,12 +1,17 @@
 // One-time weight re-layout for the stage-2 kernels.
 //
 // A stage-2 work item multiplies a tile of activation rows by one output block
-// of 128 weight rows, 128 bytes of the contraction at a time.  The packed
-// layout stores, per slot, output block by output block, the contraction steps
-// of that block one after another, each step as a 16 KB tile of 128 rows x 8
-// chunks of 16 bytes, chunk c of row r at position c ^ (r & 7).  A DMA group
-// of 8 rows is then one contiguous 1 KB that lands in LDS already swizzled,
-// and a work item streams its 128 rows x K weights as one contiguous block.
+// of 128 weight rows, 128 bytes of the contraction at a time (a step).  Each
+// of the four wavefronts of a workgroup multiplies 32 of the block's rows and
+// loads them itself, straight into registers, as MFMA operands.  The packed
+// layout therefore stores, per slot, output block by output block, the steps
+// of the block one after another; a step is four 4 KB pieces (one per
+// wavefront, rows 32w..32w+31), and a piece is four 1 KB loads in the order
+// the MFMA operand registers want them: load j, lane l holds the 16-byte
+// chunk c(j, l) of row 32w + (l & 31), with
+//   bf16 (32x32x16 MFMA):    c = 2j + (l >> 5)
+//   fp8  (32x32x64 MFMA):    c = 4(j >> 1) + 2(l >> 5) + (j & 1)
+// so every load instruction of the stream reads 1 KB of consecutive bytes.
 // For the gate/up matrix an output block pairs gate rows n..n+63 with up rows
 // I+n..I+n+63, interleaved in groups of 16 (gate n..n+15, up I+n..I+n+15,
 // gate n+16.., ...), so a 32-row slice multiplied by one wavefront holds
@@ -23,25 +28,28 @@ namespace {
 
 // one thread per 16-byte chunk of the packed slot
 __global__ __launch_bounds__(256) void k_pack(const uint4* __restrict__ src, uint4* __restrict__ dst, int S,
-                                              int rows, int row_chunks, int gateup, int half_rows) {
+                                              int rows, int row_chunks, int gateup, int half_rows, int fp8) {
   const size_t per_slot = (size_t)rows * row_chunks;
   const size_t total = per_slot * S;
   const int KT = row_chunks / 8;
   for (size_t o = (size_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (size_t)gridDim.x * 256) {
     const size_t s = o / per_slot;
     size_t q = o % per_slot;
-    const int p = (int)(q & 7);
-    q >>= 3;
-    const int r = (int)(q & 127);
-    q >>= 7;
+    const int l = (int)(q & 63);
+    q >>= 6;
+    const int j = (int)(q & 3);
+    q >>= 2;
+    const int w = (int)(q & 3);
+    q >>= 2;
     const int kt = (int)(q % KT);
     const int nb = (int)(q / KT);
+    const int r = 32 * w + (l & 31);  // row of the output block
+    const int c = fp8 ? 4 * (j >> 1) + 2 * (l >> 5) + (j & 1) : 2 * j + (l >> 5);
     int row;
     // gate/up: 16-row groups alternate gate and up: group 2w holds gate rows
     // 64nb+16w.., group 2w+1 the matching up rows
     if (gateup) row = ((r >> 4) & 1 ? half_rows : 0) + nb * 64 + (r >> 5) * 16 + (r & 15);
     else row = nb * 128 + r;
-    const int c = p ^ (r & 7);
     dst[o] = src[s * per_slot + (size_t)row * row_chunks + kt * 8 + c];
   }
 }
@@ -78,9 +86,9 @@ hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& nat
   const int g13 = (int)((n13 + 255) / 256 < 65536 ? (n13 + 255) / 256 : 65536);
   const int g2 = (int)((n2 + 255) / 256 < 65536 ? (n2 + 255) / 256 : 65536);
   hipLaunchKernelGGL(k_pack, dim3(g13), dim3(256), 0, st, static_cast<const uint4*>(nat.w13),
-                     static_cast<uint4*>(const_cast<void*>(pk.w13)), s.S, 2 * s.I, rc13, 1, s.I);
+                     static_cast<uint4*>(const_cast<void*>(pk.w13)), s.S, 2 * s.I, rc13, 1, s.I, es == 1);
   hipLaunchKernelGGL(k_pack, dim3(g2), dim3(256), 0, st, static_cast<const uint4*>(nat.w2),
-                     static_cast<uint4*>(const_cast<void*>(pk.w2)), s.S, s.H, rc2, 0, 0);
+                     static_cast<uint4*>(const_cast<void*>(pk.w2)), s.S, s.H, rc2, 0, 0, es == 1);
   if (s.dtype == TEMPO_FP8_E4M3) {
     // gate/up: I/64 output blocks x H/128 steps; down: H/128 blocks x I/128 steps
     const size_t m13 = (size_t)s.S * (s.I / 64) * (s.H / 128), m2 = (size_t)s.S * (s.H / 128) * (s.I / 128);

@@ -171,42 +171,62 @@ def test_forward_full_size_sampled(name, plan):
     assert np.all((st > 0) == (d["slot_counts"] > 0))
 
 
-def test_pack_layout():
-    """The packed weight layout: per slot, output block by output block, each
-    128-byte contraction step a 16 KB tile of 128 rows x 8 chunks of 16
-    bytes, chunk c of row r at position c ^ (r & 7); gate/up blocks pair gate
-    rows n..n+63 with up rows I+n..I+n+63, interleaved in groups of 16."""
+def _expect_packed(w, rows_of_block, nblk, fp8):
+    """Packed layout: per slot, output block by output block, contraction
+    step by step (128 bytes of every row), four 4 KB pieces (wavefront w:
+    rows 32w..32w+31), each four 1 KB loads; load j, lane l holds 16-byte
+    chunk c(j, l) of row 32w + (l % 32): bf16 c = 2j + l // 32, fp8
+    c = 4 (j // 2) + 2 (l // 32) + j % 2."""
+    S_, R, C = w.shape
+    per = 16 // w.itemsize
+    ch = w.reshape(S_, R, C // per, per)  # 16-byte chunks
+    KT = C // (128 // w.itemsize)
+    out = np.empty((S_, nblk, KT, 4, 4, 64, per), w.dtype)
+    for nb in range(nblk):
+        rows = rows_of_block(nb)
+        for kt in range(KT):
+            for wv in range(4):
+                for j in range(4):
+                    for l in range(64):
+                        c = 4 * (j // 2) + 2 * (l // 32) + j % 2 if fp8 else 2 * j + l // 32
+                        out[:, nb, kt, wv, j, l] = ch[:, rows[32 * wv + l % 32], kt * 8 + c]
+    return out.reshape(S_, -1)
+
+
+def _gu_rows(I):
+    def rows(nb):  # 16-row groups alternate gate and the matching up rows
+        return [(I if (r // 16) % 2 else 0) + nb * 64 + (r // 32) * 16 + r % 16 for r in range(128)]
+    return rows
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+def test_pack_layout(dtype):
+    """The packed weight layout (MFMA operand order, one wavefront's 32 rows
+    per 4 KB piece); gate/up blocks pair gate rows n..n+63 with up rows
+    I+n..I+n+63, interleaved in groups of 16."""
     import torch
     from paper_2608_13057_amd import moe
 
     rng = np.random.default_rng(3)
     S, H, I = 2, 256, 384
-    shape = moe.MoEShape(T=4, K=1, E=2, S=S, H=H, I=I)
-    w13 = rng.integers(0, 2**16, size=(S, 2 * I, H), dtype=np.uint16)
-    w2 = rng.integers(0, 2**16, size=(S, H, I), dtype=np.uint16)
-    pk = moe.pack_weights(shape, moe.WeightTensors(to_dev(w13), to_dev(w2)))
+    fp8 = dtype == "fp8"
+    shape = moe.MoEShape(T=4, K=1, E=2, S=S, H=H, I=I, dtype=dtype)
+    if fp8:
+        w13 = rng.integers(0, 256, size=(S, 2 * I, H), dtype=np.uint8)
+        w2 = rng.integers(0, 256, size=(S, H, I), dtype=np.uint8)
+        s13 = np.ones((S, 2 * I // 128, H // 128), np.float32)
+        s2 = np.ones((S, H // 128, I // 128), np.float32)
+        nat = moe.WeightTensors(to_dev(w13), to_dev(w2), to_dev(s13), to_dev(s2))
+    else:
+        w13 = rng.integers(0, 2**16, size=(S, 2 * I, H), dtype=np.uint16)
+        w2 = rng.integers(0, 2**16, size=(S, H, I), dtype=np.uint16)
+        nat = moe.WeightTensors(to_dev(w13), to_dev(w2))
+    pk = moe.pack_weights(shape, nat)
     torch.cuda.synchronize()
-
-    def expect(w, rows_of_block, nblk):
-        S_, R, C = w.shape
-        ch = w.reshape(S_, R, C // 8, 8)  # 16-byte chunks of 8 bf16
-        KT = C // 64
-        out = np.empty((S_, nblk, KT, 128, 8, 8), np.uint16)
-        for nb in range(nblk):
-            rows = rows_of_block(nb)
-            for kt in range(KT):
-                for r in range(128):
-                    for p in range(8):
-                        out[:, nb, kt, r, p] = ch[:, rows[r], kt * 8 + (p ^ (r & 7))]
-        return out.reshape(S_, -1)
-
-    def gu_rows(nb):  # 16-row groups alternate gate and the matching up rows
-        return [(I if (r // 16) % 2 else 0) + nb * 64 + (r // 32) * 16 + r % 16 for r in range(128)]
-
-    e13 = expect(w13, gu_rows, I // 64)
-    e2 = expect(w2, lambda nb: list(range(nb * 128, nb * 128 + 128)), H // 128)
-    assert np.array_equal(to_host(pk.w13).reshape(S, -1), e13)
-    assert np.array_equal(to_host(pk.w2).reshape(S, -1), e2)
+    e13 = _expect_packed(w13, _gu_rows(I), I // 64, fp8)
+    e2 = _expect_packed(w2, lambda nb: list(range(nb * 128, nb * 128 + 128)), H // 128, fp8)
+    assert np.array_equal(to_host(pk.w13).reshape(S, -1).view(w13.dtype), e13)
+    assert np.array_equal(to_host(pk.w2).reshape(S, -1).view(w2.dtype), e2)
 
 
 def test_pack_fp8_scales():
