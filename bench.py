@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_decode_bf16")
     ap.add_argument("--plan", default=None)
-    ap.add_argument("--m-tile", type=int, default=128)
+    ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, else 128")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copies", type=int, default=0, help="weight copies rotated per step (0 = auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -167,7 +167,10 @@ def main():
     from paper_2608_13057_amd import moe, synth
     from paper_2608_13057_amd.moe import to_device as to_dev
 
+    from paper_2608_13057_amd import measure
+
     wl = synth.make_workload(args.workload, seed=args.seed)
+    args.m_tile = args.m_tile or measure.auto_m_tile(wl)
     plan_name = args.plan or next(iter(wl.plans))
     plan = wl.plans[plan_name]
     log(f"workload {args.workload} plan {plan_name} T={wl.T} K={wl.K} E={wl.E} S={wl.S} H={wl.H} I={wl.I}")
@@ -236,7 +239,9 @@ def main():
     ms_per_step = ev_a.elapsed_time(ev_b) / K
 
     # (2) per-kernel times: K eager steps with HIP events between the stages
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(K)]
+    # and around the two GEMM kernels, all on the stream the kernels run on
+    NE = moe.STAGE_EVENTS
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(NE)] for _ in range(K)]
     for e in evs:
         for x_ in e:
             x_.record()
@@ -245,22 +250,29 @@ def main():
     for i in range(K):
         fwd[i % copies](stage_events=evs[i])
     torch.cuda.synchronize()
-    st = np.array([[evs[i][j].elapsed_time(evs[i][j + 1]) for j in range(4)] for i in range(K)])  # ms
-    eager_ms = evs[0][0].elapsed_time(evs[K - 1][4]) / K
-    stage_us = {n: float(st[:, j].mean() * 1e3) for j, n in enumerate(("dispatch", "gate_up", "down", "combine"))}
-    log(f"graph ms/step {ms_per_step:.4f} eager(events) ms/step {eager_ms:.4f} stages_us {stage_us}")
+    at = np.array([[evs[i][0].elapsed_time(evs[i][j]) for j in range(NE)] for i in range(K)]) * 1e3  # us
+    eager_ms = evs[0][0].elapsed_time(evs[K - 1][NE - 1]) / K
+    stage_us = {
+        "dispatch": float(np.mean(at[:, 1])),
+        "gate_up": float(np.mean(at[:, 3] - at[:, 1])),
+        "down": float(np.mean(at[:, 5] - at[:, 3])),
+        "combine": float(np.mean(at[:, 6] - at[:, 5])),
+    }
+    kernel_us = {"gate_up_gemm": float(np.mean(at[:, 2] - at[:, 1])), "down_gemm": float(np.mean(at[:, 4] - at[:, 3]))}
+    log(f"graph ms/step {ms_per_step:.4f} eager(events) ms/step {eager_ms:.4f} stages_us {stage_us} kernels_us {kernel_us}")
     copy_gbs = attainable_copy_gbs(torch, spin)
     log(f"attainable copy bandwidth {copy_gbs:.0f} GB/s")
 
-    gu_s = st[:, 1].mean() * 1e-3
-    dn_s = st[:, 2].mean() * 1e-3
+    gu_s = kernel_us["gate_up_gemm"] * 1e-6
+    dn_s = kernel_us["down_gemm"] * 1e-6
     gu_bytes = gemm_bytes(wl, wl.dtype, G, N, "gateup")
     dn_bytes = gemm_bytes(wl, wl.dtype, G, N, "down")
-    block_bytes = gu_bytes + dn_bytes
+    traffic, traffic_current = measure.committed_traffic(args.workload, args.m_tile)
     roof = {"bound": "hbm", "achieved": gu_bytes / gu_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gu_bytes / gu_s / 1e9 / HBM_PEAK_GBS, "traffic": None,
-            "kernel": "k_gemm_bf16<gate_up>" if wl.dtype == "bf16" else "k_gemm_fp8<gate_up>",
-            "bytes_per_launch": gu_bytes}
+            "frac": gu_bytes / gu_s / 1e9 / HBM_PEAK_GBS,
+            "traffic": traffic if traffic_current else None,
+            "kernel": f"tempo::gemm::k_gemm<{'true' if wl.dtype != 'bf16' else 'false'}, {args.m_tile}, true> (gate/up)",
+            "bytes_per_launch": gu_bytes, "launch_us": kernel_us["gate_up_gemm"]}
     mfma = {
         "gate_up_tflops": gemm_flops(wl, N, "gateup") / gu_s / 1e12,
         "down_tflops": gemm_flops(wl, N, "down") / dn_s / 1e12,
@@ -289,9 +301,10 @@ def main():
         },
         "roofline": roof,
         "stages_us": stage_us,
+        "kernels_us": kernel_us,
         "eager_ms_per_step": eager_ms,
         "attainable_copy_gbs": copy_gbs,
-        "block_hbm_gbs": block_bytes / ((gu_s + dn_s)) / 1e9,
+        "stage2_hbm_gbs": (gu_bytes + dn_bytes) / (gu_s + dn_s) / 1e9,
         "mfma": mfma,
     }
     if not args.no_cpu_baseline:

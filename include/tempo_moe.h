@@ -73,7 +73,7 @@ extern "C" {
  *   S        local expert slots (replicas held by this GPU), 1 <= S <= 256
  *   H, I     hidden and expert-intermediate sizes, multiples of 128
  *   m_tile   M-tile: every activated slot's rows are padded to a multiple of
- *            it (Sec. 2.2, Eq. 2); 64 or 128
+ *            it (Sec. 2.2, Eq. 2); 64, 128 or 256
  *   dtype    TEMPO_BF16 or TEMPO_FP8_E4M3 (activations and weights)
  */
 typedef struct tempo_moe_shape {
@@ -238,10 +238,14 @@ int tempo_moe_combine(const tempo_moe_shape* shape, const int32_t* pair_row, con
  * first stage-2 tile that started on it to the last that ended, measured
  * with the GPU's 100 MHz real-time counter (0 for slots with c_s = 0).
  * Spans of concurrently running slots overlap; it is exact for one slot.
- * stage_events: nullable host array of 5 hipEvent_t (created by the caller)
- * recorded on `stream` before stage 1, after stage 1, after the gate/up GEMM,
- * after the down GEMM and after stage 3, for per-stage timing.
+ * stage_events: nullable host array of TEMPO_STAGE_EVENTS (7) hipEvent_t
+ * (created by the caller) recorded on `stream` before stage 1, after stage 1,
+ * after the gate/up GEMM kernel, after the whole gate/up step (split-item
+ * fixup and, for fp8, the re-quantisation of h), after the down GEMM kernel,
+ * after the whole down step and after stage 3, for per-stage and per-kernel
+ * timing.
  */
+#define TEMPO_STAGE_EVENTS 7
 int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
                       const float* topk_w, const void* x, const float* x_scale, const tempo_expert_weights* weights,
                       const tempo_dispatch_out* disp, void* y, uint64_t* slot_time_ns, void* const* stage_events,

@@ -73,7 +73,7 @@ static int check_shape(const tempo_moe_shape* s) {
     return TEMPO_EINVAL;
   if (s->K > kMaxK || s->K > s->E || s->E > kMaxE || s->S > kMaxS) return TEMPO_EINVAL;
   if (s->H % 128 || s->I % 128) return TEMPO_EINVAL;
-  if (s->m_tile != 64 && s->m_tile != 128) return TEMPO_EINVAL;
+  if (s->m_tile != 64 && s->m_tile != 128 && s->m_tile != 256) return TEMPO_EINVAL;
   if (s->dtype != TEMPO_BF16 && s->dtype != TEMPO_FP8_E4M3) return TEMPO_EINVAL;
   // row indices and element offsets stay within int32 / the addressable range
   const long long P = (long long)s->T * s->K;
@@ -209,9 +209,9 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   hipStream_t st = static_cast<hipStream_t>(stream);
   const bool timing = slot_time_ns != nullptr;
   void* y_perm = ws + L.y_perm;
-  hipEvent_t ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t ev[TEMPO_STAGE_EVENTS] = {};
   if (stage_events)
-    for (int i = 0; i < 5; i++) ev[i] = static_cast<hipEvent_t>(stage_events[i]);
+    for (int i = 0; i < TEMPO_STAGE_EVENTS; i++) ev[i] = static_cast<hipEvent_t>(stage_events[i]);
   auto mark = [&](int i) { return !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!mark(0)) return TEMPO_EDEVICE;
@@ -222,14 +222,14 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, !gemm_gathers, st);
   if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
   e = shape->dtype == TEMPO_BF16
-          ? launch_experts_bf16(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev[2], st)
-          : launch_experts_fp8(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev[2], st);
+          ? launch_experts_bf16(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev + 2, st)
+          : launch_experts_fp8(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev + 2, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
-  if (e != hipSuccess || !mark(3)) return TEMPO_EDEVICE;
+  if (e != hipSuccess || !mark(5)) return TEMPO_EDEVICE;
   e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,
                      reinterpret_cast<const uint64_t*>(ws + L.slot_t0),
                      reinterpret_cast<const uint64_t*>(ws + L.slot_t1), slot_time_ns, st);
-  if (e != hipSuccess || !mark(4)) return TEMPO_EDEVICE;
+  if (e != hipSuccess || !mark(6)) return TEMPO_EDEVICE;
   return TEMPO_OK;
 }
 

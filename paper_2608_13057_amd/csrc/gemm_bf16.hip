@@ -10,7 +10,7 @@ using namespace gemm;
 
 template <int BM>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                      hipStream_t st) {
   const int grid = persistent_grid(1);
   GemmArgs a{};
@@ -36,9 +36,11 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.C = h;
   gu.Kd = s.H;
   gu.Nout = s.I;
+  auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   hipLaunchKernelGGL((k_gemm<false, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
+  if (!mark(0)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<false, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
-  if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
+  if (!mark(1)) return hipErrorLaunchFailure;
 
   // down -> y_perm [row_cap, H] bf16
   GemmArgs dn = a;
@@ -49,6 +51,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.Kd = s.I;
   dn.Nout = s.H;
   hipLaunchKernelGGL((k_gemm<false, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
+  if (!mark(2)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<false, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }
@@ -66,14 +69,15 @@ bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L) {
   const long long max_tiles = L.row_cap / s.m_tile;
   const long long wfull = W_BASE + s.m_tile / 32, wmin = W_BASE + 1;
   const long long tiles = (max_tiles * wfull + wpx * wmin - 1) / (wpx * wmin) + 2;
-  return tiles <= NROWT;
+  return tiles <= nrowt_of(s.m_tile);
 }
 
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                                hipStream_t st) {
-  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
-  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
+  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 256) return launch_bm<256>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   return hipErrorInvalidValue;
 }
 

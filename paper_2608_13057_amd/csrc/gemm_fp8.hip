@@ -40,7 +40,7 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
 
 template <int BM>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                      hipStream_t st) {
   const int grid = persistent_grid(1);
   GemmArgs a{};
@@ -71,11 +71,13 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.C = h32;
   gu.Kd = s.H;
   gu.Nout = s.I;
+  auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   hipLaunchKernelGGL((k_gemm<true, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
+  if (!mark(0)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
   hipLaunchKernelGGL(k_quant_h, dim3(ceil_div(L.row_cap, 4)), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
-  if (mid && hipEventRecord(mid, st) != hipSuccess) return hipErrorLaunchFailure;
+  if (!mark(1)) return hipErrorLaunchFailure;
 
   // down -> y_perm [row_cap, H] bf16
   GemmArgs dn = a;
@@ -89,6 +91,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.Kd = s.I;
   dn.Nout = s.H;
   hipLaunchKernelGGL((k_gemm<true, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
+  if (!mark(2)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }
@@ -98,10 +101,11 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
 bool experts_supported(const tempo_moe_shape&) { return true; }
 
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, hipEvent_t mid,
+                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                               hipStream_t st) {
-  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
-  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, mid, st);
+  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 256) return launch_bm<256>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   return hipErrorInvalidValue;
 }
 

@@ -9,8 +9,8 @@
 // Work decomposition (stream-K over fixed contraction chunks).  A work item
 // is one (M-tile, output block of 128 weight rows) pair; its contraction of
 // KT steps (128 bytes of every row per step) is cut into C <= 8 fixed chunks
-// of SPC steps, SPC a multiple of the pipeline depth DR (the last chunk is
-// padded with empty steps to a multiple of DR).  The chunks of all items,
+// of SPC steps, SPC a multiple of CQ = 8 for every tile size (the last chunk
+// is padded with empty steps to a multiple of the pipeline depth DR).  The chunks of all items,
 // item by item, form one sequence that is split into contiguous ranges, one
 // per workgroup (one workgroup per CU).  Range boundaries balance estimated
 // time rather than chunk counts: a chunk of an M-tile with m live row blocks
@@ -69,7 +69,8 @@ namespace tempo {
 namespace gemm {
 
 constexpr int NQ = 8;           // ring slots at most (the one being multiplied + the ones in flight)
-constexpr int NROWT = 16;       // row tables (M-tiles) per workgroup range for the in-GEMM gather
+// row tables (M-tiles) per workgroup range for the in-GEMM gather
+__host__ __device__ constexpr int nrowt_of(int bm) { return bm >= 256 ? 8 : 16; }
 constexpr int CMAX = 8;         // contraction chunks per work item (at most)
 constexpr int PART_TILE = 128;  // columns of a partial tile (the 128 weight rows of an item)
 // fixup record of a GEMM workgroup: source count (-1: nothing to complete),
@@ -112,7 +113,12 @@ struct GemmArgs {
 #ifndef TEMPO_DR128
 #define TEMPO_DR128 4
 #endif
-__host__ __device__ constexpr int gemm_dr(int bm) { return bm == 64 ? TEMPO_DR64 : TEMPO_DR128; }
+__host__ __device__ constexpr int gemm_dr(int bm) { return bm == 64 ? TEMPO_DR64 : bm == 128 ? TEMPO_DR128 : 2; }
+// Chunks are whole multiples of CQ steps for every tile size, so that the
+// fixed summation order (the chunk boundaries) is the same whichever M-tile
+// the rows land in; each DR divides CQ.
+constexpr int CQ = 8;
+static_assert(CQ % gemm_dr(64) == 0 && CQ % gemm_dr(128) == 0 && CQ % gemm_dr(256) == 0, "DR divides CQ");
 
 // Work geometry; identical in the GEMM and in its fixup kernel.  Chunks are
 // whole multiples of DR steps (the register ring is indexed by step mod DR at
@@ -203,7 +209,7 @@ __device__ __forceinline__ Geo make_geo(int KT, int NB, int NT, int b, int grid,
   Geo g;
   constexpr int DR = gemm_dr(BM);
   g.KT = KT;
-  g.SPC = ((KT + CMAX - 1) / CMAX + DR - 1) / DR * DR;
+  g.SPC = ((KT + CMAX - 1) / CMAX + CQ - 1) / CQ * CQ;
   g.C = (KT + g.SPC - 1) / g.SPC;
   g.SL = (KT - (g.C - 1) * g.SPC + DR - 1) / DR * DR;
   g.KTV = (g.C - 1) * g.SPC + g.SL;
@@ -246,14 +252,16 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   constexpr int MI = BM / 32;               // row blocks of 32
   constexpr int AG = BM / 32;               // activation 8-row groups per wavefront
   constexpr int DR = gemm_dr(BM);
-  constexpr int EXTRA = FP8 ? 640 : 0;      // fp8: BM activation scales (<= 512 B), then 4 weight-scale words
+  constexpr int EXTRA = FP8 ? BM * 4 + 128 : 0;  // fp8: BM activation scales, then 4 weight-scale words
   constexpr int NCOLS = GATEUP ? 64 : 128;  // output columns per item
   constexpr int BK = FP8 ? 128 : 64;        // contraction elements per step
   constexpr int NSL = DR + 1;               // activation ring slots
   constexpr int SLOT_MAX = BM * ROWB + EXTRA;
   constexpr int OUT_ES = GATEUP && FP8 ? 4 : 2;    // bytes per output element
   constexpr int ROW_OUT = NCOLS * OUT_ES;           // bytes of an item's output row: 128 or 256
-  constexpr int STG_BYTES = BM * ROW_OUT;           // an item's output rows, staged for coalesced stores
+  constexpr int STG_ROWS = BM < 128 ? BM : 128;     // output rows staged at a time (coalesced stores)
+  constexpr int STG_BYTES = STG_ROWS * ROW_OUT;
+  constexpr int NROWT = nrowt_of(BM);
 
   __shared__ __attribute__((aligned(1024))) char ring[NSL * SLOT_MAX];
   __shared__ __attribute__((aligned(16))) char stg[STG_BYTES];
@@ -386,7 +394,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
           if (wave == 3) {
             if (lane < BM / 4) lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES);
           } else if (wave == 2) {
-            if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + 512);
+            if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + BM * 4);
           }
         }
         wp = reinterpret_cast<const i32x4*>(w_base + (size_t)is_kt * B_BYTES);
@@ -434,6 +442,39 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
     }
   };
 
+  // Epilogue of a finished item: rows [r][NCOLS] into the staging area, then
+  // out as whole rows (STG_ROWS rows at a time).
+  auto finish = [&](const f32x16 (&v)[MI], int live, int nvalid, int row0, int nb) {
+    const int rb = 4 * (lane >> 5);
+#pragma unroll
+    for (int h = 0; h < BM / STG_ROWS; h++) {
+      if (h * STG_ROWS >= nvalid) break;
+      if (h > 0) barrier_nofence();  // every wavefront is done reading the previous rows
+#pragma unroll
+      for (int mi = h * (STG_ROWS / 32); mi < (h + 1) * (STG_ROWS / 32); mi++) {
+        if (mi >= live) break;
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+          const int r = rb + (mi - h * (STG_ROWS / 32)) * 32 + 8 * (i >> 2) + (i & 3);
+          if (GATEUP) {
+            // lanes l and l ^ 16 hold the gate and the up value of one column
+            const float up = __shfl_xor(v[mi][i], 16);
+            if ((lane & 16) == 0) {
+              const float hv = silu_mul(v[mi][i], up);
+              const int o = r * NCOLS + wave * 16 + (lane & 15);
+              if (FP8) reinterpret_cast<float*>(stg)[o] = hv;
+              else reinterpret_cast<uint16_t*>(stg)[o] = f32_to_bf16_rne(hv);
+            }
+          } else {
+            reinterpret_cast<uint16_t*>(stg)[r * NCOLS + wave * 32 + (lane & 31)] = f32_to_bf16_rne(v[mi][i]);
+          }
+        }
+      }
+      flush_rows(static_cast<char*>(p.C) + ((size_t)(row0 + h * STG_ROWS) * p.Nout + (size_t)nb * NCOLS) * OUT_ES,
+                 (size_t)p.Nout * OUT_ES, min(nvalid - h * STG_ROWS, STG_ROWS));
+    }
+  };
+
   // the first DR steps (F is a multiple of DR)
   static_for<DR>([&](auto dd) { issue(dd); });
 
@@ -446,24 +487,30 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
       // every fragment read of the step first, then the MFMAs (the scheduling
       // barrier keeps the reads from being spread between the MFMAs, which
       // would expose the LDS latency once per read)
-      bf16x8 a[MI][4];
+      // (in groups of at most four row blocks, to bound the registers held)
+      constexpr int GB = MI < 4 ? MI : 4;
 #pragma unroll
-      for (int mi = 0; mi < MI; mi++)
-        if (mi < live)
+      for (int m0 = 0; m0 < MI; m0 += GB) {
+        if (m0 >= live) break;
+        bf16x8 a[GB][4];
 #pragma unroll
-          for (int ks = 0; ks < 4; ks++)
-            a[mi][ks] = *reinterpret_cast<const bf16x8*>(st + swz(mi * 32 + bcol, 2 * ks + (lane >> 5)));
-      __builtin_amdgcn_sched_barrier(0);
+        for (int j = 0; j < GB; j++)
+          if (m0 + j < live)
 #pragma unroll
-      for (int mi = 0; mi < MI; mi++)
-        if (mi < live)
+            for (int ks = 0; ks < 4; ks++)
+              a[j][ks] = *reinterpret_cast<const bf16x8*>(st + swz((m0 + j) * 32 + bcol, 2 * ks + (lane >> 5)));
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int ks = 0; ks < 4; ks++)
-            acc[mi] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][ks], reinterpret_cast<const bf16x8&>(wr[d][ks]),
-                                                             acc[mi], 0, 0, 0);
+        for (int j = 0; j < GB; j++)
+          if (m0 + j < live)
+#pragma unroll
+            for (int ks = 0; ks < 4; ks++)
+              acc[m0 + j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  a[j][ks], reinterpret_cast<const bf16x8&>(wr[d][ks]), acc[m0 + j], 0, 0, 0);
+      }
     } else {
       const float* sa_lds = reinterpret_cast<const float*>(st + A_BYTES);
-      const float* sw_lds = sa_lds + 128;
+      const float* sw_lds = sa_lds + BM;
       // gate/up: lanes with bit 4 clear hold gate columns, the others up columns
       const float sw = GATEUP ? sw_lds[(lane >> 4) & 1] : sw_lds[0];
       const i32x8 b0 = (i32x8){wr[d][0][0], wr[d][0][1], wr[d][0][2], wr[d][0][3],
@@ -565,30 +612,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
         }
         if (piece_end) {
           if (c == g.C - 1) {
-            // the whole item is here: epilogue, rows [r][NCOLS] into the staging area
-            const int rb = 4 * (lane >> 5);
-#pragma unroll
-            for (int mi = 0; mi < MI; mi++) {
-              if (mi >= live) break;
-#pragma unroll
-              for (int i = 0; i < 16; i++) {
-                const int r = rb + mi * 32 + 8 * (i >> 2) + (i & 3);
-                if (GATEUP) {
-                  // lanes l and l ^ 16 hold the gate and the up value of one column
-                  const float up = __shfl_xor(R[mi][i], 16);
-                  if ((lane & 16) == 0) {
-                    const float h = silu_mul(R[mi][i], up);
-                    const int o = r * NCOLS + wave * 16 + (lane & 15);
-                    if (FP8) reinterpret_cast<float*>(stg)[o] = h;
-                    else reinterpret_cast<uint16_t*>(stg)[o] = f32_to_bf16_rne(h);
-                  }
-                } else {
-                  reinterpret_cast<uint16_t*>(stg)[r * NCOLS + wave * 32 + (lane & 31)] = f32_to_bf16_rne(R[mi][i]);
-                }
-              }
-            }
-            flush_rows(static_cast<char*>(p.C) + ((size_t)row0 * p.Nout + (size_t)nb * NCOLS) * OUT_ES,
-                       (size_t)p.Nout * OUT_ES, nvalid);
+            finish(R, live, nvalid, row0, nb);  // the whole item is here
           } else {
             store_tile(part_mine, R, live);  // running sum of chunks 0..c
           }

@@ -57,16 +57,17 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
                            const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
                            const Layout& L, bool timing, bool gather_rows, hipStream_t st);
 
-// mid_event (nullable) is recorded between the gate/up and the down GEMM.
+// ev: null, or 3 events (each nullable) recorded after the gate/up GEMM
+// kernel, after the gate/up step and after the down GEMM kernel.
 // x_rows: null -> the gate/up GEMM reads d.x_perm; otherwise it reads the
 // activation rows x_rows[row_token[row]] (x_rows = the unpermuted x).
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                                const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
-                               hipEvent_t mid_event, hipStream_t st);
+                               const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
-                              hipEvent_t mid_event, hipStream_t st);
+                              const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,

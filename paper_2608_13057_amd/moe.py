@@ -251,12 +251,18 @@ def combine(shape: MoEShape, pair_row, topk_w, y_perm, y, stream=None):
     return y
 
 
+# events of tempo_moe_forward's stage_events (TEMPO_STAGE_EVENTS)
+STAGE_EVENTS = 7
+
+
 def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, weights: WeightTensors,
             disp: DispatchBuffers, y, ws: Workspace, slot_time_ns=None, stage_events=None, stream=None):
     """Stages 1-3 (tempo_moe_forward): writes y [T, H] bf16 (int16 bits);
     weights must be packed (pack_weights).
-    stage_events: optional list of 5 torch.cuda.Event (created with
-    enable_timing=True) recorded around the stages."""
+    stage_events: optional list of STAGE_EVENTS (7) torch.cuda.Event (created
+    with enable_timing=True) recorded before stage 1, after stage 1, after the
+    gate/up GEMM kernel, after the gate/up step, after the down GEMM kernel,
+    after the down step and after stage 3."""
     _check_inputs(shape, topk_ids, x, x_scale)
     _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
     _check_plan(shape, plan)
@@ -268,9 +274,9 @@ def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, we
     sh, pl, w, do = shape.c(), plan.c(), weights.c(), disp.c()
     evs = None
     if stage_events is not None:
-        if len(stage_events) != 5:
-            raise ValueError("stage_events must hold 5 events")
-        evs = (ctypes.c_void_p * 5)(*[_event_handle(e) for e in stage_events])
+        if len(stage_events) != STAGE_EVENTS:
+            raise ValueError(f"stage_events must hold {STAGE_EVENTS} events")
+        evs = (ctypes.c_void_p * STAGE_EVENTS)(*[_event_handle(e) for e in stage_events])
     check(_lib.load().tempo_moe_forward(ctypes.byref(sh), ctypes.byref(pl), _ptr(topk_ids), _ptr(topk_w), _ptr(x),
                                         _ptr(x_scale), ctypes.byref(w), ctypes.byref(do), _ptr(y),
                                         _ptr(slot_time_ns), evs, ws.ptr, ws.nbytes, _stream(stream)),
@@ -304,7 +310,9 @@ class PreparedForward:
     def __call__(self, stage_events=None, stream=None):
         evs = None
         if stage_events is not None:
-            evs = (ctypes.c_void_p * 5)(*[_event_handle(e) for e in stage_events])
+            if len(stage_events) != STAGE_EVENTS:
+                raise ValueError(f"stage_events must hold {STAGE_EVENTS} events")
+            evs = (ctypes.c_void_p * STAGE_EVENTS)(*[_event_handle(e) for e in stage_events])
         check(self._fn(*self._args, evs, *self._tail, _stream(stream)), "tempo_moe_forward")
 
 

@@ -41,7 +41,7 @@ def _local_rows(d_ref, T_valid):
     return np.nonzero(has)[0], np.nonzero(~has)[0]
 
 
-@pytest.mark.parametrize("m_tile", [64, 128])
+@pytest.mark.parametrize("m_tile", [64, 128, 256])
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
 def test_experts_stage_tiny(m_tile, name):
     """Stage 2 alone: y_perm real rows against the oracle's per-row FFN."""
@@ -90,7 +90,7 @@ def test_combine_stage():
         assert np.all(got[Tv:] == 0)
 
 
-@pytest.mark.parametrize("m_tile", [64, 128])
+@pytest.mark.parametrize("m_tile", [64, 128, 256])
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
 def test_forward_tiny(m_tile, name):
     from paper_2608_13057_amd import synth
@@ -114,7 +114,7 @@ def test_forward_tiny(m_tile, name):
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
 def test_forward_split_invariance_bit_exact(name):
     """The same batch under different splits of the replicated experts over
-    their two local slots (and both M-tiles) gives bit-identical y."""
+    their two local slots (and every M-tile) gives bit-identical y."""
     from paper_2608_13057_amd import synth
 
     wl = synth.make_workload(name)
@@ -122,7 +122,7 @@ def test_forward_split_invariance_bit_exact(name):
     outs = []
     for sw in ([1] * 8, [1, 1, 1, 1, 1, 1, 0, 0], [0, 0, 1, 1, 1, 1, 1, 1], [3, 1, 1, 1, 1, 1, 1, 5]):
         wl.plans["p"] = synth.Plan(np.array(sw, np.uint32), base.remote_weight, base.remote_replicas, "p")
-        for m_tile in (64, 128):
+        for m_tile in (64, 128, 256):
             c = Case(wl, "p", m_tile)
             outs.append(_run_forward(c)[0])
     for o in outs[1:]:
@@ -146,16 +146,19 @@ def test_forward_padding_rows_and_empty_batch():
     assert np.all(y0 == 0)
 
 
-@pytest.mark.parametrize("name,plan", [("qwen3_decode_bf16", "token_balancing"), ("qwen3_decode_fp8", "uniform"),
-                                       ("qwen3_decode_fp8", "replica_min"), ("dsv3_decode_fp8", "uniform")])
-def test_forward_full_size_sampled(name, plan):
-    """The full-size workload in the benchmark's launch configuration; y is
-    checked on a seeded sample of tokens (the oracle computes each one)."""
-    from paper_2608_13057_amd import synth
+@pytest.mark.parametrize("name,plan,m_tile", [("qwen3_decode_bf16", "token_balancing", 0),
+                                              ("qwen3_decode_bf16", "token_balancing", 256),
+                                              ("qwen3_decode_fp8", "uniform", 0), ("qwen3_decode_fp8", "replica_min", 0),
+                                              ("dsv3_decode_fp8", "uniform", 0), ("dsv3_decode_fp8", "uniform", 128)])
+def test_forward_full_size_sampled(name, plan, m_tile):
+    """The full-size workload in the benchmark's launch configuration (M-tile
+    0: the one bench.py picks); y is checked on a seeded sample of tokens (the
+    oracle computes each one)."""
+    from paper_2608_13057_amd import measure, synth
 
     wl = synth.make_workload(name)
-    c = Case(wl, plan, 128)
-    print(f"[forward {name}] running", flush=True)
+    c = Case(wl, plan, m_tile or measure.auto_m_tile(wl))
+    print(f"[forward {name} M={c.m_tile}] running", flush=True)
     y, st = _run_forward(c, timing=True)
     d = c.oracle_dispatch()
     loc, none = _local_rows(d, c.T_valid)
