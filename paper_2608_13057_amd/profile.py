@@ -13,6 +13,7 @@ one replica per expert.  Two scopes are timed: "gemm" (stage 2 only: the two
 grouped GEMMs) and "block" (stages 1-3).
 
     python -m paper_2608_13057_amd.profile --dtype bf16 --out sweep.jsonl
+    python -m paper_2608_13057_amd.profile --from-jsonl sweep.jsonl --md summary.md --command "..."
 """
 from __future__ import annotations
 
@@ -173,6 +174,41 @@ def summarize(rows, scope="gemm") -> dict:
     return dict(scope=scope, points=len(R), eq1=clean(e1), eq2=clean(e2), b_ci95=ci)
 
 
+def markdown(rows, title: str, command: str, ns=DEFAULT_N) -> str:
+    """A summary of a sweep: the fits of Eq. 1 / Eq. 2 per scope, the grid of
+    stage-2 times, and the single-slot staircase (every 16th point)."""
+    grid = [r for r in rows if not (r["G"] == 1 and r["n"] not in ns)]
+    out = [f"# Stage-4 profile: {title}", "", "Commands (repo root, MI355X):", "", "```", command, "```", ""]
+    for scope in ("gemm", "block"):
+        if not any(r["scope"] == scope for r in grid):
+            continue
+        sm = summarize(grid, scope)
+        out += [f"## Fit, scope `{scope}` ({sm['points']} grid points)", "",
+                "| model | a (us) | b (us/slot) | c (us) | beta (us/token) | b2 (us/extra tile) | n* = b/beta | mean rel. err | "
+                "max rel. err | rounds |", "|---|---|---|---|---|---|---|---|---|---|"]
+        for k, lab in (("eq1", "Eq. 1"), ("eq2", "Eq. 2 (tiles)")):
+            e = sm[k]
+            b2 = "" if e.get("b2") is None else f"{e['b2']:.3f}"
+            out.append(f"| {lab} | {e['a']:.2f} | {e['b']:.3f} | {e['c']:.2f} | {e['beta']:.5f} | {b2} | "
+                       f"{e['n_star']:.1f} | {e['err_mean']:.3f} | {e['err_max']:.3f} | {e['iterations']} |")
+        lo, med, hi = sm["b_ci95"]
+        out += ["", f"Bootstrap 95% interval of b: {lo:.3f} .. {hi:.3f} us (median {med:.3f}).", ""]
+    g = sorted({r["G"] for r in grid})
+    nn = sorted({r["n"] for r in grid})
+    t = {(r["G"], r["n"]): r["t_us"] for r in grid if r["scope"] == "gemm"}
+    out += ["## Stage-2 time (us), median of the repetitions", "", "| n \\ G | " + " | ".join(map(str, g)) + " |",
+            "|---" * (len(g) + 1) + "|"]
+    for n in nn:
+        out.append(f"| {n} | " + " | ".join(f"{t[(G, n)]:.1f}" if (G, n) in t else "" for G in g) + " |")
+    fine = sorted((r["n"], r["t_us"], r["tiles"]) for r in rows if r["G"] == 1 and r["scope"] == "gemm" and r["n"] not in ns)
+    if fine:
+        out += ["", "## Single slot, n = 1..2048 (every 16th point; the tile staircase of Eq. 2)", "",
+                "| n | tiles | stage-2 us |", "|---|---|---|"]
+        out += [f"| {n} | {tl} | {tu:.1f} |" for n, tu, tl in fine[::16]]
+    out.append("")
+    return "\n".join(out)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--dtype", default="bf16")
@@ -181,7 +217,20 @@ def main():
     ap.add_argument("--reps", type=int, default=30)
     ap.add_argument("--quick", action="store_true", help="small grid")
     ap.add_argument("--fine", action="store_true", help="add the single-slot sweep n = 1..2048")
+    ap.add_argument("--from-jsonl", default=None, help="summarise an earlier sweep instead of running one")
+    ap.add_argument("--md", default=None, help="with --from-jsonl: write a markdown summary here")
+    ap.add_argument("--title", default="")
+    ap.add_argument("--command", default="")
     args = ap.parse_args()
+    if args.from_jsonl:
+        with open(args.from_jsonl) as fh:
+            rows = [json.loads(l) for l in fh if l.strip()]
+        md = markdown(rows, args.title or f"{rows[0]['dtype']}, M-tile {rows[0]['m_tile']}", args.command)
+        if args.md:
+            with open(args.md, "w") as fh:
+                fh.write(md)
+        print(md)
+        return
     Gs, ns = (DEFAULT_G, DEFAULT_N) if not args.quick else ((1, 4, 16), (1, 64, 128, 129, 512, 2048))
     fine = tuple(range(1, 2049)) if args.fine else ()
     rows = run_sweep(args.dtype, args.m_tile, Gs, ns, fine, args.out, args.reps)
