@@ -73,7 +73,7 @@ extern "C" {
  *   S        local expert slots (replicas held by this GPU), 1 <= S <= 256
  *   H, I     hidden and expert-intermediate sizes, multiples of 128
  *   m_tile   M-tile: every activated slot's rows are padded to a multiple of
- *            it (Sec. 2.2, Eq. 2); 64, 128 or 256
+ *            it (Sec. 2.2, Eq. 2); 64, 128, 192 or 256
  *   dtype    TEMPO_BF16 or TEMPO_FP8_E4M3 (activations and weights)
  */
 typedef struct tempo_moe_shape {

@@ -73,7 +73,7 @@ static int check_shape(const tempo_moe_shape* s) {
     return TEMPO_EINVAL;
   if (s->K > kMaxK || s->K > s->E || s->E > kMaxE || s->S > kMaxS) return TEMPO_EINVAL;
   if (s->H % 128 || s->I % 128) return TEMPO_EINVAL;
-  if (s->m_tile != 64 && s->m_tile != 128 && s->m_tile != 256) return TEMPO_EINVAL;
+  if (s->m_tile != 64 && s->m_tile != 128 && s->m_tile != 192 && s->m_tile != 256) return TEMPO_EINVAL;
   if (s->dtype != TEMPO_BF16 && s->dtype != TEMPO_FP8_E4M3) return TEMPO_EINVAL;
   // row indices and element offsets stay within int32 / the addressable range
   const long long P = (long long)s->T * s->K;

@@ -78,6 +78,7 @@ hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_ou
   if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   if (s.m_tile == 256) return launch_bm<256>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 192) return launch_bm<192>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   return hipErrorInvalidValue;
 }
 

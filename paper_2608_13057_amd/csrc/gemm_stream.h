@@ -70,7 +70,7 @@ namespace gemm {
 
 constexpr int NQ = 8;           // ring slots at most (the one being multiplied + the ones in flight)
 // row tables (M-tiles) per workgroup range for the in-GEMM gather
-__host__ __device__ constexpr int nrowt_of(int bm) { return bm >= 256 ? 8 : 16; }
+__host__ __device__ constexpr int nrowt_of(int bm) { return bm >= 192 ? 8 : 16; }
 constexpr int CMAX = 8;         // contraction chunks per work item (at most)
 constexpr int PART_TILE = 128;  // columns of a partial tile (the 128 weight rows of an item)
 // fixup record of a GEMM workgroup: source count (-1: nothing to complete),
@@ -113,12 +113,13 @@ struct GemmArgs {
 #ifndef TEMPO_DR128
 #define TEMPO_DR128 4
 #endif
-__host__ __device__ constexpr int gemm_dr(int bm) { return bm == 64 ? TEMPO_DR64 : bm == 128 ? TEMPO_DR128 : 2; }
+__host__ __device__ constexpr int gemm_dr(int bm) { return bm == 64 ? TEMPO_DR64 : bm <= 192 ? TEMPO_DR128 : 2; }
 // Chunks are whole multiples of CQ steps for every tile size, so that the
 // fixed summation order (the chunk boundaries) is the same whichever M-tile
 // the rows land in; each DR divides CQ.
 constexpr int CQ = 8;
-static_assert(CQ % gemm_dr(64) == 0 && CQ % gemm_dr(128) == 0 && CQ % gemm_dr(256) == 0, "DR divides CQ");
+static_assert(CQ % gemm_dr(64) == 0 && CQ % gemm_dr(128) == 0 && CQ % gemm_dr(192) == 0 && CQ % gemm_dr(256) == 0,
+              "DR divides CQ");
 
 // Work geometry; identical in the GEMM and in its fixup kernel.  Chunks are
 // whole multiples of DR steps (the register ring is indexed by step mod DR at
@@ -259,7 +260,9 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   constexpr int SLOT_MAX = BM * ROWB + EXTRA;
   constexpr int OUT_ES = GATEUP && FP8 ? 4 : 2;    // bytes per output element
   constexpr int ROW_OUT = NCOLS * OUT_ES;           // bytes of an item's output row: 128 or 256
-  constexpr int STG_ROWS = BM < 128 ? BM : 128;     // output rows staged at a time (coalesced stores)
+  // output rows staged at a time (coalesced stores); 64 for 192-row tiles, whose
+  // activation ring takes most of the LDS
+  constexpr int STG_ROWS = BM % 128 == 0 ? 128 : 64;
   constexpr int STG_BYTES = STG_ROWS * ROW_OUT;
   constexpr int NROWT = nrowt_of(BM);
 

@@ -32,7 +32,7 @@ def _compare(case, d_ref, check_rows=True):
 
 @pytest.mark.parametrize("name", ["tiny", "qwen3_decode_bf16", "qwen3_decode_fp8", "dsv3_decode_fp8",
                                   "qwen3_prefill_bf16"])
-@pytest.mark.parametrize("m_tile", [64, 128, 256])
+@pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
 def test_dispatch_workloads_bit_exact(name, m_tile):
     from paper_2608_13057_amd import moe, synth
 
@@ -73,7 +73,7 @@ def test_dispatch_random_bit_exact(seed):
     S = int(rng.integers(1, 40))
     wl = _random_workload(rng, T, K, E, S, "bf16" if seed % 2 == 0 else "fp8")
     T_valid = int(rng.integers(0, T + 1))
-    m_tile = (64, 128, 256)[seed % 3]
+    m_tile = (64, 128, 192, 256)[seed % 4]
     print(f"[dispatch-rand] seed={seed} T={T} K={K} E={E} S={S} Tv={T_valid} M={m_tile}", flush=True)
     c = Case(wl, "rand", m_tile, weights=False, T_valid=T_valid)
     moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)

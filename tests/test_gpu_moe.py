@@ -41,7 +41,7 @@ def _local_rows(d_ref, T_valid):
     return np.nonzero(has)[0], np.nonzero(~has)[0]
 
 
-@pytest.mark.parametrize("m_tile", [64, 128, 256])
+@pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
 def test_experts_stage_tiny(m_tile, name):
     """Stage 2 alone: y_perm real rows against the oracle's per-row FFN."""
@@ -90,7 +90,7 @@ def test_combine_stage():
         assert np.all(got[Tv:] == 0)
 
 
-@pytest.mark.parametrize("m_tile", [64, 128, 256])
+@pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8"])
 def test_forward_tiny(m_tile, name):
     from paper_2608_13057_amd import synth
@@ -122,7 +122,7 @@ def test_forward_split_invariance_bit_exact(name):
     outs = []
     for sw in ([1] * 8, [1, 1, 1, 1, 1, 1, 0, 0], [0, 0, 1, 1, 1, 1, 1, 1], [3, 1, 1, 1, 1, 1, 1, 5]):
         wl.plans["p"] = synth.Plan(np.array(sw, np.uint32), base.remote_weight, base.remote_replicas, "p")
-        for m_tile in (64, 128, 256):
+        for m_tile in (64, 128, 192, 256):
             c = Case(wl, "p", m_tile)
             outs.append(_run_forward(c)[0])
     for o in outs[1:]:
@@ -147,6 +147,7 @@ def test_forward_padding_rows_and_empty_batch():
 
 
 @pytest.mark.parametrize("name,plan,m_tile", [("qwen3_decode_bf16", "token_balancing", 0),
+                                              ("qwen3_decode_bf16", "token_balancing", 192),
                                               ("qwen3_decode_bf16", "token_balancing", 256),
                                               ("qwen3_decode_fp8", "uniform", 0), ("qwen3_decode_fp8", "replica_min", 0),
                                               ("dsv3_decode_fp8", "uniform", 0), ("dsv3_decode_fp8", "uniform", 128)])
