@@ -23,11 +23,17 @@ FLAGS = [
     "-fPIC",
     # no packed-fp32 instructions anywhere in the device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # MFMA accumulators in VGPRs: the stage-2 GEMMs add chunk accumulators
-    # with VALU, and the AGPR form would copy them back and forth every step
-    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wno-unused-result",
 ]
+# MFMA accumulators in VGPRs: the stream-K GEMMs add chunk accumulators with
+# VALU, and the AGPR form would copy them back and forth every step.  The
+# large-tile GEMM (files ending in _agpr.hip) keeps its 256 accumulator
+# registers per lane in AGPRs instead.
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form"]
+
+
+def flags_for(src: str):
+    return FLAGS if src.endswith("_agpr.hip") else FLAGS + VGPR_FORM
 
 
 def sources():
@@ -43,9 +49,9 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
         for src in sources():
             obj = os.path.join(tmp, os.path.basename(src) + ".o")
             objs.append(obj)
-            cmd = [HIPCC, *FLAGS, "-c", src, "-o", obj]
+            cmd = [HIPCC, *flags_for(src), "-c", src, "-o", obj]
             if src.endswith(".cpp"):
-                cmd = [HIPCC, "-x", "hip", *FLAGS, "-c", src, "-o", obj]
+                cmd = [HIPCC, "-x", "hip", *flags_for(src), "-c", src, "-o", obj]
             if verbose:
                 print(" ".join(cmd), flush=True)
             procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)))

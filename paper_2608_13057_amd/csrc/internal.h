@@ -69,6 +69,13 @@ hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out
                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
                               const hipEvent_t* ev, hipStream_t st);
 
+// bf16 with 256-row M-tiles (and H a multiple of 256): both GEMMs as 256 x 256
+// items on MFMA-blocked wavefronts (the large-tile kernel); reads x_perm.
+bool experts_big_supported(const tempo_moe_shape& s);
+hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
+                              void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
+                              hipStream_t st);
+
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
                           uint64_t* slot_time_ns, hipStream_t st);
