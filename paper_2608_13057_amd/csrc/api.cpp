@@ -43,6 +43,8 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + (s.dtype == TEMPO_BF16 ? 0 : (size_t)L.row_cap * s.I * 4));
   L.y_perm = o;
   o = align_up(o + (size_t)L.row_cap * s.H * 2);
+  L.apack = o;
+  o = align_up(o + experts_big_pack_bytes(s, L.row_cap));
   // stage-2 partial tiles: per workgroup of the persistent grid, 8 tiles of
   // m_tile x 128 fp32 (the running sum and the chunks of split work items)
   L.part = o;

@@ -59,7 +59,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
 }  // namespace
 
 bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L) {
-  if (experts_big_supported(s)) return false;  // the large-tile kernel reads x_perm
+  if (experts_big_supported(s)) return true;  // the large-tile kernel packs the token rows itself
   // upper bound of the M-tiles one workgroup range of the gate/up GEMM spans
   const int grid = persistent_grid(1);
   const int NB = s.I / 64;
@@ -79,7 +79,7 @@ hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_ou
   if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   if (s.m_tile == 256) {
-    if (experts_big_supported(s)) return launch_experts_big(s, d, w, y_perm, ws, L, timing, ev, st);
+    if (experts_big_supported(s)) return launch_experts_big(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
     return launch_bm<256>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   }
   if (s.m_tile == 192) return launch_bm<192>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);

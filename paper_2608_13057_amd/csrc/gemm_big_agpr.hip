@@ -4,22 +4,35 @@
 // contraction, so it is organised for MFMA throughput rather than for HBM
 // streaming:
 //
+// * Both operands are packed in MFMA operand order: the weights by
+//   tempo_moe_pack_weights, the activation rows of each 256-row tile by
+//   k_pack_rows below, and the gate/up result h by the gate/up epilogue, in
+//   the layout the down GEMM reads.  One 16-element sub-step of 256 rows is
+//   then eight 1 KB pieces of consecutive bytes, each the fragment of 32
+//   rows that one MFMA operand register quadruple takes.
 // * A work item is one (M-tile of 256 rows, 256 packed weight rows) pair;
 //   items are handed out round-robin to a persistent grid (one workgroup per
-//   CU).  There is no split of the contraction: each item accumulates its
-//   steps in order, so the result of a row depends only on its own inputs.
+//   CU) in an XCD-aware order.  There is no split of the contraction: each
+//   item accumulates its sub-steps in order, so the result of a row depends
+//   only on its own inputs.
 // * Four wavefronts in a 2 x 2 arrangement each own a 128 x 128 block of the
 //   item: 4 x 4 MFMA tiles of 32 x 32 (256 accumulator registers per lane,
-//   kept in AGPRs).  Per 16-element sub-step a wavefront reads 4 activation
-//   and 4 weight fragments from LDS for 16 MFMAs -- half the LDS bytes per
-//   MFMA of the streaming kernel's 1 x 4 arrangement.
-// * A step (128 bytes of every row: 32 KB of activation rows, 32 KB of
-//   weights) goes from global memory into LDS by DMA; two stages, the next
-//   step's DMA issued before the current step's MFMAs.  The packed weight
-//   layout stores each 32-row piece in MFMA operand order, so a weight
-//   fragment read is 1 KB of consecutive LDS bytes.
-// * Epilogue: SwiGLU (gate/up) or the bf16 rounding (down) on the fp32 sums,
-//   staged in LDS and written out as whole rows.
+//   kept in AGPRs).  The MFMAs take the weights as their first operand, so a
+//   tile holds the transposed product: a lane owns one token row and runs of
+//   four consecutive output columns.
+// * The operands stream through an LDS ring of NSS slots of 16 KB, one slot
+//   per sub-step (activations, then weights), filled by DMA.  A slot is
+//   released one sub-step at a time: after each sub-step's barrier the DMA
+//   of the sub-step NSS ahead goes into the slot freed by the previous one,
+//   so the loads leave in an even stream well ahead of their use (a whole
+//   step's burst at once would queue in the vector L1 and arrive late), and
+//   the stream runs on across item boundaries: the next item's first
+//   sub-steps load during this item's epilogue.  Fragments are
+//   double-buffered in registers: the LDS reads of sub-step u + 1 are
+//   interleaved with the MFMAs of sub-step u.
+// * Epilogue straight from the accumulators: SwiGLU (gate/up) into packed h
+//   with 8-byte stores that fill 512 consecutive bytes per instruction, or
+//   the bf16 rows of y_perm (down).
 #include "gemm_stream.h"
 
 namespace tempo {
@@ -27,17 +40,47 @@ namespace {
 
 using namespace gemm;
 
-constexpr int BIG_M = 256;                       // rows per item (the M-tile)
-constexpr int BIG_N = 256;                       // packed weight rows per item (two blocks of 128)
-constexpr int A_STAGE = BIG_M * ROWB;            // 32 KB of activation rows per step
-constexpr int STAGE = A_STAGE + 2 * B_BYTES;     // + two 16 KB weight blocks
+constexpr int BIG_M = 256;             // rows per item (the M-tile)
+constexpr int BIG_N = 256;             // packed weight rows per item (two blocks of 128)
+constexpr int SUB_BYTES = 8 * 1024;    // one 16-element sub-step of 256 rows: eight 1 KB fragment pieces
+constexpr int SLOT = 2 * SUB_BYTES;    // ring slot: the activations, then the weights of one sub-step
+constexpr int NSS = 9;                 // ring slots
+constexpr int BIG_GM = 4;              // M-tiles per group of the item order
+
+// Packed 256-row tile of K-element rows: sub-step u (elements 16u .. 16u+15)
+// at u * SUB_BYTES; in it, piece b (rows 32b .. 32b+31) at b * 1024, where
+// lane l holds row 32b + (l & 31), elements 16u + 8 (l >> 5) .. + 7.
+__host__ __device__ constexpr size_t packed_tile_bytes(int K) { return (size_t)BIG_M * K * 2; }
+
+// The activation rows of every 256-row tile in the packed order, from the
+// token rows (gather: row r is token row_token[r] of A) or from permuted rows
+// (row r of A); padding rows (row_token -1) are zero.  One workgroup per
+// (tile, 64-element step): wavefront w writes sub-step w of the step.
+__global__ __launch_bounds__(256) void k_pack_rows(const char* __restrict__ A, int gather,
+                                                   const int32_t* __restrict__ row_token,
+                                                   const uint32_t* __restrict__ hdr, int max_tiles, int K,
+                                                   char* __restrict__ out) {
+  const int KT = K / 64;
+  const int tile = blockIdx.x / KT, k = blockIdx.x - tile * KT;
+  if (tile >= min((int)hdr[kHdrTiles], max_tiles)) return;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  char* dst = out + (size_t)tile * packed_tile_bytes(K) + (size_t)(4 * k + w) * SUB_BYTES;
+  const size_t row_bytes = (size_t)K * 2;
+  const int col = k * 128 + (2 * w + (lane >> 5)) * 16;
+#pragma unroll
+  for (int b = 0; b < 8; b++) {
+    const int row = tile * BIG_M + 32 * b + (lane & 31);
+    const int tok = row_token[row];
+    i32x4 v = {0, 0, 0, 0};
+    if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + (size_t)(gather ? tok : row) * row_bytes + col);
+    *reinterpret_cast<i32x4*>(dst + b * 1024 + lane * 16) = v;
+  }
+}
 
 template <bool GATEUP>
 __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
   constexpr int NCOLS = GATEUP ? BIG_N / 2 : BIG_N;  // output columns per item
-  constexpr int ROW_OUT = NCOLS * 2;                  // bf16 output bytes per row of an item
-  static_assert(BIG_M * ROW_OUT <= 2 * STAGE, "staged output rows fit in the ring");
-  __shared__ __attribute__((aligned(1024))) char ring[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char ring[NSS * SLOT];
   __shared__ int32_t s_off[kMaxS + 1];
   __shared__ int32_t s_cnt[kMaxS];
 
@@ -50,118 +93,198 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
   for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
   __syncthreads();
   const int NT = __builtin_amdgcn_readfirstlane(min(nt_hdr, p.max_tiles));
-  const int KT = p.Kd / 64;       // steps of 64 bf16
+  const int KT = p.Kd / 64;        // steps of 64 bf16
+  const int NU = 4 * KT;           // sub-steps per item
   const int NBT = p.Nout / NCOLS;  // items per M-tile
   const int items = NT * NBT;
-  const uint32_t a_row_bytes = (uint32_t)p.Kd * 2;
+
+  // Item order.  Workgroups are dealt to the 8 XCDs in turn, so workgroup b
+  // runs on XCD b % 8; each XCD takes a contiguous run of the item list per
+  // round.  The list goes over groups of BIG_GM M-tiles with the tile index
+  // fastest, so the 32 items an XCD runs at once cover 4 M-tiles x 8 weight
+  // column blocks, which its L2 serves from 12 distinct streams.
+  const int G = gridDim.x;
+  const int lin0 = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
+  const int my_items = lin0 < items ? (items - 1 - lin0) / G + 1 : 0;
+  if (my_items == 0) return;
+  auto item_of = [&](int n, int& tile, int& nbt) {
+    const int it = lin0 + n * G;
+    const int grp = it / (BIG_GM * NBT), w_in = it - grp * (BIG_GM * NBT);
+    const int gm = min(BIG_GM, NT - grp * BIG_GM);  // tiles in this group
+    nbt = w_in / gm;
+    tile = grp * BIG_GM + (w_in - nbt * gm);
+  };
+
+  // DMA cursor: the next sub-step to load (item ordinal dn, sub-step du)
+  // and the sources of its item.  Past the last item it keeps loading the
+  // last item's sub-steps, which nobody reads, so that every sub-step issues
+  // the same number of loads and the waits below stay exact.
+  int dn = 0, du = 0;
+  const char* da = nullptr;  // packed activation tile
+  const char* dw = nullptr;  // the item's first packed weight block
+  auto dma_item = [&]() {
+    int tile, nbt;
+    item_of(dn, tile, nbt);
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * BIG_M));
+    da = p.A + (size_t)tile * packed_tile_bytes(p.Kd);
+    dw = p.W + (size_t)slot * p.w_slot_bytes + (size_t)(2 * nbt) * KT * B_BYTES;
+  };
   const uint32_t ring_lds = lds_addr(ring);
-  const int lrow = lane >> 3, gchunk = (lane & 7) ^ (lane >> 3);
+  // This wavefront's share of a sub-step's DMA, as four 1 KB pieces:
+  // activation pieces 2w and 2w + 1, weight pieces 2w and 2w + 1 (block
+  // w >> 1, its 32-row blocks 2 (w & 1) and 2 (w & 1) + 1).  After piece 3
+  // the cursor moves on.
+  auto dma_piece = [&](int slot, int pc) {
+    const uint32_t sl = ring_lds + slot * SLOT;
+    if (pc < 2) {
+      const int b = 2 * wave + pc;
+      lds_dma16s(da + (size_t)du * SUB_BYTES, b * 1024 + lane * 16, sl + b * 1024);
+    } else {
+      const int k = du >> 2, ks = du & 3, q = 2 * (wave & 1) + (pc - 2);
+      const char* wb = dw + (size_t)(wave >> 1) * KT * B_BYTES + (size_t)k * B_BYTES + ks * 1024;
+      lds_dma16s(wb, q * 4096 + lane * 16, sl + SUB_BYTES + (2 * wave + pc - 2) * 1024);
+    }
+    if (pc == 3 && ++du == NU) {
+      du = 0;
+      if (dn + 1 < my_items) {
+        ++dn;
+        dma_item();
+      }
+    }
+  };
+
+  f32x16 acc[4][4];
+  bf16x8 fa[2][4], fb[2][4];
+  auto frag_pair = [&](int slot, int buf, int i) {
+    const char* s = ring + slot * SLOT;
+    fa[buf][i] = *reinterpret_cast<const bf16x8*>(s + (4 * wm + i) * 1024 + lane * 16);
+    fb[buf][i] = *reinterpret_cast<const bf16x8*>(s + SUB_BYTES + (4 * wn + i) * 1024 + lane * 16);
+  };
+
+  // Sub-step g, in ring slot sc = g % NSS, in four groups i = 0..3: the four
+  // MFMAs of row block i interleaved with two LDS reads of sub-step g + 1
+  // (from slot sn), then one DMA piece of sub-step g + NSS - 1 into slot sp =
+  // (g - 1) % NSS, whose sub-step g - 1 every wavefront read before the
+  // previous barrier.  Then, once sub-step g + 2 has landed and every
+  // wavefront holds sub-step g + 1, the barrier.  Loads complete in order,
+  // and NSS - 3 sub-steps of four loads each were issued after sub-step
+  // g + 2.  first: the item's first sub-step, which starts its sums from zero.
+  int sc = 0;
+  auto substep = [&](int buf, bool first) {
+    const int sn = sc + 1 == NSS ? 0 : sc + 1;
+    const int sp = sc == 0 ? NSS - 1 : sc - 1;
+    const f32x16 zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+#pragma unroll
+      for (int j = 0; j < 4; j++)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], first ? zero : acc[i][j], 0, 0, 0);
+      frag_pair(sn, buf ^ 1, i);
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_barrier(0);
+      dma_piece(sp, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    wait_lgkm0();
+    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(4 * (NSS - 3)));
+    barrier_nofence();
+    __builtin_amdgcn_sched_barrier(0);
+    sc = sn;
+  };
+
+  // prologue: sub-steps 0 .. NSS - 2 into slots 0 .. NSS - 2 (the first
+  // sub-step loads NSS - 1 into the last slot); sub-steps 0 and 1 landed
+  // before the first reads
+  dma_item();
+#pragma unroll 1
+  for (int g = 0; g < NSS - 1; g++)
+#pragma unroll
+    for (int pc = 0; pc < 4; pc++) dma_piece(g, pc);
+  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(4 * (NSS - 3)));
+  barrier_nofence();
+#pragma unroll
+  for (int i = 0; i < 4; i++) frag_pair(0, 0, i);
+  __builtin_amdgcn_sched_barrier(0);
 
 #pragma unroll 1
-  for (int it = blockIdx.x; it < items; it += gridDim.x) {
-    const int tile = it / NBT, nbt = it - tile * NBT;
+  for (int n = 0; n < my_items; n++) {
+    int tile, nbt;
+    item_of(n, tile, nbt);
     const int row0 = tile * BIG_M;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     const int nvalid = __builtin_amdgcn_readfirstlane(min(BIG_M, s_off[slot] + s_cnt[slot] - row0));
     uint64_t tstart = 0;
     if (p.timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
 
-    // DMA sources: activation 8-row group g = wave + 4j (rows past the real
-    // ones re-read the last real row); weight piece q = wave + 4j of the two
-    // blocks' 32 1 KB pieces of a step
-    const char* a_base = p.A + (size_t)row0 * a_row_bytes;
-    uint32_t a_voff[8];
-#pragma unroll
-    for (int j = 0; j < 8; j++) {
-      const int r = min((wave + 4 * j) * 8 + lrow, nvalid - 1);
-      a_voff[j] = (uint32_t)r * a_row_bytes + gchunk * 16;
-    }
-    const char* w_base = p.W + (size_t)slot * p.w_slot_bytes + (size_t)(2 * nbt) * KT * B_BYTES;
-    auto issue = [&](int k, int stg) {
-      const uint32_t sl = ring_lds + stg * STAGE;
-      const char* ab = a_base + k * ROWB;
-#pragma unroll
-      for (int j = 0; j < 8; j++) lds_dma16s(ab, a_voff[j], sl + (wave + 4 * j) * 1024);
-#pragma unroll
-      for (int j = 0; j < 8; j++) {
-        const int q = wave + 4 * j;
-        const char* bb = w_base + (size_t)(q >> 4) * KT * B_BYTES + (size_t)k * B_BYTES;
-        lds_dma16s(bb, (q & 15) * 1024 + lane * 16, sl + A_STAGE + q * 1024);
-      }
-    };
-
-    f32x16 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; i++)
-#pragma unroll
-      for (int j = 0; j < 4; j++)
-#pragma unroll
-        for (int e = 0; e < 16; e++) acc[i][j][e] = 0.f;
-
-    barrier_nofence();  // the previous item's output rows have left the ring
-    issue(0, 0);
+    substep(0, true);
+    substep(1, false);
 #pragma unroll 1
-    for (int k = 0; k < KT; k++) {
-      const int stg = k & 1;
-      barrier_nofence();  // every wavefront is done with step k - 1, whose stage step k + 1 reuses
-      if (k + 1 < KT) {
-        issue(k + 1, stg ^ 1);
-        __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(16));  // this wavefront's loads of step k are done
-      } else {
-        __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
-      }
-      barrier_nofence();  // and everyone's
-      const char* st = ring + stg * STAGE;
-#pragma unroll
-      for (int ks = 0; ks < 4; ks++) {
-        bf16x8 a[4], b[4];
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-          a[i] = *reinterpret_cast<const bf16x8*>(st + swz(128 * wm + 32 * i + (lane & 31), 2 * ks + (lane >> 5)));
-#pragma unroll
-        for (int j = 0; j < 4; j++)
-          b[j] = *reinterpret_cast<const bf16x8*>(st + A_STAGE + wn * B_BYTES + j * 4096 + ks * 1024 + lane * 16);
-#pragma unroll
-        for (int i = 0; i < 4; i++)
-#pragma unroll
-          for (int j = 0; j < 4; j++) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
+    for (int u = 2; u < NU; u += 2) {
+      substep(0, false);
+      substep(1, false);
     }
 
-    // epilogue: rows [r][NCOLS] of bf16 into the ring, then out as whole rows
-    barrier_nofence();  // every wavefront is done reading the last step
-    const int rb = 4 * (lane >> 5);
+    // Epilogue.  Lane l of tile (i, j) holds token row 128 wm + 32 i + (l & 31)
+    // and, in element e, packed weight row 8 (e / 4) + 4 (l / 32) + e % 4 of
+    // the 32-row piece j of block wn.  In a gate/up piece rows 0..15 are gate
+    // columns and rows 16..31 the up columns with the same indices, so gate
+    // and up of a column are elements e and e + 8 of one lane.
+    // (the lane index is produced afresh here, so that the compiler keeps no
+    // per-lane store address live across the item loop: a spill reload would
+    // make it wait for every load in flight, the ring's DMA included)
+    int lid;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lid));
+    const int l31 = lid & 31, h = lid >> 5;
+    auto pack4 = [](float v0, float v1, float v2, float v3) {
+      uint2 w;
+      w.x = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+      w.y = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+      return w;
+    };
+    if (GATEUP) {
+      // h column c = 128 nbt + 64 wn + 16 j + 8 q + 4 h + m is element 4 h + m
+      // of 8-column chunk q of sub-step j of the down GEMM's step 2 nbt + wn;
+      // the chunk of row r is lane (r & 31) + 32 q of the piece of rows r / 32
+      char* hb = static_cast<char*>(p.C) + (size_t)tile * packed_tile_bytes(p.Nout);
 #pragma unroll
-    for (int i = 0; i < 4; i++)
+      for (int i = 0; i < 4; i++)
 #pragma unroll
-      for (int j = 0; j < 4; j++)
+        for (int j = 0; j < 4; j++) {
+          const f32x16& v = acc[i][j];
+          char* pb = hb + ((size_t)((2 * nbt + wn) * 4 + j) * 8 + 4 * wm + i) * 1024 + l31 * 16 + 8 * h;
 #pragma unroll
-        for (int e = 0; e < 16; e++) {
-          const int r = 128 * wm + 32 * i + rb + 8 * (e >> 2) + (e & 3);
-          if (GATEUP) {
-            // lanes l and l ^ 16 hold the gate and the up value of one column
-            const float up = __shfl_xor(acc[i][j][e], 16);
-            if ((lane & 16) == 0) {
-              const int col = 64 * wn + 16 * j + (lane & 15);
-              reinterpret_cast<uint16_t*>(ring)[r * NCOLS + col] = f32_to_bf16_rne(silu_mul(acc[i][j][e], up));
-            }
-          } else {
-            const int col = 128 * wn + 32 * j + (lane & 31);
-            reinterpret_cast<uint16_t*>(ring)[r * NCOLS + col] = f32_to_bf16_rne(acc[i][j][e]);
-          }
+          for (int q = 0; q < 2; q++)
+            *reinterpret_cast<uint2*>(pb + q * 512) =
+                pack4(silu_mul(v[4 * q], v[4 * q + 8]), silu_mul(v[4 * q + 1], v[4 * q + 9]),
+                      silu_mul(v[4 * q + 2], v[4 * q + 10]), silu_mul(v[4 * q + 3], v[4 * q + 11]));
+          // one tile at a time: reading every accumulator out at once would
+          // spill, and a spill reload makes the compiler wait for all loads
+          // (the ring's DMA included)
+          __builtin_amdgcn_sched_barrier(0);
         }
-    wait_lgkm0();
-    barrier_nofence();
-    {
-      constexpr int PER = ROW_OUT / 16;  // 16-byte pieces per row
-      char* dst = static_cast<char*>(p.C) + ((size_t)row0 * p.Nout + (size_t)nbt * NCOLS) * 2;
-      const size_t stride = (size_t)p.Nout * 2;
-      int t0 = tid;
-      asm volatile("" : "+v"(t0));
-#pragma unroll 2
-      for (int idx = t0; idx < nvalid * PER; idx += 256) {
-        const int r = idx / PER, c = idx % PER;
-        *reinterpret_cast<i32x4*>(dst + r * stride + c * 16) = *reinterpret_cast<const i32x4*>(ring + r * ROW_OUT + c * 16);
+    } else {
+      const size_t ld = (size_t)p.Nout * 2;
+      char* yb = static_cast<char*>(p.C) + (size_t)row0 * ld + (size_t)(nbt * NCOLS + 128 * wn + 4 * h) * 2;
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int r = 128 * wm + 32 * i + l31;
+        char* yr = yb + r * ld;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          const f32x16& v = acc[i][j];
+          uint2 w[4];
+#pragma unroll
+          for (int q = 0; q < 4; q++) w[q] = pack4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+          if (r < nvalid) {  // padding rows of y_perm stay unwritten
+#pragma unroll
+            for (int q = 0; q < 4; q++) *reinterpret_cast<uint2*>(yr + (32 * j + 8 * q) * 2) = w[q];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
     if (p.timing && tid == 0) {
@@ -170,6 +293,8 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
       atomicMax(reinterpret_cast<unsigned long long*>(&p.t1[slot]), (unsigned long long)tend);
     }
   }
+  // no DMA into this workgroup's LDS may outlive it
+  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
 }
 
 }  // namespace
@@ -178,28 +303,40 @@ bool experts_big_supported(const tempo_moe_shape& s) {
   return s.dtype == TEMPO_BF16 && s.m_tile == BIG_M && s.H % BIG_N == 0 && s.I % 128 == 0;
 }
 
-// Both GEMMs of stage 2 with 256 x 256 items (x_perm must hold the permuted
-// rows: this kernel does not gather).
+size_t experts_big_pack_bytes(const tempo_moe_shape& s, int row_cap) {
+  return experts_big_supported(s) ? (size_t)row_cap * s.H * 2 : 0;
+}
+
+// Both GEMMs of stage 2 with 256 x 256 items.  The activation rows come from
+// x_rows (token rows, gathered through row_token) or, if that is null, from
+// the permuted rows in x_perm.
 hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
-                              hipStream_t st) {
+                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                              const hipEvent_t* ev, hipStream_t st) {
   const int grid = persistent_grid(1);
+  const int max_tiles = L.row_cap / BIG_M;
+  const uint32_t* hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
+  auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
+
+  const char* src = static_cast<const char*>(x_rows ? x_rows : d.x_perm);
+  hipLaunchKernelGGL(k_pack_rows, dim3(max_tiles * (s.H / 64)), dim3(256), 0, st, src, x_rows ? 1 : 0,
+                     d.row_token, hdr, max_tiles, s.H, ws + L.apack);
+
   GemmArgs a{};
   a.slot_counts = d.slot_counts;
   a.slot_offsets = d.slot_offsets;
   a.S = s.S;
-  a.max_tiles = L.row_cap / BIG_M;
-  a.hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
+  a.max_tiles = max_tiles;
+  a.hdr = hdr;
   a.t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   a.t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   a.timing = timing ? 1 : 0;
-  auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
 
   GemmArgs gu = a;
-  gu.A = static_cast<const char*>(d.x_perm);
+  gu.A = ws + L.apack;
   gu.W = static_cast<const char*>(w.w13);
   gu.w_slot_bytes = (size_t)2 * s.I * s.H * 2;
-  gu.C = ws + L.h;
+  gu.C = ws + L.h;  // packed h
   gu.Kd = s.H;
   gu.Nout = s.I;
   hipLaunchKernelGGL(k_gemm_big<true>, dim3(grid), dim3(256), 0, st, gu);

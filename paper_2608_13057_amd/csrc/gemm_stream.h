@@ -226,7 +226,11 @@ __device__ __forceinline__ Geo make_geo(int KT, int NB, int NT, int b, int grid,
   return g;
 }
 
-__device__ __forceinline__ float silu_mul(float g, float u) { return g / (1.0f + __expf(-g)) * u; }
+// SwiGLU of one column: silu(g) * u, with silu(g) = g / (1 + e^-g) taken
+// through the hardware reciprocal (v_rcp_f32, about 1 ulp).
+__device__ __forceinline__ float silu_mul(float g, float u) {
+  return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)) * u;
+}
 
 // Partial tiles are stored lane-native: the 16 accumulator values of lane l
 // of wavefront w for row block mi are 16 consecutive floats at

@@ -35,10 +35,11 @@ struct Layout {
   size_t local_rank;  // [T*K] int32 stable rank of a pair within its block and expert
   size_t slot_t0;     // [S] uint64 first stage-2 tile start (real-time counter)
   size_t slot_t1;     // [S] uint64 last stage-2 tile end
-  size_t h;           // [row_cap, I] bf16 or e4m3
+  size_t h;           // [row_cap, I] bf16 or e4m3 (256-row bf16 tiles: packed in MFMA operand order)
   size_t h_scale;     // [I/128, row_cap] fp32 (fp8 only; scale-block-major)
   size_t h32;         // [row_cap, I] fp32 gate/up output before re-quantisation (fp8 only)
   size_t y_perm;      // [row_cap, H] bf16
+  size_t apack;       // 256-row bf16 tiles only: the activation rows packed in MFMA operand order
   size_t part;        // [grid][8][m_tile][128] fp32 stage-2 partial tiles
   size_t fix;         // [grid][12] int32 stage-2 fixup records
   size_t total;
@@ -70,11 +71,14 @@ hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out
                               const hipEvent_t* ev, hipStream_t st);
 
 // bf16 with 256-row M-tiles (and H a multiple of 256): both GEMMs as 256 x 256
-// items on MFMA-blocked wavefronts (the large-tile kernel); reads x_perm.
+// items on MFMA-blocked wavefronts (the large-tile kernel), with the
+// activation rows first packed into the workspace (experts_big_pack_bytes of
+// it) from x_rows (token rows, through row_token) or, if null, from x_perm.
 bool experts_big_supported(const tempo_moe_shape& s);
+size_t experts_big_pack_bytes(const tempo_moe_shape& s, int row_cap);
 hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
-                              hipStream_t st);
+                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                              const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
@@ -83,10 +87,11 @@ hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, con
 hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& natural,
                        const tempo_expert_weights& packed, hipStream_t st);
 
-// Whether the gate/up GEMM gathers the activation rows itself (through
-// row_token, with the row tables of a workgroup's M-tiles in LDS) rather than
-// reading rows that stage 1 permuted into x_perm: true when every
-// workgroup's range spans few enough M-tiles.
+// Whether stage 2 gathers the activation rows itself (through row_token)
+// rather than reading rows that stage 1 permuted into x_perm: true for the
+// large-tile kernel, whose pack step gathers them, and for the streaming
+// GEMM when every workgroup's range spans few enough M-tiles (the row tables
+// of its M-tiles sit in LDS).
 bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L);
 
 // Whether stage-2 kernels exist for this shape's element type and M-tile.
