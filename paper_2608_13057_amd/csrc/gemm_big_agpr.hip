@@ -29,7 +29,8 @@
 //   the stream runs on across item boundaries: the next item's first
 //   sub-steps load during this item's epilogue.  Fragments are
 //   double-buffered in registers: the LDS reads of sub-step u + 1 are
-//   interleaved with the MFMAs of sub-step u.
+//   interleaved with the MFMAs of sub-step u, and so are the DMA pieces,
+//   at a different point for each wavefront.
 // * Epilogue straight from the accumulators: SwiGLU (gate/up) into packed h
 //   with 8-byte stores that fill 512 consecutive bytes per instruction, or
 //   the bf16 rows of y_perm (down).
@@ -77,22 +78,17 @@ __global__ __launch_bounds__(256) void k_pack_rows(const char* __restrict__ A, i
   }
 }
 
-template <bool GATEUP>
-__global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
+// The GEMM of one wavefront of a workgroup; WV is the wavefront's index.
+// Each of the four wavefronts runs its own instance (chosen once, at the top
+// of the kernel), so that its position in the 2 x 2 arrangement and the
+// point where it issues its DMA are constants.
+template <bool GATEUP, int WV>
+__device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const int32_t* s_off, const int32_t* s_cnt) {
   constexpr int NCOLS = GATEUP ? BIG_N / 2 : BIG_N;  // output columns per item
-  __shared__ __attribute__((aligned(1024))) char ring[NSS * SLOT];
-  __shared__ int32_t s_off[kMaxS + 1];
-  __shared__ int32_t s_cnt[kMaxS];
+  constexpr int wm = WV & 1, wn = WV >> 1;           // this wavefront's 128-row and 128-weight-row halves
+  const int lane = threadIdx.x & 63;
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave & 1, wn = wave >> 1;  // this wavefront's 128-row and 128-weight-row halves
-
-  const int nt_hdr = (int)p.hdr[kHdrTiles];
-  for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
-  for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
-  __syncthreads();
-  const int NT = __builtin_amdgcn_readfirstlane(min(nt_hdr, p.max_tiles));
+  const int NT = __builtin_amdgcn_readfirstlane(min((int)p.hdr[kHdrTiles], p.max_tiles));
   const int KT = p.Kd / 64;        // steps of 64 bf16
   const int NU = 4 * KT;           // sub-steps per item
   const int NBT = p.Nout / NCOLS;  // items per M-tile
@@ -116,84 +112,94 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
   };
 
   // DMA cursor: the next sub-step to load (item ordinal dn, sub-step du)
-  // and the sources of its item.  Past the last item it keeps loading the
-  // last item's sub-steps, which nobody reads, so that every sub-step issues
-  // the same number of loads and the waits below stay exact.
+  // and where its pieces come from: a_src (activations) and w_src (this
+  // wavefront's weight block), advanced per sub-step.  Past the last item
+  // it loads the last item's sub-steps again, which nobody reads, so that
+  // every sub-step issues the same number of loads and the waits below stay
+  // exact.
   int dn = 0, du = 0;
-  const char* da = nullptr;  // packed activation tile
-  const char* dw = nullptr;  // the item's first packed weight block
+  const char* a_src = nullptr;
+  const char* w_src = nullptr;
   auto dma_item = [&]() {
     int tile, nbt;
     item_of(dn, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * BIG_M));
-    da = p.A + (size_t)tile * packed_tile_bytes(p.Kd);
-    dw = p.W + (size_t)slot * p.w_slot_bytes + (size_t)(2 * nbt) * KT * B_BYTES;
+    a_src = p.A + (size_t)tile * packed_tile_bytes(p.Kd);
+    w_src = p.W + (size_t)slot * p.w_slot_bytes + (size_t)(2 * nbt + (WV >> 1)) * KT * B_BYTES;
   };
+  // This wavefront's share of a sub-step, as four 1 KB pieces: activation
+  // pieces 2 WV and 2 WV + 1; weight pieces 2 WV and 2 WV + 1, i.e. the
+  // 32-row blocks 2 (WV & 1) and 2 (WV & 1) + 1 of weight block WV >> 1,
+  // whose sub-step ks sits at ks * 1 KB of the 4 KB piece of each 32-row
+  // block in every 16 KB step.
   const uint32_t ring_lds = lds_addr(ring);
-  // This wavefront's share of a sub-step's DMA, as four 1 KB pieces:
-  // activation pieces 2w and 2w + 1, weight pieces 2w and 2w + 1 (block
-  // w >> 1, its 32-row blocks 2 (w & 1) and 2 (w & 1) + 1).  After piece 3
-  // the cursor moves on.
-  auto dma_piece = [&](int slot, int pc) {
-    const uint32_t sl = ring_lds + slot * SLOT;
-    if (pc < 2) {
-      const int b = 2 * wave + pc;
-      lds_dma16s(da + (size_t)du * SUB_BYTES, b * 1024 + lane * 16, sl + b * 1024);
-    } else {
-      const int k = du >> 2, ks = du & 3, q = 2 * (wave & 1) + (pc - 2);
-      const char* wb = dw + (size_t)(wave >> 1) * KT * B_BYTES + (size_t)k * B_BYTES + ks * 1024;
-      lds_dma16s(wb, q * 4096 + lane * 16, sl + SUB_BYTES + (2 * wave + pc - 2) * 1024);
-    }
-    if (pc == 3 && ++du == NU) {
+  uint32_t voff[4];
+  voff[0] = (2 * WV) * 1024 + lane * 16;
+  voff[1] = voff[0] + 1024;
+  voff[2] = (2 * (WV & 1)) * 4096 + lane * 16;
+  voff[3] = voff[2] + 4096;
+  auto dma_piece = [&](uint32_t sl, int pc) {
+    lds_dma16s(pc < 2 ? a_src : w_src, voff[pc], sl + (pc < 2 ? 0 : SUB_BYTES) + (2 * WV + (pc & 1)) * 1024);
+  };
+  auto dma_advance = [&]() {
+    a_src += SUB_BYTES;
+    w_src += (du & 3) == 3 ? B_BYTES - 3 * 1024 : 1024;
+    if (++du == NU) {
       du = 0;
-      if (dn + 1 < my_items) {
-        ++dn;
-        dma_item();
-      }
+      if (dn + 1 < my_items) ++dn;
+      dma_item();
     }
   };
 
   f32x16 acc[4][4];
   bf16x8 fa[2][4], fb[2][4];
-  auto frag_pair = [&](int slot, int buf, int i) {
-    const char* s = ring + slot * SLOT;
-    fa[buf][i] = *reinterpret_cast<const bf16x8*>(s + (4 * wm + i) * 1024 + lane * 16);
-    fb[buf][i] = *reinterpret_cast<const bf16x8*>(s + SUB_BYTES + (4 * wn + i) * 1024 + lane * 16);
+  auto frag_a = [&](int slot, int buf, int i) {
+    fa[buf][i] = *reinterpret_cast<const bf16x8*>(ring + slot * SLOT + (4 * wm + i) * 1024 + lane * 16);
+  };
+  auto frag_b = [&](int slot, int buf, int j) {
+    fb[buf][j] = *reinterpret_cast<const bf16x8*>(ring + slot * SLOT + SUB_BYTES + (4 * wn + j) * 1024 + lane * 16);
   };
 
   // Sub-step g, in ring slot sc = g % NSS, in four groups i = 0..3: the four
-  // MFMAs of row block i interleaved with two LDS reads of sub-step g + 1
-  // (from slot sn), then one DMA piece of sub-step g + NSS - 1 into slot sp =
-  // (g - 1) % NSS, whose sub-step g - 1 every wavefront read before the
-  // previous barrier.  Then, once sub-step g + 2 has landed and every
-  // wavefront holds sub-step g + 1, the barrier.  Loads complete in order,
-  // and NSS - 3 sub-steps of four loads each were issued after sub-step
-  // g + 2.  first: the item's first sub-step, which starts its sums from zero.
-  int sc = 0;
+  // MFMAs of row block i, two LDS reads of sub-step g + 1 (from slot sn)
+  // after the first two, and after MFMA number WV one DMA piece of sub-step
+  // g + NSS - 1 into slot (g - 1) % NSS (address sl), whose sub-step g - 1
+  // every wavefront read before the previous barrier.  The four
+  // wavefronts' pieces thus reach the texture addresser 32 cycles apart
+  // (issued together they queue there and hold up the later wavefronts),
+  // and the few non-MFMA instructions between two MFMAs stay in their
+  // shadow (a wavefront issues about one instruction per four cycles).
+  // Then, once sub-step g + 2 has landed and every wavefront holds sub-step
+  // g + 1, the barrier.  Loads complete in order, and NSS - 3 sub-steps of
+  // four loads each were issued after sub-step g + 2.  first: the item's
+  // first sub-step, which starts its sums from zero.  The slots of the next
+  // sub-step are worked out before the barrier.
+  int sc = 0, sn = 1;
+  uint32_t sl = ring_lds + (NSS - 1) * SLOT;
   auto substep = [&](int buf, bool first) {
-    const int sn = sc + 1 == NSS ? 0 : sc + 1;
-    const int sp = sc == 0 ? NSS - 1 : sc - 1;
     const f32x16 zero = {};
 #pragma unroll
     for (int i = 0; i < 4; i++) {
 #pragma unroll
-      for (int j = 0; j < 4; j++)
+      for (int j = 0; j < 4; j++) {
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[buf][j], fa[buf][i], first ? zero : acc[i][j], 0, 0, 0);
-      frag_pair(sn, buf ^ 1, i);
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_barrier(0);
-      dma_piece(sp, i);
-      __builtin_amdgcn_sched_barrier(0);
+        if (j == 0) frag_a(sn, buf ^ 1, i);
+        if (j == 1) frag_b(sn, buf ^ 1, i);
+        __builtin_amdgcn_sched_barrier(0);
+        if (j == WV) {
+          dma_piece(sl, i);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
     }
+    dma_advance();
+    sl = ring_lds + sc * SLOT;
+    sc = sn;
+    sn = sn + 1 == NSS ? 0 : sn + 1;
     wait_lgkm0();
     __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(4 * (NSS - 3)));
     barrier_nofence();
     __builtin_amdgcn_sched_barrier(0);
-    sc = sn;
   };
 
   // prologue: sub-steps 0 .. NSS - 2 into slots 0 .. NSS - 2 (the first
@@ -201,13 +207,18 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
   // before the first reads
   dma_item();
 #pragma unroll 1
-  for (int g = 0; g < NSS - 1; g++)
+  for (int g = 0; g < NSS - 1; g++) {
 #pragma unroll
-    for (int pc = 0; pc < 4; pc++) dma_piece(g, pc);
+    for (int pc = 0; pc < 4; pc++) dma_piece(ring_lds + g * SLOT, pc);
+    dma_advance();
+  }
   __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(4 * (NSS - 3)));
   barrier_nofence();
 #pragma unroll
-  for (int i = 0; i < 4; i++) frag_pair(0, 0, i);
+  for (int i = 0; i < 4; i++) {
+    frag_a(0, 0, i);
+    frag_b(0, 0, i);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
 #pragma unroll 1
@@ -217,8 +228,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
     const int row0 = tile * BIG_M;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     const int nvalid = __builtin_amdgcn_readfirstlane(min(BIG_M, s_off[slot] + s_cnt[slot] - row0));
-    uint64_t tstart = 0;
-    if (p.timing && tid == 0) tstart = __builtin_amdgcn_s_memrealtime();
+    const uint64_t tstart = p.timing ? __builtin_amdgcn_s_memrealtime() : 0;  // (uniform: scalar registers)
 
     substep(0, true);
     substep(1, false);
@@ -233,9 +243,9 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
     // the 32-row piece j of block wn.  In a gate/up piece rows 0..15 are gate
     // columns and rows 16..31 the up columns with the same indices, so gate
     // and up of a column are elements e and e + 8 of one lane.
-    // (the lane index is produced afresh here, so that the compiler keeps no
+    // (The lane index is produced afresh here, so that the compiler keeps no
     // per-lane store address live across the item loop: a spill reload would
-    // make it wait for every load in flight, the ring's DMA included)
+    // make it wait for every load in flight, the ring's DMA included.)
     int lid;
     asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lid));
     const int l31 = lid & 31, h = lid >> 5;
@@ -262,8 +272,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
                 pack4(silu_mul(v[4 * q], v[4 * q + 8]), silu_mul(v[4 * q + 1], v[4 * q + 9]),
                       silu_mul(v[4 * q + 2], v[4 * q + 10]), silu_mul(v[4 * q + 3], v[4 * q + 11]));
           // one tile at a time: reading every accumulator out at once would
-          // spill, and a spill reload makes the compiler wait for all loads
-          // (the ring's DMA included)
+          // spill
           __builtin_amdgcn_sched_barrier(0);
         }
     } else {
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
         }
       }
     }
-    if (p.timing && tid == 0) {
+    if (p.timing && WV == 0 && lid == 0) {
       const uint64_t tend = __builtin_amdgcn_s_memrealtime();
       atomicMin(reinterpret_cast<unsigned long long*>(&p.t0[slot]), (unsigned long long)tstart);
       atomicMax(reinterpret_cast<unsigned long long*>(&p.t1[slot]), (unsigned long long)tend);
@@ -295,6 +304,23 @@ __global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
   }
   // no DMA into this workgroup's LDS may outlive it
   __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
+}
+
+template <bool GATEUP>
+__global__ __launch_bounds__(256, 1) void k_gemm_big(const GemmArgs p) {
+  __shared__ __attribute__((aligned(1024))) char ring[NSS * SLOT];
+  __shared__ int32_t s_off[kMaxS + 1];
+  __shared__ int32_t s_cnt[kMaxS];
+  const int tid = threadIdx.x;
+  for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
+  for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
+  __syncthreads();
+  switch (__builtin_amdgcn_readfirstlane(tid >> 6)) {
+    case 0: big_body<GATEUP, 0>(p, ring, s_off, s_cnt); break;
+    case 1: big_body<GATEUP, 1>(p, ring, s_off, s_cnt); break;
+    case 2: big_body<GATEUP, 2>(p, ring, s_off, s_cnt); break;
+    default: big_body<GATEUP, 3>(p, ring, s_off, s_cnt); break;
+  }
 }
 
 }  // namespace
