@@ -32,8 +32,8 @@
 //   interleaved with the MFMAs of sub-step u, and so are the DMA pieces,
 //   at a different point for each wavefront.
 // * Epilogue straight from the accumulators: SwiGLU (gate/up) into packed h
-//   with 8-byte stores that fill 512 consecutive bytes per instruction, or
-//   the bf16 rows of y_perm (down).
+//   with 16-byte stores that fill 1 KB per instruction, or the bf16 rows of
+//   y_perm (down), 16 bytes per lane and row.
 #include "gemm_stream.h"
 
 namespace tempo {
@@ -132,14 +132,13 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
   // 32-row blocks 2 (WV & 1) and 2 (WV & 1) + 1 of weight block WV >> 1,
   // whose sub-step ks sits at ks * 1 KB of the 4 KB piece of each 32-row
   // block in every 16 KB step.
+  // (the piece offsets go into the scalar source address, so that a single
+  // per-lane register, lane * 16, serves every piece)
   const uint32_t ring_lds = lds_addr(ring);
-  uint32_t voff[4];
-  voff[0] = (2 * WV) * 1024 + lane * 16;
-  voff[1] = voff[0] + 1024;
-  voff[2] = (2 * (WV & 1)) * 4096 + lane * 16;
-  voff[3] = voff[2] + 4096;
+  const uint32_t lane16 = lane * 16;
   auto dma_piece = [&](uint32_t sl, int pc) {
-    lds_dma16s(pc < 2 ? a_src : w_src, voff[pc], sl + (pc < 2 ? 0 : SUB_BYTES) + (2 * WV + (pc & 1)) * 1024);
+    const char* src = pc < 2 ? a_src + (2 * WV + pc) * 1024 : w_src + (2 * (WV & 1) + (pc & 1)) * 4096;
+    lds_dma16s(src, lane16, sl + (pc < 2 ? 0 : SUB_BYTES) + (2 * WV + (pc & 1)) * 1024);
   };
   auto dma_advance = [&]() {
     a_src += SUB_BYTES;
@@ -255,29 +254,40 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
       w.y = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
       return w;
     };
+    // Lanes l and l + 32 hold the two 8-byte halves (columns 8 q .. 8 q + 3
+    // and 8 q + 4 .. 8 q + 7) of the same row; one lane swap per pair of
+    // column chunks (q0, q1) gives lane l < 32 chunk q0 and lane l + 32
+    // chunk q1 of row l, each as 16 consecutive bytes.
+    auto swap16 = [](uint2 w0, uint2 w1) {
+      const auto x = __builtin_amdgcn_permlane32_swap(w0.x, w1.x, false, false);
+      const auto y = __builtin_amdgcn_permlane32_swap(w0.y, w1.y, false, false);
+      return i32x4{(int)x[0], (int)y[0], (int)x[1], (int)y[1]};
+    };
     if (GATEUP) {
       // h column c = 128 nbt + 64 wn + 16 j + 8 q + 4 h + m is element 4 h + m
       // of 8-column chunk q of sub-step j of the down GEMM's step 2 nbt + wn;
-      // the chunk of row r is lane (r & 31) + 32 q of the piece of rows r / 32
-      char* hb = static_cast<char*>(p.C) + (size_t)tile * packed_tile_bytes(p.Nout);
+      // chunk q of row r is lane (r & 31) + 32 q of the piece of rows r / 32,
+      // so after the swap lane l stores at l * 16: 1 KB in one instruction
+      char* hb = static_cast<char*>(p.C) + (size_t)tile * packed_tile_bytes(p.Nout) + lid * 16;
 #pragma unroll
       for (int i = 0; i < 4; i++)
 #pragma unroll
         for (int j = 0; j < 4; j++) {
           const f32x16& v = acc[i][j];
-          char* pb = hb + ((size_t)((2 * nbt + wn) * 4 + j) * 8 + 4 * wm + i) * 1024 + l31 * 16 + 8 * h;
+          uint2 w[2];
 #pragma unroll
           for (int q = 0; q < 2; q++)
-            *reinterpret_cast<uint2*>(pb + q * 512) =
-                pack4(silu_mul(v[4 * q], v[4 * q + 8]), silu_mul(v[4 * q + 1], v[4 * q + 9]),
-                      silu_mul(v[4 * q + 2], v[4 * q + 10]), silu_mul(v[4 * q + 3], v[4 * q + 11]));
+            w[q] = pack4(silu_mul(v[4 * q], v[4 * q + 8]), silu_mul(v[4 * q + 1], v[4 * q + 9]),
+                         silu_mul(v[4 * q + 2], v[4 * q + 10]), silu_mul(v[4 * q + 3], v[4 * q + 11]));
+          *reinterpret_cast<i32x4*>(hb + ((size_t)((2 * nbt + wn) * 4 + j) * 8 + 4 * wm + i) * 1024) =
+              swap16(w[0], w[1]);
           // one tile at a time: reading every accumulator out at once would
           // spill
           __builtin_amdgcn_sched_barrier(0);
         }
     } else {
       const size_t ld = (size_t)p.Nout * 2;
-      char* yb = static_cast<char*>(p.C) + (size_t)row0 * ld + (size_t)(nbt * NCOLS + 128 * wn + 4 * h) * 2;
+      char* yb = static_cast<char*>(p.C) + (size_t)row0 * ld + (size_t)(nbt * NCOLS + 128 * wn + 8 * h) * 2;
 #pragma unroll
       for (int i = 0; i < 4; i++) {
         const int r = 128 * wm + 32 * i + l31;
@@ -288,9 +298,10 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
           uint2 w[4];
 #pragma unroll
           for (int q = 0; q < 4; q++) w[q] = pack4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+          const i32x4 c0 = swap16(w[0], w[1]), c1 = swap16(w[2], w[3]);  // chunks 0 | 1 and 2 | 3
           if (r < nvalid) {  // padding rows of y_perm stay unwritten
-#pragma unroll
-            for (int q = 0; q < 4; q++) *reinterpret_cast<uint2*>(yr + (32 * j + 8 * q) * 2) = w[q];
+            *reinterpret_cast<i32x4*>(yr + (32 * j) * 2) = c0;
+            *reinterpret_cast<i32x4*>(yr + (32 * j + 16) * 2) = c1;
           }
           __builtin_amdgcn_sched_barrier(0);
         }

@@ -1,0 +1,47 @@
+"""Register and LDS budget of the large-tile stage-2 GEMM, from the compiler's
+kernel metadata (CPU only: hipcc cross-compiles for gfx950).
+
+The kernel streams its operands with LDS DMA issued from inline assembly,
+which the compiler does not track; a register spill makes it wait for every
+vector-memory load in flight before the reload, which drains the DMA ring.
+So the kernel must compile without spills, and its ring must fit the 160 KB
+of LDS of a gfx950 CU.
+"""
+import os
+import re
+import shutil
+import subprocess
+
+import pytest
+
+from paper_2608_13057_amd import build
+
+SRC = os.path.join(build.CSRC, "gemm_big_agpr.hip")
+
+
+def _metadata(tmp_path):
+    if not os.path.exists(build.HIPCC) and shutil.which("hipcc") is None:
+        pytest.skip("hipcc not available")
+    out = tmp_path / "big.s"
+    cmd = [build.HIPCC, *build.flags_for(SRC), "-Wno-inline-asm", "--cuda-device-only", "-S", SRC, "-o", str(out)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    text = out.read_text()
+    kernels = {}
+    # the metadata lists one block per kernel: ".name: <symbol>" with its
+    # resource fields around it
+    for block in text.split("  - .agpr_count:")[1:]:
+        name = re.search(r"\.name:\s+(\S+)", block).group(1)
+        fields = {k: int(v) for k, v in re.findall(r"\.(\w+):\s+(\d+)\n", block)}
+        kernels[name] = fields
+    return kernels
+
+
+def test_large_tile_gemm_has_no_spills_and_fits_lds(tmp_path):
+    kernels = _metadata(tmp_path)
+    big = {n: f for n, f in kernels.items() if "k_gemm_big" in n}
+    assert len(big) == 2, sorted(kernels)  # gate/up and down
+    for name, f in big.items():
+        assert f["vgpr_spill_count"] == 0, (name, f)
+        assert f["sgpr_spill_count"] == 0, (name, f)
+        assert f["group_segment_fixed_size"] <= 160 * 1024, (name, f)
+        assert f.get("private_segment_fixed_size", 0) == 0, (name, f)
