@@ -138,7 +138,7 @@ __host__ __device__ __forceinline__ int geo_groups(int NB, int grid) { return (N
 // m row blocks of 32 real rows costs W_BASE + m (a step's fixed work plus its
 // MFMA and activation traffic per row block).  s_sw[s] holds the summed tile
 // weights of slots before s (s_sw[S] = all tiles).
-constexpr int W_BASE = 5;
+constexpr int W_BASE = 4;
 
 template <int BM>
 __device__ __forceinline__ int tile_weight(int rows) { return W_BASE + ((rows + 31) >> 5); }

@@ -26,6 +26,7 @@ import time
 import numpy as np
 
 QWEN = dict(H=4096, I=1536)
+SHAPES = {"qwen3": QWEN, "dsv3": dict(H=7168, I=2048)}  # expert shapes of the paper's two models
 DEFAULT_G = (1, 2, 4, 8, 12, 16, 24, 32)
 DEFAULT_N = (1, 2, 4, 8, 16, 32, 48, 64, 96, 128, 129, 160, 192, 256, 257, 320, 384, 512, 768, 1024, 2048)
 POOL_SLOTS = 32
@@ -137,8 +138,9 @@ class Harness:
         return rows
 
 
-def run_sweep(dtype="bf16", m_tile=128, Gs=DEFAULT_G, ns=DEFAULT_N, single_slot_ns=(), out=None, reps=30):
-    h = Harness(dtype=dtype, m_tile=m_tile, max_tokens=max(max(Gs) * max(ns), max(single_slot_ns, default=1)))
+def run_sweep(dtype="bf16", m_tile=128, Gs=DEFAULT_G, ns=DEFAULT_N, single_slot_ns=(), out=None, reps=30, shape="qwen3"):
+    h = Harness(dtype=dtype, m_tile=m_tile, max_tokens=max(max(Gs) * max(ns), max(single_slot_ns, default=1)),
+                **SHAPES[shape])
     rows = []
     f = open(out, "a") if out else None
     pts = [(G, n) for G in Gs for n in ns] + [(1, n) for n in single_slot_ns]
@@ -213,6 +215,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--dtype", default="bf16")
     ap.add_argument("--m-tile", type=int, default=128)
+    ap.add_argument("--shape", default="qwen3", choices=sorted(SHAPES), help="expert shape (H, I)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--reps", type=int, default=30)
     ap.add_argument("--quick", action="store_true", help="small grid")
@@ -233,7 +236,7 @@ def main():
         return
     Gs, ns = (DEFAULT_G, DEFAULT_N) if not args.quick else ((1, 4, 16), (1, 64, 128, 129, 512, 2048))
     fine = tuple(range(1, 2049)) if args.fine else ()
-    rows = run_sweep(args.dtype, args.m_tile, Gs, ns, fine, args.out, args.reps)
+    rows = run_sweep(args.dtype, args.m_tile, Gs, ns, fine, args.out, args.reps, args.shape)
     res = {s: summarize([r for r in rows if not (r["G"] == 1 and r["n"] not in ns)], s) for s in ("gemm", "block")}
     print(json.dumps(dict(dtype=args.dtype, m_tile=args.m_tile, fits=res)))
 
