@@ -106,9 +106,12 @@ struct GemmArgs {
 
 // Steps in flight per wavefront (DR): the weight slices of DR steps sit in
 // registers (four 16-byte loads per lane and step), the activation rows of
-// DR + 1 steps in the LDS ring.  Small M-tiles afford a deeper pipeline.
+// DR + 1 steps in the LDS ring.  Four steps (64 KB per workgroup) already
+// exceed what the vector L1 keeps outstanding; a deeper ring only queues
+// (measured: 8 steps were slightly slower than 4 on 64-row tiles, 2 much
+// slower).
 #ifndef TEMPO_DR64
-#define TEMPO_DR64 8
+#define TEMPO_DR64 4
 #endif
 #ifndef TEMPO_DR128
 #define TEMPO_DR128 4
