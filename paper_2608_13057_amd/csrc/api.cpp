@@ -26,6 +26,8 @@ Layout make_layout(const tempo_moe_shape& s) {
   o = align_up(o + 256);
   L.blk_hist = o;
   o = align_up(o + (size_t)L.nblk * s.E * 4);
+  L.blk_pre = o;
+  o = align_up(o + (size_t)(L.nblk + 1) * s.E * 4);
   L.blk_err = o;
   o = align_up(o + (size_t)L.nblk * 4);
   L.local_rank = o;

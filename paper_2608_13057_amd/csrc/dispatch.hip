@@ -20,14 +20,17 @@
 // give the offset of earlier wavefronts and a running count the offset of
 // earlier rounds.  No atomics decide positions.
 //
-// Two launches, no block ever waits for or signals another (device-scope
-// fences write back L2 on this multi-XCD chip and cost more than the work):
+// Two launches (three for large batches, see k_scan); no block ever waits
+// for or signals another (device-scope fences write back L2 on this
+// multi-XCD chip and cost more than the work):
 //   k_count  blocks of 256 pairs: in-block stable ranks and per-block expert
 //            histograms.
-//   k_place  blocks of 64 pairs: each sums the block histograms (n_e and the
-//            prefix of its own count block), recomputes the small plan -- the
-//            split of every expert over its slots, padded sizes, offsets,
-//            per-expert slot lists -- in LDS (block 0 also writes the
+//   k_place  blocks of 64 pairs (256 for large batches): each sums the block
+//            histograms (n_e and the prefix of its own count block; read
+//            from k_scan's output for large batches), recomputes the small
+//            plan -- the split of every expert over its slots, padded
+//            sizes, offsets, per-expert slot lists -- in LDS (block 0 also
+//            writes the
 //            per-expert / per-slot outputs and the header), then maps its
 //            pairs rank -> slot -> row and writes the index outputs and
 //            copies the rows, one wavefront per row with every load in
@@ -40,7 +43,12 @@
 namespace tempo {
 namespace {
 
-constexpr int kPlaceChunk = 64;  // pairs per k_place block
+// pairs per k_place block: 64 for decode-sized batches (more blocks in
+// flight, each with a short critical path), 256 when k_scan runs (a quarter
+// of the blocks recomputing the plan)
+constexpr int kPlaceChunk = 64;
+constexpr int kPlaceChunkLarge = 256;
+constexpr int kScanBlocks = 32;  // above this many count blocks, k_scan computes the prefixes once
 
 // ---------------------------------------------------------------------------
 // shared pieces
@@ -222,7 +230,8 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t*
 // slot-order position come from a readlane loop over the slots, offsets and
 // totals from wavefront scans.  Fills the LDS slot tables (se, lo, c, off and
 // the per-expert slot lists first[E] / next[S]; first must hold INT_MAX on
-// entry) and, when write is set, the global per-slot outputs and the header.
+// entry) and, when write is set, the global per-slot outputs and the header
+// (the caller marks the padding rows, with the whole block).
 __device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
                                 const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                                 const int32_t* __restrict__ remote_replicas, SlotLds& L, int32_t* first,
@@ -302,7 +311,6 @@ __device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int
   if (live) {
     slot_counts[lane] = c;
     slot_offsets[lane] = off;
-    for (int r = c; r < P; r++) row_token[off + r] = -1;
     if (timing) {
       t0[lane] = ~0ull;
       t1[lane] = 0ull;
@@ -354,14 +362,66 @@ __global__ __launch_bounds__(kCountThreads) void k_count(const int32_t* __restri
 }
 
 // ---------------------------------------------------------------------------
+// launch 1b, large batches only: for every expert, the exclusive prefix of
+// the per-block counts over the count blocks, blk_pre[b][e] = sum over b' < b
+// of blk_hist[b'][e], and in row nblk the total n_e.  Without it every k_place
+// block would sum all the block histograms itself, which for a prefill-sized
+// batch re-reads them a thousand times.  A block of 256 threads takes 8
+// experts; the 32 threads of an expert each sum a contiguous run of count
+// blocks and scan the run totals with shuffles.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void k_scan(const int32_t* __restrict__ blk_hist, int nblk, int E,
+                                              int32_t* __restrict__ blk_pre) {
+  const int tid = threadIdx.x, q = tid & 31;
+  const int e = blockIdx.x * 8 + (tid >> 5);
+  const int per = (nblk + 31) / 32;
+  const int b0 = min(q * per, nblk), b1 = min(b0 + per, nblk);
+  // loads in batches of 8, all in flight (the values of the first batch are
+  // kept for the second pass when a run is at most 8 blocks)
+  int v[8];
+  int sum = 0;
+  for (int b = b0; b < b1; b += 8) {
+#pragma unroll
+    for (int u = 0; u < 8; u++) v[u] = (e < E && b + u < b1) ? blk_hist[(size_t)(b + u) * E + e] : 0;
+#pragma unroll
+    for (int u = 0; u < 8; u++) sum += v[u];
+  }
+  int incl = sum;
+#pragma unroll
+  for (int d = 1; d < 32; d <<= 1) {
+    const int v = __shfl_up(incl, d, 32);
+    if (q >= d) incl += v;
+  }
+  if (e < E) {
+    int run = incl - sum;
+    if (b1 - b0 <= 8) {
+#pragma unroll
+      for (int u = 0; u < 8; u++)
+        if (b0 + u < b1) {
+          blk_pre[(size_t)(b0 + u) * E + e] = run;
+          run += v[u];
+        }
+    } else {
+      for (int b = b0; b < b1; b++) {
+        blk_pre[(size_t)b * E + e] = run;
+        run += blk_hist[(size_t)b * E + e];
+      }
+    }
+    if (q == 31) blk_pre[(size_t)nblk * E + e] = incl;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // launch 2: plan (recomputed per block), rows of the pairs, index outputs,
 // row copies
 // ---------------------------------------------------------------------------
 
-template <int ESIZE>
+template <int ESIZE, int CHUNK>
 __global__ __launch_bounds__(256) void k_place(
     const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int H, int row_cap, int nblk,
-    int gather_rows, const int32_t* __restrict__ blk_hist, const uint32_t* __restrict__ blk_err,
+    int gather_rows, const int32_t* __restrict__ blk_hist, const int32_t* __restrict__ blk_pre,
+    const uint32_t* __restrict__ blk_err,
     const int32_t* __restrict__ local_rank, const int32_t* __restrict__ slot_expert,
     const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
     const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts,
@@ -379,24 +439,31 @@ __global__ __launch_bounds__(256) void k_place(
   __shared__ uint32_t s_w[kMaxS];
   __shared__ int s_tmp[64];
   __shared__ uint32_t s_err;
-  __shared__ int32_t s_prow[kPlaceChunk], s_ptok[kPlaceChunk];
+  __shared__ int32_t s_prow[CHUNK], s_ptok[CHUNK];
+  __shared__ int s_wn[4];
   __shared__ int s_nplaced;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int base = blockIdx.x * kPlaceChunk;
+  const int base = blockIdx.x * CHUNK;
   const bool writer = blockIdx.x == 0;
   // own pairs' ids and in-block ranks (issued first)
   const int p = base + tid;
   int own_e = -1, own_rk = 0;
-  if (tid < kPlaceChunk && p < Pv) {
+  if (tid < CHUNK && p < Pv) {
     own_e = ids[p];
     if (own_e >= 0 && own_e < E) own_rk = local_rank[p];
     else own_e = -1;
   }
   if (tid == 0) s_err = 0;
-  // n_e and the prefix of this block's count block, from the block histograms
+  // n_e and the prefix of this block's count block: from the scan (large
+  // batches) or summed here from the block histograms
   const int cb = base / kCountThreads;
   for (int ex = tid; ex < E; ex += 256) {
     int all = 0, bef = 0, b = 0;
+    if (blk_pre) {
+      all = blk_pre[(size_t)nblk * E + ex];
+      bef = blk_pre[(size_t)cb * E + ex];
+      b = nblk;
+    }
     for (; b + 16 <= nblk; b += 16) {
       int v[16];
 #pragma unroll
@@ -453,9 +520,15 @@ __global__ __launch_bounds__(256) void k_place(
     }
   }
   __syncthreads();
-  // own pairs: rank -> slot -> row
-  if (tid < kPlaceChunk) {
-    int row = -1;
+  // block 0 marks the padding rows of every slot, all threads together (one
+  // lane per slot would take up to M - 1 dependent stores)
+  if (writer && S <= 64)
+    for (int s2 = 0; s2 < S; s2++)
+      for (int r = L.off[s2] + L.c[s2] + tid; r < L.off[s2 + 1]; r += 256) row_token[r] = -1;
+  // own pairs: rank -> slot -> row; the placed ones are compacted in pair
+  // order (per wavefront by ballot, wavefronts in order)
+  int row = -1;
+  if (tid < CHUNK) {
     if (own_e >= 0) {
       const int r = n_before[own_e] + own_rk;
       for (int s2 = first[own_e]; s2 >= 0 && s2 < S; s2 = s_next[s2])
@@ -469,14 +542,18 @@ __global__ __launch_bounds__(256) void k_place(
       pair_row[p] = row;
       if (row >= 0) row_token[row] = p / K;
     }
-    const uint64_t m = __ballot(row >= 0);
-    if (row >= 0) {
-      const int pos = __popcll(m & ((1ull << lane) - 1ull));
-      s_prow[pos] = row;
-      s_ptok[pos] = p / K;
-    }
-    if (lane == 0) s_nplaced = __popcll(m);
   }
+  const uint64_t m = __ballot(row >= 0);
+  if (lane == 0) s_wn[w] = __popcll(m);
+  __syncthreads();
+  int wbase = 0;
+  for (int i = 0; i < w; i++) wbase += s_wn[i];
+  if (row >= 0) {
+    const int pos = wbase + __popcll(m & ((1ull << lane) - 1ull));
+    s_prow[pos] = row;
+    s_ptok[pos] = p / K;
+  }
+  if (tid == 0) s_nplaced = s_wn[0] + s_wn[1] + s_wn[2] + s_wn[3];
   __syncthreads();
   const int R = s_nplaced;
   const int nch = H * ESIZE / 16;
@@ -518,20 +595,30 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
 
   hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t), st,
                      topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);
-  const int nb = ceil_div(P, kPlaceChunk);
+  // with more than kScanBlocks count blocks the prefixes are scanned once
+  const int32_t* blk_pre = nullptr;
+  if (L.nblk > kScanBlocks) {
+    int32_t* pre = reinterpret_cast<int32_t*>(ws + L.blk_pre);
+    hipLaunchKernelGGL(k_scan, dim3((s.E + 7) / 8), dim3(256), 0, st, blk_hist, L.nblk, s.E, pre);
+    blk_pre = pre;
+  }
+  const bool large = blk_pre != nullptr;
+  const int nb = ceil_div(P, large ? kPlaceChunkLarge : kPlaceChunk);
   const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
-  if (s.dtype == TEMPO_BF16)
-    hipLaunchKernelGGL(k_place<2>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H,
-                       L.row_cap, L.nblk, gather_rows ? 1 : 0, blk_hist, blk_err, local_rank, plan.slot_expert,
+  auto launch = [&](auto kern) {
+    hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H, L.row_cap,
+                       L.nblk, gather_rows ? 1 : 0, blk_hist, blk_pre, blk_err, local_rank, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),
                        x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
-  else
-    hipLaunchKernelGGL(k_place<1>, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H,
-                       L.row_cap, L.nblk, gather_rows ? 1 : 0, blk_hist, blk_err, local_rank, plan.slot_expert,
-                       plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
-                       out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),
-                       x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
+  };
+  if (s.dtype == TEMPO_BF16) {
+    if (large) launch(k_place<2, kPlaceChunkLarge>);
+    else launch(k_place<2, kPlaceChunk>);
+  } else {
+    if (large) launch(k_place<1, kPlaceChunkLarge>);
+    else launch(k_place<1, kPlaceChunk>);
+  }
   return hipGetLastError();
 }
 

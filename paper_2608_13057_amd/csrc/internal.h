@@ -30,7 +30,8 @@ enum HeaderWord : int {
 // Byte offsets of the workspace regions for one shape.
 struct Layout {
   size_t header;      // 256 B of uint32 words
-  size_t blk_hist;    // [nblk][E] int32 per-block counts, then per-block prefixes
+  size_t blk_hist;    // [nblk][E] int32 per-block counts
+  size_t blk_pre;     // [nblk + 1][E] int32 exclusive prefixes over the count blocks, then the totals (large batches)
   size_t blk_err;     // [nblk] uint32
   size_t local_rank;  // [T*K] int32 stable rank of a pair within its block and expert
   size_t slot_t0;     // [S] uint64 first stage-2 tile start (real-time counter)
