@@ -55,26 +55,34 @@ __host__ __device__ constexpr size_t packed_tile_bytes(int K) { return (size_t)B
 
 // The activation rows of every 256-row tile in the packed order, from the
 // token rows (gather: row r is token row_token[r] of A) or from permuted rows
-// (row r of A); padding rows (row_token -1) are zero.  One workgroup per
-// (tile, 64-element step): wavefront w writes sub-step w of the step.
+// (row r of A); padding rows (row_token -1) are zero.  The workgroups of a
+// fixed grid take the (tile, 64-element step) blocks of the live tiles in
+// turn (the tile count is only known on the device; a grid sized for the
+// most tiles the buffers allow would be mostly workgroups that exit at
+// once, and launching those costs more than the copy).  In a block,
+// wavefront w writes sub-step w: lane l loads the 16 bytes of row
+// 32b + (l & 31), chunk 2w + (l >> 5), and the stores fill 1 KB each.
 __global__ __launch_bounds__(256) void k_pack_rows(const char* __restrict__ A, int gather,
                                                    const int32_t* __restrict__ row_token,
                                                    const uint32_t* __restrict__ hdr, int max_tiles, int K,
                                                    char* __restrict__ out) {
   const int KT = K / 64;
-  const int tile = blockIdx.x / KT, k = blockIdx.x - tile * KT;
-  if (tile >= min((int)hdr[kHdrTiles], max_tiles)) return;
+  const int blocks = min((int)hdr[kHdrTiles], max_tiles) * KT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  char* dst = out + (size_t)tile * packed_tile_bytes(K) + (size_t)(4 * k + w) * SUB_BYTES;
   const size_t row_bytes = (size_t)K * 2;
-  const int col = k * 128 + (2 * w + (lane >> 5)) * 16;
+#pragma unroll 1
+  for (int blk = blockIdx.x; blk < blocks; blk += gridDim.x) {
+    const int tile = blk / KT, k = blk - tile * KT;
+    char* dst = out + (size_t)tile * packed_tile_bytes(K) + (size_t)(4 * k + w) * SUB_BYTES;
+    const int col = k * 128 + (2 * w + (lane >> 5)) * 16;
 #pragma unroll
-  for (int b = 0; b < 8; b++) {
-    const int row = tile * BIG_M + 32 * b + (lane & 31);
-    const int tok = row_token[row];
-    i32x4 v = {0, 0, 0, 0};
-    if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + (size_t)(gather ? tok : row) * row_bytes + col);
-    *reinterpret_cast<i32x4*>(dst + b * 1024 + lane * 16) = v;
+    for (int b = 0; b < 8; b++) {
+      const int row = tile * BIG_M + 32 * b + (lane & 31);
+      const int tok = row_token[row];
+      i32x4 v = {0, 0, 0, 0};
+      if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + (size_t)(gather ? tok : row) * row_bytes + col);
+      *reinterpret_cast<i32x4*>(dst + b * 1024 + lane * 16) = v;
+    }
   }
 }
 
@@ -356,7 +364,7 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
 
   const char* src = static_cast<const char*>(x_rows ? x_rows : d.x_perm);
-  hipLaunchKernelGGL(k_pack_rows, dim3(max_tiles * (s.H / 64)), dim3(256), 0, st, src, x_rows ? 1 : 0,
+  hipLaunchKernelGGL(k_pack_rows, dim3(persistent_grid(4)), dim3(256), 0, st, src, x_rows ? 1 : 0,
                      d.row_token, hdr, max_tiles, s.H, ws + L.apack);
 
   GemmArgs a{};

@@ -6,6 +6,8 @@
 //   requant:  h -> e4m3 with per-row 1 x 128 scales amax / 448 (saturating)
 //   down:     y_perm = sum_kb (h_kb W2_kb^T) * sh[row,kb] * sW2[blk,kb]  -> bf16
 // One pipeline step is one 128-element scale block of the contraction.
+#include <algorithm>
+
 #include "gemm_stream.h"
 
 namespace tempo {
@@ -21,20 +23,25 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
                                                  const int32_t* __restrict__ row_token,
                                                  const int32_t* __restrict__ slot_offsets, int S,
                                                  uint8_t* __restrict__ h8, float* __restrict__ h_scale) {
+  // a fixed grid walks the rows in use (one wavefront per row): a grid sized
+  // for row_cap would be mostly workgroups that exit at once
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= row_cap || row >= slot_offsets[S] || row_token[row] < 0) return;
-  const float2* src = reinterpret_cast<const float2*>(h32 + (size_t)row * I);
-  uint16_t* dst = reinterpret_cast<uint16_t*>(h8 + (size_t)row * I);
-  for (int b = 0; b < I / 128; b++) {
-    const float2 v = src[b * 64 + lane];
-    float m = fmaxf(fabsf(v.x), fabsf(v.y));
+  const int used = min(row_cap, slot_offsets[S]);
+#pragma unroll 1
+  for (int row = blockIdx.x * 4 + (threadIdx.x >> 6); row < used; row += gridDim.x * 4) {
+    if (row_token[row] < 0) continue;
+    const float2* src = reinterpret_cast<const float2*>(h32 + (size_t)row * I);
+    uint16_t* dst = reinterpret_cast<uint16_t*>(h8 + (size_t)row * I);
+    for (int b = 0; b < I / 128; b++) {
+      const float2 v = src[b * 64 + lane];
+      float m = fmaxf(fabsf(v.x), fabsf(v.y));
 #pragma unroll
-    for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d));
-    const float sc = m > 0.f ? m / 448.0f : 1.0f;
-    const float q0 = fminf(fmaxf(v.x / sc, -448.f), 448.f), q1 = fminf(fmaxf(v.y / sc, -448.f), 448.f);
-    dst[b * 64 + lane] = (uint16_t)(__builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false) & 0xFFFF);
-    if (lane == 0) h_scale[(size_t)b * row_cap + row] = sc;
+      for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d));
+      const float sc = m > 0.f ? m / 448.0f : 1.0f;
+      const float q0 = fminf(fmaxf(v.x / sc, -448.f), 448.f), q1 = fminf(fmaxf(v.y / sc, -448.f), 448.f);
+      dst[b * 64 + lane] = (uint16_t)(__builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false) & 0xFFFF);
+      if (lane == 0) h_scale[(size_t)b * row_cap + row] = sc;
+    }
   }
 }
 
@@ -75,7 +82,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   hipLaunchKernelGGL((k_gemm<true, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
   if (!mark(0)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
-  hipLaunchKernelGGL(k_quant_h, dim3(ceil_div(L.row_cap, 4)), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
+  hipLaunchKernelGGL(k_quant_h, dim3(std::min(ceil_div(L.row_cap, 4), persistent_grid(8))), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
   if (!mark(1)) return hipErrorLaunchFailure;
 
