@@ -20,9 +20,11 @@
 // give the offset of earlier wavefronts and a running count the offset of
 // earlier rounds.  No atomics decide positions.
 //
-// Two launches (three for large batches, see k_scan); no block ever waits
-// for or signals another (device-scope fences write back L2 on this
-// multi-XCD chip and cost more than the work):
+// One launch for decode-sized bf16 batches whose rows stage 2 gathers itself
+// (k_dispatch_small: one workgroup does all of it); otherwise two launches
+// (three for large batches, see k_scan); no block ever waits for or signals
+// another (device-scope fences write back L2 on this multi-XCD chip and cost
+// more than the work):
 //   k_count  blocks of 256 pairs: in-block stable ranks and per-block expert
 //            histograms.
 //   k_place  blocks of 64 pairs (256 for large batches): each sums the block
@@ -49,6 +51,12 @@ namespace {
 constexpr int kPlaceChunk = 64;
 constexpr int kPlaceChunkLarge = 256;
 constexpr int kScanBlocks = 32;  // above this many count blocks, k_scan computes the prefixes once
+// single-workgroup stage 1: 16 wavefronts, at most kSmallRounds pairs per
+// thread (batches up to 8192 pairs), per-wavefront masks and counts of up to
+// 256 experts in LDS
+constexpr int kSmallWaves = 16;
+constexpr int kSmallRounds = 8;
+constexpr int kSmallMaxE = 256;
 
 // ---------------------------------------------------------------------------
 // shared pieces
@@ -132,7 +140,7 @@ struct SlotLds {
 // read from n (LDS or global); runs on one block of NW wavefronts with
 // S <= 64 * NW.  WRITE = false computes the LDS tables only.
 template <int NW, bool WRITE>
-__device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
+__device__ __forceinline__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
                            const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                            const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ slot_counts,
                            int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
@@ -231,14 +239,16 @@ __device__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t*
 // totals from wavefront scans.  Fills the LDS slot tables (se, lo, c, off and
 // the per-expert slot lists first[E] / next[S]; first must hold INT_MAX on
 // entry) and, when write is set, the global per-slot outputs and the header
-// (the caller marks the padding rows, with the whole block).
-__device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
+// (the caller marks the padding rows, with the whole block); the sticky
+// error word is read from sticky_in (the header itself, or a copy the
+// caller loaded early).
+__device__ __forceinline__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
                                 const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                                 const int32_t* __restrict__ remote_replicas, SlotLds& L, int32_t* first,
                                 int32_t* next, bool write, int32_t* __restrict__ slot_counts,
                                 int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
-                                uint32_t* __restrict__ hdr, uint32_t err_in, int timing, uint64_t* __restrict__ t0,
-                                uint64_t* __restrict__ t1) {
+                                uint32_t* __restrict__ hdr, const uint32_t* sticky_in, uint32_t err_in, int timing,
+                                uint64_t* __restrict__ t0, uint64_t* __restrict__ t1) {
   const int lane = threadIdx.x & 63;
   const bool live = lane < S;
   const int e = live ? slot_expert[lane] : -1;
@@ -281,7 +291,18 @@ __device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int
       before = (uint64_t)nbefore;
       mine = 1;
     }
-    const uint64_t blo = (uint64_t)ne * before / W, bhi = (uint64_t)ne * (before + mine) / W;
+    uint64_t blo, bhi;
+    if (ne < (1 << 20)) {
+      // floor(a / W) in fp64 is exact here: a = n_e C < 2^52 is exact, the
+      // quotient is below 2^20 so its spacing (<= 2^-33) is finer than the
+      // distance 1/W of a non-integer a / W to the next integer
+      const double dW = (double)W;
+      blo = (uint64_t)floor((double)((uint64_t)ne * before) / dW);
+      bhi = (uint64_t)floor((double)((uint64_t)ne * (before + mine)) / dW);
+    } else {
+      blo = (uint64_t)ne * before / W;
+      bhi = (uint64_t)ne * (before + mine) / W;
+    }
     lo = (int)blo;
     c = (int)(bhi - blo);
   }
@@ -322,7 +343,7 @@ __device__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int
     hdr[kHdrActive] = (uint32_t)g;
     hdr[kHdrPairs] = (uint32_t)pairs;
     hdr[kHdrLastErr] = err;
-    hdr[kHdrSticky] = hdr[kHdrSticky] | err;
+    hdr[kHdrSticky] = *sticky_in | err;
   }
 }
 
@@ -497,7 +518,7 @@ __global__ __launch_bounds__(256) void k_place(
   if (S <= 64) {
     if (tid < 64)
       plan_slots_wave(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, L, first, s_next,
-                      writer, slot_counts, slot_offsets, row_token, hdr, s_err, timing, t0, t1);
+                      writer, slot_counts, slot_offsets, row_token, hdr, hdr + kHdrSticky, s_err, timing, t0, t1);
   } else {
     if (writer)
       plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
@@ -578,6 +599,199 @@ __global__ __launch_bounds__(256) void k_place(
   }
 }
 
+// ---------------------------------------------------------------------------
+// the whole of stage 1 in one workgroup (decode-sized bf16 batches whose rows
+// the gate/up GEMM gathers itself).  Wavefront w ranks the contiguous run of
+// pairs [w R 64, (w + 1) R 64) (R rounds of 64) without barriers: per round
+// each lane ORs its bit into the wavefront's 64-bit mask of its expert (LDS),
+// reads the mask back (its peers: the lanes with the same expert), and the
+// wavefront's own running count per expert gives the offset of its earlier
+// rounds; the first lane of a group advances the count and clears the mask.
+// One scan per expert over the wavefronts' counts then turns the ranks into
+// global stable ranks and gives n_e.  The plan's inputs are loaded into LDS
+// together with the ids, so the plan runs on LDS alone.  Then rank -> slot ->
+// row for every pair.  Same outputs as k_count + k_place without x_perm.
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int row_cap,
+    const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
+    const uint32_t* __restrict__ remote_weight, const int32_t* __restrict__ remote_replicas,
+    int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
+    int32_t* __restrict__ slot_offsets, int32_t* __restrict__ pair_row, int32_t* __restrict__ row_token,
+    uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0, uint64_t* __restrict__ t1) {
+  constexpr int NW = kSmallWaves, BD = NW * 64;
+  // dynamic LDS: peer masks [NW][E] (u64), run[E], first[E], remote_replicas[E],
+  // remote_weight[E], wavefront counts wc[NW][E]
+  extern __shared__ uint64_t dyn64[];
+  uint64_t* masks = dyn64;
+  int32_t* run = reinterpret_cast<int32_t*>(dyn64 + NW * E);
+  int32_t* first = run + E;
+  int32_t* s_rr = run + 2 * E;
+  uint32_t* s_rw = reinterpret_cast<uint32_t*>(run + 3 * E);
+  int32_t* wc = run + 4 * E;
+  __shared__ SlotLds L;
+  __shared__ int32_t s_next[kMaxS];
+  __shared__ int32_t s_se[kMaxS];
+  __shared__ uint32_t s_sw[kMaxS];
+  __shared__ uint32_t s_w[kMaxS];
+  __shared__ int s_tmp[64];
+  __shared__ uint32_t s_err, s_sticky;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int R = (Pv + BD - 1) / BD;  // rounds per wavefront (<= kSmallRounds)
+  const int pw = w * R * 64 + lane;  // this lane's pair in round 0
+  const float invK = 1.0f / (float)K;
+  // every global load in flight first: the plan's inputs and the ids
+  int se_in = -1, rr_in = 0;
+  uint32_t sw_in = 0, rw_in = 0, sticky = 0;
+  if (tid == 0) sticky = hdr[kHdrSticky];
+  if (tid < S) {
+    se_in = slot_expert[tid];
+    sw_in = slot_weight[tid];
+  }
+  if (tid < E) {
+    rr_in = remote_replicas[tid];
+    rw_in = remote_weight[tid];
+  }
+  int e[kSmallRounds];
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) {
+    const int p = pw + r * 64;
+    e[r] = (r < R && p < Pv) ? ids[p] : -1;
+  }
+  for (int i = tid; i < NW * E; i += BD) {
+    masks[i] = 0;
+    wc[i] = 0;
+  }
+  if (tid == 0) {
+    s_err = 0;
+    s_sticky = sticky;
+  }
+  if (tid < S) {
+    s_se[tid] = se_in;
+    s_sw[tid] = sw_in;
+  }
+  if (tid < E) {
+    s_rr[tid] = rr_in;
+    s_rw[tid] = rw_in;
+  }
+  int bad = 0;
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) {
+    if (e[r] != -1 && (e[r] < 0 || e[r] >= E)) {
+      bad = 1;
+      e[r] = -1;
+    }
+  }
+  __syncthreads();
+  // ranks within the wavefront's run
+  int32_t* const mine = wc + w * E;
+  uint64_t* const mk = masks + w * E;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int rk[kSmallRounds];
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) {
+    rk[r] = -1;
+    const int ex = e[r];
+    if (r < R && ex >= 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(&mk[ex]), 1ull << lane);
+      // (one LDS instruction for the whole wavefront: every lane's bit is in
+      // before any lane reads the mask, and every read is done before the
+      // first lane's clear)
+      const uint64_t peers = mk[ex];
+      const int rw = __popcll(peers & below);
+      const int cnt = mine[ex];
+      rk[r] = cnt + rw;
+      if (rw == 0) {
+        mine[ex] = cnt + __popcll(peers);
+        mk[ex] = 0;
+      }
+    }
+  }
+  if (bad) atomicOr(&s_err, TEMPO_DERR_BAD_ID);
+  __syncthreads();
+  // per expert: exclusive prefix over the wavefronts (in place) and n_e
+  for (int ex = tid; ex < E; ex += BD) {
+    int acc = 0;
+#pragma unroll
+    for (int w2 = 0; w2 < NW; w2++) {
+      const int v = wc[w2 * E + ex];
+      wc[w2 * E + ex] = acc;
+      acc += v;
+    }
+    run[ex] = acc;
+    expert_counts[ex] = acc;
+    if (cum_counts) cum_counts[ex] = cum_counts[ex] + (uint32_t)acc;
+    first[ex] = 0x7fffffff;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++)
+    if (e[r] >= 0) rk[r] += mine[e[r]];
+  if (S <= 64) {
+    if (tid < 64)
+      plan_slots_wave(run, E, S, M, s_se, s_sw, s_rw, s_rr, L, first, s_next, true, slot_counts, slot_offsets,
+                      row_token, hdr, &s_sticky, s_err, timing, t0, t1);
+    __syncthreads();
+    // padding rows: one wavefront per slot
+    for (int s2 = w; s2 < S; s2 += NW)
+      for (int r = L.off[s2] + L.c[s2] + lane; r < L.off[s2 + 1]; r += 64) row_token[r] = -1;
+  } else {
+    plan_slots<NW, true>(run, E, S, M, s_se, s_sw, s_rw, s_rr, slot_counts, slot_offsets, row_token, hdr, L,
+                         &s_err, s_w, s_tmp, timing, t0, t1);
+    for (int s2 = tid; s2 < S; s2 += BD) {
+      const int ex = L.se[s2];
+      int nx = -1;
+      if (ex >= 0 && ex < E) {
+        atomicMin(&first[ex], s2);
+        for (int s3 = s2 + 1; s3 < S; s3++)
+          if (L.se[s3] == ex) {
+            nx = s3;
+            break;
+          }
+      }
+      s_next[s2] = nx;
+    }
+    __syncthreads();
+  }
+  // rank -> slot -> row for every pair (pairs of padding tokens: -1): the
+  // expert's first slot for every round at once, the rest of its slot list
+  // only where the rank lies beyond that slot
+  int row[kSmallRounds];
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) {
+    row[r] = -1;
+    if (e[r] >= 0) {
+      const int s2 = first[e[r]];
+      if (s2 < S) {
+        const int d = rk[r] - L.lo[s2];
+        row[r] = d >= 0 && d < L.c[s2] ? L.off[s2] + d : -2;  // -2: look further
+      }
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) {
+    if (row[r] == -2) {
+      row[r] = -1;
+      for (int s2 = s_next[first[e[r]]]; s2 >= 0 && s2 < S; s2 = s_next[s2])
+        if (rk[r] >= L.lo[s2] && rk[r] < L.lo[s2] + L.c[s2]) {
+          row[r] = L.off[s2] + (rk[r] - L.lo[s2]);
+          break;
+        }
+    }
+    if (row[r] >= row_cap) row[r] = -1;  // defensive: never index past the buffers
+    const int p = pw + r * 64;
+    if (r < R && p < P) {
+      pair_row[p] = row[r];
+      // the token p / K in fp32: for p < 2^13 and K <= 32 the product is
+      // within 2^-10 of (p + 0.5) / K, whose distance to an integer is at
+      // least 0.5 / K
+      if (row[r] >= 0) row_token[row[r]] = (int)(((float)p + 0.5f) * invK);
+    }
+  }
+  for (int p = R * BD + tid; p < P; p += BD) pair_row[p] = -1;
+}
+
 }  // namespace
 
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids, const void* x,
@@ -592,6 +806,15 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
+
+  if (s.dtype == TEMPO_BF16 && !gather_rows && P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE) {
+    const size_t lds = (size_t)kSmallWaves * s.E * 8 + (size_t)(kSmallWaves + 4) * s.E * sizeof(int32_t);
+    hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
+                       s.m_tile, L.row_cap, plan.slot_expert,
+                       plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
+                       out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, hdr, timing ? 1 : 0, t0, t1);
+    return hipGetLastError();
+  }
 
   hipLaunchKernelGGL(k_count, dim3(L.nblk), dim3(kCountThreads), (kCountThreads / 64 + 1) * s.E * sizeof(int32_t), st,
                      topk_ids, Pv, s.E, ebits, blk_hist, blk_err, local_rank);

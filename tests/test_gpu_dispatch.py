@@ -129,3 +129,56 @@ def test_dispatch_empty_batch_and_cumulative_counter():
     after = to_host(c2.disp.cum_counts).view(np.uint32)
     ref = c2.oracle_dispatch()
     assert np.array_equal((after - before).astype(np.uint32), ref["expert_counts"].astype(np.uint32))
+
+
+def _forward(c):
+    import torch
+    from paper_2608_13057_amd import moe
+
+    y = torch.empty(c.wl.T, c.wl.H, dtype=torch.int16, device="cuda")
+    moe.forward(c.shape, c.d_plan, c.d_ids, c.d_w, c.d_x, c.d_xs, c.d_weights, c.disp, y, c.ws)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_forward_stage1_bit_exact(seed):
+    """Stage 1 as the forward runs it: for decode-sized bf16 batches one
+    workgroup does all of it (x_perm stays unwritten, the gate/up GEMM
+    gathers the rows).  Bit-exact counts, offsets and permutation across one
+    to eight rounds of 1024 pairs and beyond, more than 64 slots (the
+    block-wide plan), padding tokens, bad ids and every M-tile; the
+    cumulative counter advances by n_e."""
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(700 + seed)
+    T = int(rng.choice([1, 37, 300, 1024, 1500]))
+    K = int(rng.integers(1, 9))
+    E = int(rng.integers(K, 300))
+    S = int(rng.choice([5, 40, 90]))
+    wl = _random_workload(rng, T, K, E, S, "bf16")
+    if seed % 3 == 0:
+        wl.topk_ids[0, 0] = E  # out of range: flagged and dropped
+    T_valid = int(rng.integers(0, T + 1)) if seed % 2 else T
+    m_tile = (64, 128, 192, 256)[seed % 4]
+    print(f"[forward-stage1] seed={seed} T={T} K={K} E={E} S={S} Tv={T_valid} M={m_tile}", flush=True)
+    c = Case(wl, "rand", m_tile, T_valid=T_valid)
+    c.disp.cum_counts = to_dev(rng.integers(0, 2**32, size=E, dtype=np.uint64).astype(np.uint32))
+    before = to_host(c.disp.cum_counts).view(np.uint32).copy()
+    _forward(c)
+    ref = c.oracle_dispatch()
+    _compare(c, ref, check_rows=False)
+    after = to_host(c.disp.cum_counts).view(np.uint32)
+    assert np.array_equal((after - before).astype(np.uint32), ref["expert_counts"].astype(np.uint32))
+    assert moe.device_error(c.ws) == ref["err"]
+
+
+@pytest.mark.parametrize("name", ["tiny", "qwen3_decode_bf16"])
+def test_forward_stage1_workloads_bit_exact(name):
+    from paper_2608_13057_amd import measure, synth
+
+    wl = synth.make_workload(name)
+    for plan in wl.plans:
+        print(f"[forward-stage1] {name} plan={plan}", flush=True)
+        c = Case(wl, plan, measure.auto_m_tile(wl))
+        _forward(c)
+        _compare(c, c.oracle_dispatch(), check_rows=False)
