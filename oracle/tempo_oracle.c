@@ -125,13 +125,20 @@ static double round_e4m3(double x) {
  *   row_token [slot_offsets[S]]  token of each row, -1 on padding rows.
  *   pair_row [T*K]             row of each pair, -1 if not placed locally.
  *   cum_counts [E] (nullable)  (cum + n_e) mod 2^32.
+ *   snap_tiles                 nonzero: tile-aware split (below).
  * Returns the error bits.
+ *
+ * Tile-aware split (Sec. 2.2 after Eq. 2: the solver snaps partial splits
+ * to tile boundaries so that an expert's rows fill whole M-tiles).  Reading:
+ * every boundary floor(n_e C_j / W) other than n_e itself moves to the
+ * nearest multiple of M (halves round up), capped at n_e; the expert's last
+ * entry takes the remainder.  With M = 1 this is the plain split.
  */
 uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const int32_t* topk_ids,
                          const int32_t* slot_expert, const uint32_t* slot_weight,
                          const uint32_t* remote_weight, const int32_t* remote_replicas,
                          int32_t* expert_counts, int32_t* slot_counts, int32_t* slot_offsets,
-                         int32_t* row_token, int32_t* pair_row, uint32_t* cum_counts) {
+                         int32_t* row_token, int32_t* pair_row, uint32_t* cum_counts, int snap_tiles) {
   uint32_t err = 0;
   int P = T * K;
 
@@ -196,7 +203,12 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
     ent_b[0] = 0;
     for (int j = 0; j < nent; j++) {
       C += ent_w[j];
-      ent_b[j + 1] = (int64_t)((n * C) / W);
+      int64_t b = (int64_t)((n * C) / W);
+      if (snap_tiles && b != (int64_t)n) {
+        int64_t q = (b + M / 2) / M * M;
+        b = q < (int64_t)n ? q : (int64_t)n;
+      }
+      ent_b[j + 1] = b;
     }
     for (int j = 0; j < nent; j++)
       if (ent_slot[j] >= 0) {

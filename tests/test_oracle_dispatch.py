@@ -224,3 +224,96 @@ def test_synthetic_workloads_dispatch_invariants():
                 assert d["err"] == 0
                 _check_invariants(wl.topk_ids, wl.T_valid, wl.E, M, wl.placement.slot_expert, plan.slot_weight,
                                   plan.remote_weight, plan.remote_replicas, d)
+
+
+# ---- tile-aware split (Sec. 2.2 after Eq. 2: partial splits snapped to
+# tile boundaries).  Reading: every boundary other than n_e moves to the
+# nearest multiple of M (halves up), capped at n_e. ----
+
+@settings(max_examples=200, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 60), st.integers(1, 4), st.integers(1, 9), st.integers(1, 10))
+def test_snap_is_plain_split_at_tile_one(seed, T, K, E, S):
+    """With M = 1 every integer is a tile boundary: snapping changes nothing."""
+    rng = np.random.default_rng(seed)
+    ids, T_valid, se, sw, rw, rr = _rand_case(rng, T, K, E, S, 1)
+    a = oracle.dispatch(ids, T_valid, E, 1, se, sw, rw, rr)
+    b = oracle.dispatch(ids, T_valid, E, 1, se, sw, rw, rr, snap=True)
+    for k in ("expert_counts", "slot_counts", "slot_offsets", "row_token", "pair_row"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+@settings(max_examples=300, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 80), st.integers(1, 8), st.integers(1, 6), st.integers(1, 10),
+       st.sampled_from([2, 4, 8, 16, 64]))
+def test_snap_invariants_random(seed, T, K, E, S, M):
+    """Snapped splits: the same placement invariants as the plain split; the
+    local boundaries of an expert (cumulative counts over its slots in slot
+    order) are multiples of M unless they reach n_e; each lies within M / 2
+    of the plain split's boundary; an expert without a remote share fills
+    exactly ceil(n_e / M) tiles."""
+    rng = np.random.default_rng(seed)
+    ids, T_valid, se, sw, rw, rr = _rand_case(rng, T, K, E, S, M)
+    plain = oracle.dispatch(ids, T_valid, E, M, se, sw, rw, rr)
+    d = oracle.dispatch(ids, T_valid, E, M, se, sw, rw, rr, snap=True)
+    assert np.array_equal(d["expert_counts"], plain["expert_counts"])
+    assert d["err"] == plain["err"]
+    # placement invariants (the proportional-share bound of the plain split
+    # does not apply: shares move by up to M / 2)
+    sc, so, rt, pr = d["slot_counts"], d["slot_offsets"], d["row_token"], d["pair_row"]
+    Pz = so[1:] - so[:-1]
+    assert np.all(Pz % M == 0) and np.all(Pz >= sc) and np.all(Pz - sc < M)
+    placed = pr.reshape(-1) >= 0
+    rows = pr.reshape(-1)[placed]
+    assert len(np.unique(rows)) == len(rows)
+    assert np.array_equal(rt[rows], np.nonzero(placed)[0] // ids.shape[1])
+    for e in range(E):
+        loc = [s for s in range(S) if se[s] == e]
+        if not loc:
+            continue
+        n = int(d["expert_counts"][e])
+        has_remote = rw[e] > 0 or rr[e] > 0
+        b = np.cumsum([int(sc[s]) for s in loc])
+        b0 = np.cumsum([int(plain["slot_counts"][s]) for s in loc])
+        for x, x0 in zip(b.tolist(), b0.tolist()):
+            assert x == n or x % M == 0, (e, b, n)
+            assert abs(x - x0) <= M // 2
+        if not has_remote:
+            assert b[-1] == n
+            assert sum(-(-int(sc[s]) // M) for s in loc) == -(-n // M)
+        # ranks on each slot are a contiguous run in slot order: the slot's
+        # first pair is the (b_{j-1})-th pair of the expert by pair index
+        p_e = np.nonzero((ids.reshape(-1) == e) & np.repeat(np.arange(ids.shape[0]) < T_valid, ids.shape[1]))[0]
+        lo = 0
+        for s, hi in zip(loc, b.tolist()):
+            want = [i for i in range(len(p_e)) if so[s] <= pr.reshape(-1)[p_e[i]] < so[s] + sc[s]]
+            assert want == list(range(lo, hi)), (e, s)
+            lo = hi
+
+
+def test_snap_hand_worked():
+    """Hand-worked snapped splits (M = 128):
+    * 300 pairs, two local slots of equal weight: the plain boundary 150
+      moves to 128 -> 128 + 172 rows (3 tiles instead of 2 + 2);
+    * 200 pairs, one local slot and a remote share of equal weight: the
+      boundary 100 moves to 128 -> 128 local rows, 72 pairs stay remote;
+    * 128 pairs over two equal slots: the boundary 64 is a half and rounds
+      up -> 128 + 0 (one tile, one slot left empty);
+    * 300 pairs over slots of weights 1, 1, 2 (boundaries 75, 150, 300):
+      128, 128, 300 -> 128 + 0 + 172."""
+    z1 = np.zeros(1, np.uint32)
+    zr = np.zeros(1, np.int32)
+
+    def run(n, se, sw, rw=z1, rr=zr):
+        ids = np.zeros((n, 1), np.int32)
+        return oracle.dispatch(ids, n, 1, 128, np.array(se, np.int32), np.array(sw, np.uint32), rw, rr, snap=True)
+
+    d = run(300, [0, 0], [1, 1])
+    assert d["slot_counts"].tolist() == [128, 172] and d["slot_offsets"].tolist() == [0, 128, 384]
+    assert d["pair_row"].reshape(-1)[:130].tolist() == list(range(128)) + [128, 129]
+    d = run(200, [0], [1], np.array([1], np.uint32), np.array([1], np.int32))
+    assert d["slot_counts"].tolist() == [128]
+    assert (d["pair_row"].reshape(-1) >= 0).sum() == 128 and d["pair_row"].reshape(-1)[127] == 127
+    d = run(128, [0, 0], [1, 1])
+    assert d["slot_counts"].tolist() == [128, 0] and d["slot_offsets"].tolist() == [0, 128, 128]
+    d = run(300, [0, 0, 0], [1, 1, 2])
+    assert d["slot_counts"].tolist() == [128, 0, 172]
