@@ -59,6 +59,9 @@ extern "C" {
 #define TEMPO_DERR_WEIGHT_OVERFLOW 4u  /* an expert's plan weights sum to >= 2^32: split uniformly */
 
 /* element types */
+/* tempo_plan.flags */
+#define TEMPO_PLAN_SNAP_TILES 1u /* tile-aware split: boundaries on multiples of m_tile (see tempo_plan) */
+
 #define TEMPO_BF16 0
 #define TEMPO_FP8_E4M3 1
 
@@ -97,12 +100,20 @@ typedef struct tempo_moe_shape {
  *   slot_weight     [S] uint32  share weight of slot s
  *   remote_weight   [E] uint32  share weight kept by replicas on other GPUs
  *   remote_replicas [E] int32   number of replicas on other GPUs (>= 0)
+ *   flags           host value: 0, or TEMPO_PLAN_SNAP_TILES for the
+ *                   tile-aware split (Sec. 2.2 after Eq. 2: partial splits
+ *                   snapped to tile boundaries): every boundary
+ *                   floor(n_e C_j / W) other than n_e moves to the nearest
+ *                   multiple of m_tile (halves up), capped at n_e, so all of
+ *                   an expert's local rows but the last entry's fill whole
+ *                   M-tiles.  Other bits: TEMPO_EINVAL.
  */
 typedef struct tempo_plan {
   const int32_t* slot_expert;
   const uint32_t* slot_weight;
   const uint32_t* remote_weight;
   const int32_t* remote_replicas;
+  uint32_t flags;
 } tempo_plan;
 
 /*

@@ -18,6 +18,8 @@ TEMPO_DERR_BAD_ID = 1
 TEMPO_DERR_BAD_SLOT_EXPERT = 2
 TEMPO_DERR_WEIGHT_OVERFLOW = 4
 
+TEMPO_PLAN_SNAP_TILES = 1
+
 TEMPO_BF16 = 0
 TEMPO_FP8_E4M3 = 1
 
@@ -32,7 +34,8 @@ class Shape(ctypes.Structure):
 
 
 class Plan(ctypes.Structure):
-    _fields_ = [("slot_expert", _P), ("slot_weight", _P), ("remote_weight", _P), ("remote_replicas", _P)]
+    _fields_ = [("slot_expert", _P), ("slot_weight", _P), ("remote_weight", _P), ("remote_replicas", _P),
+                ("flags", ctypes.c_uint32)]
 
 
 class DispatchOut(ctypes.Structure):

@@ -88,6 +88,7 @@ static int check_shape(const tempo_moe_shape* s) {
 
 static int check_plan(const tempo_plan* p) {
   if (!p || !p->slot_expert || !p->slot_weight || !p->remote_weight || !p->remote_replicas) return TEMPO_EINVAL;
+  if (p->flags & ~TEMPO_PLAN_SNAP_TILES) return TEMPO_EINVAL;
   return TEMPO_OK;
 }
 

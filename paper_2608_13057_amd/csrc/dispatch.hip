@@ -128,6 +128,15 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* s_tmp, int* tota
   return before + x - v;
 }
 
+// Tile-aware split (Sec. 2.2 after Eq. 2: partial splits snapped to tile
+// boundaries): a boundary other than n_e moves to the nearest multiple of M
+// (halves up), capped at n_e.
+__device__ __forceinline__ uint64_t snap_boundary(uint64_t b, uint64_t n, int M) {
+  if (b == n) return b;
+  const uint64_t q = (b + (uint64_t)(M / 2)) / (uint64_t)M * (uint64_t)M;
+  return q < n ? q : n;
+}
+
 // Slot tables in LDS (filled by plan_slots).
 struct SlotLds {
   int32_t se[kMaxS];   // expert of slot
@@ -140,7 +149,7 @@ struct SlotLds {
 // read from n (LDS or global); runs on one block of NW wavefronts with
 // S <= 64 * NW.  WRITE = false computes the LDS tables only.
 template <int NW, bool WRITE>
-__device__ __forceinline__ void plan_slots(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
+__device__ __forceinline__ void plan_slots(const int32_t* n, int E, int S, int M, int snap, const int32_t* __restrict__ slot_expert,
                            const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                            const int32_t* __restrict__ remote_replicas, int32_t* __restrict__ slot_counts,
                            int32_t* __restrict__ slot_offsets, int32_t* __restrict__ row_token,
@@ -187,7 +196,11 @@ __device__ __forceinline__ void plan_slots(const int32_t* n, int E, int S, int M
         mine = 1;
       }
       const uint64_t ne = (uint64_t)n[e];
-      const uint64_t blo = ne * before / W, bhi = ne * (before + mine) / W;
+      uint64_t blo = ne * before / W, bhi = ne * (before + mine) / W;
+      if (snap) {
+        blo = snap_boundary(blo, ne, M);
+        bhi = snap_boundary(bhi, ne, M);
+      }
       lo = (int)blo;
       c = (int)(bhi - blo);
     }
@@ -242,7 +255,7 @@ __device__ __forceinline__ void plan_slots(const int32_t* n, int E, int S, int M
 // (the caller marks the padding rows, with the whole block); the sticky
 // error word is read from sticky_in (the header itself, or a copy the
 // caller loaded early).
-__device__ __forceinline__ void plan_slots_wave(const int32_t* n, int E, int S, int M, const int32_t* __restrict__ slot_expert,
+__device__ __forceinline__ void plan_slots_wave(const int32_t* n, int E, int S, int M, int snap, const int32_t* __restrict__ slot_expert,
                                 const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
                                 const int32_t* __restrict__ remote_replicas, SlotLds& L, int32_t* first,
                                 int32_t* next, bool write, int32_t* __restrict__ slot_counts,
@@ -302,6 +315,10 @@ __device__ __forceinline__ void plan_slots_wave(const int32_t* n, int E, int S, 
     } else {
       blo = (uint64_t)ne * before / W;
       bhi = (uint64_t)ne * (before + mine) / W;
+    }
+    if (snap) {
+      blo = snap_boundary(blo, (uint64_t)ne, M);
+      bhi = snap_boundary(bhi, (uint64_t)ne, M);
     }
     lo = (int)blo;
     c = (int)(bhi - blo);
@@ -440,7 +457,7 @@ __global__ __launch_bounds__(256) void k_scan(const int32_t* __restrict__ blk_hi
 
 template <int ESIZE, int CHUNK>
 __global__ __launch_bounds__(256) void k_place(
-    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int H, int row_cap, int nblk,
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int snap, int H, int row_cap, int nblk,
     int gather_rows, const int32_t* __restrict__ blk_hist, const int32_t* __restrict__ blk_pre,
     const uint32_t* __restrict__ blk_err,
     const int32_t* __restrict__ local_rank, const int32_t* __restrict__ slot_expert,
@@ -517,14 +534,14 @@ __global__ __launch_bounds__(256) void k_place(
   // the plan: one wavefront when S <= 64, the block otherwise
   if (S <= 64) {
     if (tid < 64)
-      plan_slots_wave(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, L, first, s_next,
+      plan_slots_wave(n_all, E, S, M, snap, slot_expert, slot_weight, remote_weight, remote_replicas, L, first, s_next,
                       writer, slot_counts, slot_offsets, row_token, hdr, hdr + kHdrSticky, s_err, timing, t0, t1);
   } else {
     if (writer)
-      plan_slots<NW, true>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
+      plan_slots<NW, true>(n_all, E, S, M, snap, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
                            slot_offsets, row_token, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
     else
-      plan_slots<NW, false>(n_all, E, S, M, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
+      plan_slots<NW, false>(n_all, E, S, M, snap, slot_expert, slot_weight, remote_weight, remote_replicas, slot_counts,
                             slot_offsets, row_token, hdr, L, &s_err, s_w, s_tmp, timing, t0, t1);
     for (int s2 = tid; s2 < S; s2 += 256) {
       const int ex = L.se[s2];
@@ -614,7 +631,7 @@ __global__ __launch_bounds__(256) void k_place(
 // ---------------------------------------------------------------------------
 
 __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
-    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int row_cap,
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int snap, int row_cap,
     const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
     const uint32_t* __restrict__ remote_weight, const int32_t* __restrict__ remote_replicas,
     int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
@@ -730,14 +747,14 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
     if (e[r] >= 0) rk[r] += mine[e[r]];
   if (S <= 64) {
     if (tid < 64)
-      plan_slots_wave(run, E, S, M, s_se, s_sw, s_rw, s_rr, L, first, s_next, true, slot_counts, slot_offsets,
+      plan_slots_wave(run, E, S, M, snap, s_se, s_sw, s_rw, s_rr, L, first, s_next, true, slot_counts, slot_offsets,
                       row_token, hdr, &s_sticky, s_err, timing, t0, t1);
     __syncthreads();
     // padding rows: one wavefront per slot
     for (int s2 = w; s2 < S; s2 += NW)
       for (int r = L.off[s2] + L.c[s2] + lane; r < L.off[s2 + 1]; r += 64) row_token[r] = -1;
   } else {
-    plan_slots<NW, true>(run, E, S, M, s_se, s_sw, s_rw, s_rr, slot_counts, slot_offsets, row_token, hdr, L,
+    plan_slots<NW, true>(run, E, S, M, snap, s_se, s_sw, s_rw, s_rr, slot_counts, slot_offsets, row_token, hdr, L,
                          &s_err, s_w, s_tmp, timing, t0, t1);
     for (int s2 = tid; s2 < S; s2 += BD) {
       const int ex = L.se[s2];
@@ -798,6 +815,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
                            const float* x_scale, const tempo_dispatch_out& out, char* ws, const Layout& L,
                            bool timing, bool gather_rows, hipStream_t st) {
   const int P = s.T * s.K, Pv = s.T_valid * s.K;
+  const int snap = (plan.flags & TEMPO_PLAN_SNAP_TILES) ? 1 : 0;
   int ebits = 0;
   while ((1 << ebits) < s.E) ebits++;
   int32_t* blk_hist = reinterpret_cast<int32_t*>(ws + L.blk_hist);
@@ -810,7 +828,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   if (s.dtype == TEMPO_BF16 && !gather_rows && P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE) {
     const size_t lds = (size_t)kSmallWaves * s.E * 8 + (size_t)(kSmallWaves + 4) * s.E * sizeof(int32_t);
     hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
-                       s.m_tile, L.row_cap, plan.slot_expert,
+                       s.m_tile, snap, L.row_cap, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, hdr, timing ? 1 : 0, t0, t1);
     return hipGetLastError();
@@ -829,7 +847,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   const int nb = ceil_div(P, large ? kPlaceChunkLarge : kPlaceChunk);
   const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
   auto launch = [&](auto kern) {
-    hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, s.H, L.row_cap,
+    hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, snap, s.H, L.row_cap,
                        L.nblk, gather_rows ? 1 : 0, blk_hist, blk_pre, blk_err, local_rank, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),

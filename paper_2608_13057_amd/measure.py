@@ -12,6 +12,9 @@ under profiles/).
         HBM bytes per launch of the gate/up GEMM from two `rocprofv3 --pmc`
         passes (FETCH_SIZE, WRITE_SIZE), each scaled by the reading of the
         same counter for that elementwise kernel
+    python -m paper_2608_13057_amd.measure snap --out MD
+        the tile-aware split (TEMPO_PLAN_SNAP_TILES) against the plain one:
+        M-tiles, activated slots and block time per workload and batch size
 
 The traffic summary ends with a `traffic_json:` line that bench.py reads; it
 carries a hash of the stage-2 sources, and bench.py reports no traffic once
@@ -42,8 +45,16 @@ def gemm_source_hash() -> str:
 
 
 def auto_m_tile(wl) -> int:
-    """64-row tiles when an expert sees a few dozen rows (decode), else 128."""
-    return 64 if wl.T * wl.K / wl.E <= 64 else 128
+    """64-row tiles when an expert sees a few dozen rows (decode), 128 up to
+    128 rows per expert, and beyond that 256 for bf16 (the large-tile kernel;
+    at the prefill share 586 us per block against 987 us at 128) or 128 for
+    fp8."""
+    per_expert = wl.T * wl.K / wl.E
+    if per_expert <= 64:
+        return 64
+    if per_expert <= 128 or wl.dtype != "bf16":
+        return 128
+    return 256
 
 
 def traffic_path(workload: str, m_tile: int) -> str:
@@ -191,6 +202,87 @@ def _stats(args):
     return 0
 
 
+def _snap(args):
+    """Tile-aware split against the plain one: M-tiles, activated slots and
+    block time of the forward, per workload, plan, M-tile and batch size."""
+    import numpy as np
+    import torch
+
+    from . import moe, synth
+    from .moe import to_device as td
+
+    lines = [f"# Tile-aware split (TEMPO_PLAN_SNAP_TILES) against the plain split", "",
+             "Command (repo root, MI355X):", "", "```", args.command or "python -m paper_2608_13057_amd.measure snap",
+             "```", "",
+             "Tiles = sum over slots of ceil(c_s / M) as stage 1 placed them on the GPU; extra = plain / snapped - 1 "
+             "(the padded tiles the plain split adds).  Block = one forward (stages 1-3), median of "
+             f"{args.calls} event-timed calls, the two splits alternating call by call.", "",
+             "| workload | T | plan | M | G plain / snap | N plain / snap | tiles plain / snap | extra tiles | "
+             "block plain us | block snap us | block change |", "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for spec in args.cases:
+        name, T, M, timed = spec.split(":")
+        T, M, timed = int(T), int(M), timed == "t"
+        wl = synth.make_workload(name, seed=args.seed, T=T)
+        x, xs = synth.activations(wl.T, wl.H, wl.seed, wl.dtype)
+        shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=M, dtype=wl.dtype)
+        if timed:
+            w13, s13, w2, s2 = synth.slot_weights(wl.placement.slot_expert, wl.H, wl.I, wl.seed, wl.dtype)
+            nat = moe.WeightTensors(td(w13), td(w2), None if s13 is None else td(s13), None if s2 is None else td(s2))
+            wpk = moe.pack_weights(shape, nat)
+            del nat, w13, w2
+        for pname, plan in wl.plans.items():
+            runs = {}
+            for snap in (False, True):
+                # (a prepared forward holds device pointers only: every tensor
+                # it reads stays referenced here until the timing is done)
+                keep = dict(plan=moe.PlanTensors(td(wl.placement.slot_expert), td(plan.slot_weight),
+                                                 td(plan.remote_weight), td(plan.remote_replicas), snap_tiles=snap),
+                            ids=td(wl.topk_ids), w=td(wl.topk_w), x=td(x), xs=None if xs is None else td(xs),
+                            ws=moe.Workspace(shape))
+                keep["disp"] = moe.DispatchBuffers.allocate(shape, keep["ws"].row_cap)
+                f = None
+                if timed:
+                    keep["y"] = torch.empty(wl.T, wl.H, dtype=torch.int16, device="cuda")
+                    f = moe.PreparedForward(shape, keep["plan"], keep["ids"], keep["w"], keep["x"], keep["xs"], wpk,
+                                            keep["disp"], keep["y"], keep["ws"])
+                    for _ in range(3):
+                        f()
+                else:
+                    moe.dispatch(shape, keep["plan"], keep["ids"], keep["x"], keep["xs"], keep["disp"], keep["ws"])
+                runs[snap] = (f, keep["disp"], keep)
+            torch.cuda.synchronize()
+            # the two splits alternate call by call, so that drifts of clock
+            # and cache state hit both alike
+            ts = {False: [], True: []}
+            for _ in range(args.calls if timed else 0):
+                for snap in (False, True):
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                    runs[snap][0]()
+                    e1.record()
+                    torch.cuda.synchronize()
+                    ts[snap].append(e0.elapsed_time(e1) * 1e3)
+            row = {}
+            for snap in (False, True):
+                sc = runs[snap][1].slot_counts.cpu().numpy().astype(np.int64)
+                row[snap] = (int((sc > 0).sum()), int((-(-sc // M)).sum()), float(np.median(ts[snap])) if timed else None,
+                             int(sc.sum()))
+            del runs
+            (g0, n0, t0, N0), (g1, n1, t1, N1) = row[False], row[True]
+            tb = lambda v: "-" if v is None else f"{v:.1f}"
+            ch = "-" if t0 is None else f"{(t1 / t0 - 1) * 100:+.1f}%"
+            lines.append(f"| {name} | {T} | {pname} | {M} | {g0} / {g1} | {N0} / {N1} | {n0} / {n1} | "
+                         f"{(n0 / max(n1, 1) - 1) * 100:.1f}% "
+                         f"| {tb(t0)} | {tb(t1)} | {ch} |")
+            print(lines[-1], flush=True)
+        if timed:
+            del wpk
+        torch.cuda.empty_cache()
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -214,8 +306,17 @@ def main(argv=None):
     s.add_argument("--title", default="")
     s.add_argument("--command", default="")
     s.add_argument("--note", default="")
+    n = sub.add_parser("snap")
+    n.add_argument("--cases", nargs="+", default=[
+        "qwen3_decode_fp8:1024:128:t", "qwen3_prefill_bf16:2048:128:n", "qwen3_prefill_bf16:4096:128:n",
+        "qwen3_prefill_bf16:8192:128:t", "qwen3_prefill_bf16:8192:256:t", "qwen3_prefill_bf16:16384:128:n",
+        "qwen3_prefill_fp8:8192:128:t"], help="workload:T:M-tile:t (timed) or n (tiles only)")
+    n.add_argument("--seed", type=int, default=0)
+    n.add_argument("--calls", type=int, default=30)
+    n.add_argument("--out", required=True)
+    n.add_argument("--command", default="")
     a = ap.parse_args(argv)
-    return {"run": _run, "traffic": _traffic, "stats": _stats}[a.cmd](a)
+    return {"run": _run, "traffic": _traffic, "stats": _stats, "snap": _snap}[a.cmd](a)
 
 
 if __name__ == "__main__":

@@ -138,10 +138,11 @@ class PlanTensors:
     slot_weight: torch.Tensor  # [S] int32 holding uint32 bit patterns
     remote_weight: torch.Tensor  # [E] int32 (uint32 bits)
     remote_replicas: torch.Tensor  # [E] int32
+    snap_tiles: bool = False  # tile-aware split (TEMPO_PLAN_SNAP_TILES)
 
     def c(self) -> Plan:
         return Plan(_ptr(self.slot_expert), _ptr(self.slot_weight), _ptr(self.remote_weight),
-                    _ptr(self.remote_replicas))
+                    _ptr(self.remote_replicas), _lib.TEMPO_PLAN_SNAP_TILES if self.snap_tiles else 0)
 
 
 @dataclass

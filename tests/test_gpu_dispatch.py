@@ -182,3 +182,41 @@ def test_forward_stage1_workloads_bit_exact(name):
         c = Case(wl, plan, measure.auto_m_tile(wl))
         _forward(c)
         _compare(c, c.oracle_dispatch(), check_rows=False)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_snap_split_bit_exact(seed):
+    """The tile-aware split (TEMPO_PLAN_SNAP_TILES) against the oracle's
+    snapped mode, through both stage-1 paths: the dispatch entry point (two
+    launches, rows gathered into x_perm) and the forward (one workgroup for
+    decode-sized bf16 batches)."""
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(900 + seed)
+    T = int(rng.choice([5, 100, 700, 1500, 3000]))
+    K = int(rng.integers(1, 9))
+    E = int(rng.integers(K, 40))  # few experts: many pairs per expert, several tiles
+    S = int(rng.choice([4, 20, 70]))
+    wl = _random_workload(rng, T, K, E, S, "bf16" if seed % 3 else "fp8")
+    T_valid = int(rng.integers(0, T + 1)) if seed % 2 else T
+    m_tile = (64, 128, 192, 256)[seed % 4]
+    print(f"[snap] seed={seed} T={T} K={K} E={E} S={S} Tv={T_valid} M={m_tile} {wl.dtype}", flush=True)
+    c = Case(wl, "rand", m_tile, T_valid=T_valid, snap=True)
+    ref = c.oracle_dispatch()
+    moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    _compare(c, ref)
+    _forward(c)
+    _compare(c, ref, check_rows=False)
+
+
+def test_snap_flag_validated():
+    from paper_2608_13057_amd import _lib, moe, synth
+
+    wl = synth.make_workload("tiny")
+    c = Case(wl, "uniform", 64, weights=False)
+    pl = c.d_plan.c()
+    pl.flags = 2
+    sh, do = c.shape.c(), c.disp.c()
+    rc = _lib.load().tempo_moe_dispatch(moe.ctypes.byref(sh), moe.ctypes.byref(pl), moe._ptr(c.d_ids), moe._ptr(c.d_x),
+                                        None, moe.ctypes.byref(do), c.ws.ptr, c.ws.nbytes, None)
+    assert rc == _lib.TEMPO_EINVAL  # refused on the host, nothing launched
