@@ -54,7 +54,9 @@ def _load():
         P = ctypes.c_void_p
         i32 = ctypes.c_int
         lib.oracle_dispatch.restype = ctypes.c_uint32
-        lib.oracle_dispatch.argtypes = [i32] * 6 + [P] * 11 + [i32]
+        lib.oracle_dispatch.argtypes = [i32] * 6 + [P] * 11 + [i32, ctypes.c_uint64]
+        lib.oracle_philox4x64_10.restype = None
+        lib.oracle_philox4x64_10.argtypes = [P, P, P]
         lib.oracle_moe.restype = None
         lib.oracle_moe.argtypes = [i32] * 7 + [P] * 10
         lib.oracle_ffn_rows.restype = None
@@ -78,11 +80,13 @@ def _p(a: np.ndarray):
 
 
 def dispatch(topk_ids, T_valid, E, M, slot_expert, slot_weight, remote_weight, remote_replicas,
-             cum_counts=None, snap=False) -> dict:
+             cum_counts=None, snap=False, sample_seed=None) -> dict:
     """Stage 1.  Returns a dict with expert_counts, slot_counts, slot_offsets,
     row_token (length slot_offsets[-1]), pair_row, err and (if given) the
     updated cum_counts.  snap: the tile-aware split (interior boundaries on
-    the nearest multiple of M, Sec. 2.2 after Eq. 2)."""
+    the nearest multiple of M, Sec. 2.2 after Eq. 2).  sample_seed: sampled
+    replicas instead of the split (Sec. 4.4), one Philox-4x64-10 draw per
+    pair keyed by the seed."""
     lib = _load()
     ids = np.ascontiguousarray(topk_ids, dtype=np.int32)
     T, K = ids.shape
@@ -100,7 +104,9 @@ def dispatch(topk_ids, T_valid, E, M, slot_expert, slot_weight, remote_weight, r
     pr = np.full(max(T * K, 1), -1, np.int32)
     cum = None if cum_counts is None else np.array(cum_counts, dtype=np.uint32).copy()
     err = lib.oracle_dispatch(T, T_valid, K, E, S, M, _p(ids), _p(se), _p(sw), _p(rw), _p(rr), _p(ec),
-                              _p(sc), _p(so), _p(rt), _p(pr), None if cum is None else _p(cum), 1 if snap else 0)
+                              _p(sc), _p(so), _p(rt), _p(pr), None if cum is None else _p(cum),
+                              (1 if snap else 0) | (0 if sample_seed is None else 2),
+                              0 if sample_seed is None else int(sample_seed))
     out = dict(expert_counts=ec, slot_counts=sc, slot_offsets=so, row_token=rt[: so[S]].copy(),
                pair_row=pr[: T * K].reshape(T, K).copy(), err=int(err))
     if cum is not None:
@@ -216,3 +222,14 @@ def round_bf16(x: float) -> float:
 
 def round_e4m3(x: float) -> float:
     return _load().oracle_round_e4m3(x)
+
+
+def philox4x64_10(counter, key):
+    """One block of Philox-4x64-10 (four uint64 words) at a 4-word counter and
+    2-word key (the generator of the sampled dispatch)."""
+    lib = _load()
+    c = np.ascontiguousarray(counter, dtype=np.uint64)
+    k = np.ascontiguousarray(key, dtype=np.uint64)
+    out = np.zeros(4, np.uint64)
+    lib.oracle_philox4x64_10(_p(c), _p(k), _p(out))
+    return out

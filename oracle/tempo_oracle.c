@@ -106,6 +106,35 @@ static double round_e4m3(double x) {
 }
 
 /* ------------------------------------------------------------------ */
+/* counter-based generator: Philox-4x64 with 10 rounds (Salmon, Moraes,  */
+/* Dror, Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011).  */
+/* Each round multiplies counter words 0 and 2 by the round constants    */
+/* into 128-bit products, permutes and XORs in the key; the key is       */
+/* bumped by the Weyl constants between rounds.                          */
+/* ------------------------------------------------------------------ */
+
+void oracle_philox4x64_10(const uint64_t ctr[4], const uint64_t key[2], uint64_t out[4]) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+  uint64_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3], k0 = key[0], k1 = key[1];
+  for (int r = 0; r < 10; r++) {
+    unsigned __int128 p0 = (unsigned __int128)c0 * M0, p1 = (unsigned __int128)c2 * M1;
+    uint64_t hi0 = (uint64_t)(p0 >> 64), lo0 = (uint64_t)p0, hi1 = (uint64_t)(p1 >> 64), lo1 = (uint64_t)p1;
+    uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += W0;
+    k1 += W1;
+  }
+  out[0] = c0;
+  out[1] = c1;
+  out[2] = c2;
+  out[3] = c3;
+}
+
+/* ------------------------------------------------------------------ */
 /* stage 1: dispatch                                                   */
 /* ------------------------------------------------------------------ */
 
@@ -125,8 +154,17 @@ static double round_e4m3(double x) {
  *   row_token [slot_offsets[S]]  token of each row, -1 on padding rows.
  *   pair_row [T*K]             row of each pair, -1 if not placed locally.
  *   cum_counts [E] (nullable)  (cum + n_e) mod 2^32.
- *   snap_tiles                 nonzero: tile-aware split (below).
+ *   flags                      bit 0: tile-aware split (below); bit 1: sampled
+ *                              replicas (below; bit 0 is then ignored).
+ *   seed                       key of the generator (sampled replicas).
  * Returns the error bits.
+ *
+ * Sampled replicas (Sec. 4.4: the deployed kernel samples one replica per
+ * pair from the renormalised table row).  Pair p = t*K + k of expert e draws
+ * r = word 0 of Philox-4x64-10 at counter (p, 0, 0, 0) with key (seed, 0),
+ * u = floor(hi32(r) * W / 2^32) in [0, W), and goes to the first entry j
+ * with u < C_j (entries and weights as in the split, the zero-sum fallback
+ * included).  The rows of a slot hold its pairs in ascending p.
  *
  * Tile-aware split (Sec. 2.2 after Eq. 2: the solver snaps partial splits
  * to tile boundaries so that an expert's rows fill whole M-tiles).  Reading:
@@ -138,7 +176,8 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
                          const int32_t* slot_expert, const uint32_t* slot_weight,
                          const uint32_t* remote_weight, const int32_t* remote_replicas,
                          int32_t* expert_counts, int32_t* slot_counts, int32_t* slot_offsets,
-                         int32_t* row_token, int32_t* pair_row, uint32_t* cum_counts, int snap_tiles) {
+                         int32_t* row_token, int32_t* pair_row, uint32_t* cum_counts, int flags, uint64_t seed) {
+  const int snap_tiles = (flags & 1) && !(flags & 2), sample = (flags & 2) != 0;
   uint32_t err = 0;
   int P = T * K;
 
@@ -166,6 +205,8 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
   int32_t* ent_slot = (int32_t*)malloc(((size_t)S + 1) * sizeof(int32_t));
   uint64_t* ent_w = (uint64_t*)malloc(((size_t)S + 1) * sizeof(uint64_t));
   int64_t* ent_b = (int64_t*)malloc(((size_t)S + 2) * sizeof(int64_t));
+  int32_t* pair_slot = (int32_t*)malloc(((size_t)P + 1) * sizeof(int32_t)); /* sampled: slot of each pair */
+  for (int p = 0; p < P; p++) pair_slot[p] = -1;
   for (int e = 0; e < E; e++) {
     int nent = 0;
     for (int s = 0; s < S; s++)
@@ -198,6 +239,28 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
         W += ent_w[j];
       }
     }
+    if (sample) {
+      /* one draw per valid pair of the expert, entry by cumulative weight */
+      for (int p = 0; p < T_valid * K; p++) {
+        if (topk_ids[p] != e) continue;
+        const uint64_t ctr[4] = {(uint64_t)p, 0, 0, 0}, key[2] = {seed, 0};
+        uint64_t rnd[4];
+        oracle_philox4x64_10(ctr, key, rnd);
+        const uint64_t u = ((rnd[0] >> 32) * W) >> 32;
+        uint64_t Cj = 0;
+        for (int j = 0; j < nent; j++) {
+          Cj += ent_w[j];
+          if (u < Cj) {
+            if (ent_slot[j] >= 0) {
+              pair_slot[p] = ent_slot[j];
+              slot_counts[ent_slot[j]]++;
+            }
+            break;
+          }
+        }
+      }
+      continue;
+    }
     uint64_t n = (uint64_t)expert_counts[e];
     uint64_t C = 0;
     ent_b[0] = 0;
@@ -227,8 +290,19 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
   for (int r = 0; r < slot_offsets[S]; r++) row_token[r] = -1;
 
   /* 4+6. stable rank of each pair within its expert (ascending p), rank ->
-   * entry, entry -> row. */
-  for (int e = 0; e < E; e++) {
+   * entry, entry -> row.  Sampled: the rows of a slot in ascending p. */
+  if (sample) {
+    for (int s = 0; s < S; s++) {
+      int r = 0;
+      for (int p = 0; p < T_valid * K; p++)
+        if (pair_slot[p] == s) {
+          const int row = slot_offsets[s] + r++;
+          pair_row[p] = row;
+          row_token[row] = p / K;
+        }
+    }
+  }
+  for (int e = 0; e < E && !sample; e++) {
     int r = 0;
     for (int p = 0; p < T_valid * K; p++) {
       if (topk_ids[p] != e) continue;
@@ -250,6 +324,7 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
   free(ent_slot);
   free(ent_w);
   free(ent_b);
+  free(pair_slot);
   return err;
 }
 

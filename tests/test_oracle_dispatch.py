@@ -317,3 +317,104 @@ def test_snap_hand_worked():
     assert d["slot_counts"].tolist() == [128, 0] and d["slot_offsets"].tolist() == [0, 128, 128]
     d = run(300, [0, 0, 0], [1, 1, 2])
     assert d["slot_counts"].tolist() == [128, 0, 172]
+
+
+# ---- sampled replicas (Sec. 4.4: the deployed kernel samples a replica per
+# pair from the renormalised row).  Draw of pair p: word 0 of Philox-4x64-10
+# at counter (p, 0, 0, 0), key (seed, 0); u = floor(hi32 * W / 2^32); first
+# entry j with u < C_j. ----
+
+def _np_philox_word0(p, seed):
+    """numpy's Philox-4x64-10 (an independent implementation) at counter p:
+    numpy advances its counter before each block, so it starts from p - 1."""
+    c = np.array([(p - 1) % 2**64, 0 if p > 0 else 2**64 - 1, 0 if p > 0 else 2**64 - 1, 0 if p > 0 else 2**64 - 1],
+                 dtype=np.uint64)
+    bg = np.random.Philox(key=np.array([seed, 0], dtype=np.uint64), counter=c)
+    return int(bg.random_raw(4)[0])
+
+
+def test_philox_matches_numpy():
+    rng = np.random.default_rng(3)
+    for seed in (0, 1, 2**63 + 5, int(rng.integers(0, 2**63))):
+        for p in (0, 1, 2, 77, 4095, 123456789):
+            got = int(oracle.philox4x64_10([p, 0, 0, 0], [seed, 0])[0])
+            assert got == _np_philox_word0(p, seed), (seed, p)
+    # all four words, against numpy's block sequence from counter 0
+    bg = np.random.Philox(key=np.array([9, 0], dtype=np.uint64), counter=np.zeros(4, np.uint64))
+    raw = bg.random_raw(12).reshape(3, 4)
+    for i in range(3):
+        assert np.array_equal(oracle.philox4x64_10([i + 1, 0, 0, 0], [9, 0]), raw[i])
+
+
+@settings(max_examples=100, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 60), st.integers(1, 4), st.integers(1, 9), st.integers(0, 2**40),
+       st.sampled_from([1, 4, 64]))
+def test_sample_with_one_replica_is_the_split(seed, T, K, E, wseed, M):
+    """Every expert on at most one local slot and no remote share: there is
+    nothing to sample, so the result equals the (pinned) split."""
+    rng = np.random.default_rng(seed)
+    ids, T_valid, _, _, _, _ = _rand_case(rng, T, K, E, 1, M)
+    S = int(rng.integers(1, E + 1))
+    se = rng.permutation(E)[:S].astype(np.int32)
+    sw = rng.integers(0, 5, size=S).astype(np.uint32)
+    z = np.zeros(E, np.uint32)
+    zr = np.zeros(E, np.int32)
+    a = oracle.dispatch(ids, T_valid, E, M, se, sw, z, zr)
+    b = oracle.dispatch(ids, T_valid, E, M, se, sw, z, zr, sample_seed=wseed)
+    for k in ("expert_counts", "slot_counts", "slot_offsets", "row_token", "pair_row"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+def test_sample_frequencies_and_zero_sum_row():
+    """200000 pairs of one expert over three local slots (weights 1, 2, 5) and
+    a remote share of weight 2: each share within 5 sigma of w_j / W; with an
+    all-zero row the draw is uniform over the 3 local + 2 remote replicas."""
+    n = 200000
+    ids = np.zeros((n, 1), np.int32)
+    se = np.array([0, 0, 0], np.int32)
+    for sw, rw, rr, probs in (([1, 2, 5], [2], [1], [0.1, 0.2, 0.5]), ([0, 0, 0], [0], [2], [0.2, 0.2, 0.2])):
+        d = oracle.dispatch(ids, n, 1, 64, se, np.array(sw, np.uint32), np.array(rw, np.uint32),
+                            np.array(rr, np.int32), sample_seed=2024)
+        for c, pr_ in zip(d["slot_counts"].tolist(), probs):
+            sd = np.sqrt(n * pr_ * (1 - pr_))
+            assert abs(c - n * pr_) < 5 * sd, (c, n * pr_)
+        assert (d["pair_row"] >= 0).sum() == d["slot_counts"].sum()
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 40), st.integers(1, 4), st.integers(1, 6), st.integers(1, 8),
+       st.sampled_from([1, 4, 64]), st.integers(0, 2**62))
+def test_sample_assignment_from_numpy_draws(seed, T, K, E, S, M, wseed):
+    """Each pair's slot recomputed from numpy's Philox draw and the entry
+    weights; rows of a slot in ascending pair index; padding rows -1."""
+    rng = np.random.default_rng(seed)
+    ids, T_valid, se, sw, rw, rr = _rand_case(rng, T, K, E, S, M)
+    d = oracle.dispatch(ids, T_valid, E, M, se, sw, rw, rr, sample_seed=wseed)
+    flat = ids.reshape(-1)
+    want = np.full(flat.size, -1)
+    for p in range(T_valid * K):
+        e = int(flat[p])
+        if e < 0 or e >= E:
+            continue
+        loc = [s for s in range(S) if se[s] == e]
+        has_remote = rw[e] > 0 or rr[e] > 0
+        w = [int(sw[s]) for s in loc] + ([int(rw[e])] if has_remote else [])
+        if not loc and not has_remote:
+            continue
+        if sum(w) == 0:
+            w = [1] * len(loc) + ([int(rr[e])] if has_remote else [])
+        u = ((_np_philox_word0(p, wseed) >> 32) * sum(w)) >> 32
+        j = int(np.searchsorted(np.cumsum(w), u, side="right"))
+        if j < len(loc):
+            want[p] = loc[j]
+    so = d["slot_offsets"]
+    got = np.full(flat.size, -1)
+    for p, row in enumerate(d["pair_row"].reshape(-1).tolist()):
+        if row >= 0:
+            got[p] = int(np.searchsorted(so, row, side="right") - 1)
+    assert np.array_equal(got, want)
+    assert np.array_equal(d["slot_counts"], np.bincount(want[want >= 0], minlength=S))
+    for s in range(S):
+        ps = np.nonzero(want == s)[0]
+        assert np.array_equal(d["pair_row"].reshape(-1)[ps], so[s] + np.arange(len(ps)))
+        assert np.all(d["row_token"][so[s] + len(ps):so[s + 1]] == -1)
