@@ -61,6 +61,7 @@ extern "C" {
 /* element types */
 /* tempo_plan.flags */
 #define TEMPO_PLAN_SNAP_TILES 1u /* tile-aware split: boundaries on multiples of m_tile (see tempo_plan) */
+#define TEMPO_PLAN_SAMPLE 2u     /* one sampled replica per pair instead of the split (see tempo_plan) */
 
 #define TEMPO_BF16 0
 #define TEMPO_FP8_E4M3 1
@@ -106,7 +107,17 @@ typedef struct tempo_moe_shape {
  *                   floor(n_e C_j / W) other than n_e moves to the nearest
  *                   multiple of m_tile (halves up), capped at n_e, so all of
  *                   an expert's local rows but the last entry's fill whole
- *                   M-tiles.  Other bits: TEMPO_EINVAL.
+ *                   M-tiles.  TEMPO_PLAN_SAMPLE: the deployed semantics
+ *                   (Sec. 4.4): every valid pair p = t*K + k of expert e
+ *                   draws r = word 0 of Philox-4x64-10 (Salmon et al.,
+ *                   SC 2011) at counter (p, 0, 0, 0) with key (seed, 0),
+ *                   u = floor(hi32(r) * W / 2^32), and goes to the first
+ *                   entry j with u < C_j (same entries, weights and zero-sum
+ *                   fallback as the split); the rows of a slot hold its
+ *                   pairs in ascending p.  Supported for T*K <= 8192 and
+ *                   E <= 256 (else TEMPO_EUNSUPPORTED).  Both bits, or any
+ *                   other bit: TEMPO_EINVAL.
+ *   seed            host value: the generator key for TEMPO_PLAN_SAMPLE
  */
 typedef struct tempo_plan {
   const int32_t* slot_expert;
@@ -114,6 +125,7 @@ typedef struct tempo_plan {
   const uint32_t* remote_weight;
   const int32_t* remote_replicas;
   uint32_t flags;
+  uint64_t seed;
 } tempo_plan;
 
 /*

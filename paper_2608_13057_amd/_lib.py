@@ -19,6 +19,7 @@ TEMPO_DERR_BAD_SLOT_EXPERT = 2
 TEMPO_DERR_WEIGHT_OVERFLOW = 4
 
 TEMPO_PLAN_SNAP_TILES = 1
+TEMPO_PLAN_SAMPLE = 2
 
 TEMPO_BF16 = 0
 TEMPO_FP8_E4M3 = 1
@@ -35,7 +36,7 @@ class Shape(ctypes.Structure):
 
 class Plan(ctypes.Structure):
     _fields_ = [("slot_expert", _P), ("slot_weight", _P), ("remote_weight", _P), ("remote_replicas", _P),
-                ("flags", ctypes.c_uint32)]
+                ("flags", ctypes.c_uint32), ("seed", ctypes.c_uint64)]
 
 
 class DispatchOut(ctypes.Structure):

@@ -88,7 +88,8 @@ static int check_shape(const tempo_moe_shape* s) {
 
 static int check_plan(const tempo_plan* p) {
   if (!p || !p->slot_expert || !p->slot_weight || !p->remote_weight || !p->remote_replicas) return TEMPO_EINVAL;
-  if (p->flags & ~TEMPO_PLAN_SNAP_TILES) return TEMPO_EINVAL;
+  if (p->flags & ~(TEMPO_PLAN_SNAP_TILES | TEMPO_PLAN_SAMPLE)) return TEMPO_EINVAL;
+  if ((p->flags & TEMPO_PLAN_SNAP_TILES) && (p->flags & TEMPO_PLAN_SAMPLE)) return TEMPO_EINVAL;
   return TEMPO_OK;
 }
 
@@ -163,6 +164,7 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
   int rc = check_shape(shape);
   if (rc) return rc;
   if ((rc = check_plan(plan)) || (rc = check_disp(shape, out, true))) return rc;
+  if ((plan->flags & TEMPO_PLAN_SAMPLE) && !dispatch_sample_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!topk_ids || !x || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale)) return TEMPO_EINVAL;
   const Layout L = make_layout(*shape);
   if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
@@ -206,6 +208,7 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   if (rc) return rc;
   if ((rc = check_plan(plan)) || (rc = check_disp(shape, disp, true)) || (rc = check_weights(shape, weights)))
     return rc;
+  if ((plan->flags & TEMPO_PLAN_SAMPLE) && !dispatch_sample_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!topk_ids || !topk_w || !x || !y || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale))
     return TEMPO_EINVAL;
   const Layout L = make_layout(*shape);

@@ -40,6 +40,8 @@
 //            the activation rows through row_token directly).
 // Global loads are issued before the values are needed: at one wavefront per
 // SIMD every exposed memory latency (~0.3-0.5 us) adds up.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace tempo {
@@ -630,28 +632,57 @@ __global__ __launch_bounds__(256) void k_place(
 // row for every pair.  Same outputs as k_count + k_place without x_perm.
 // ---------------------------------------------------------------------------
 
+// Philox-4x64 with 10 rounds (Salmon, Moraes, Dror, Shaw, SC 2011): word 0
+// of the block at counter (ctr, 0, 0, 0) and key (key, 0).  A round forms the
+// 128-bit products of counter words 0 and 2 with the round multipliers,
+// permutes the words and XORs in the key, which then advances by the Weyl
+// constants.
+__device__ __forceinline__ uint64_t philox4x64_10_w0(uint64_t ctr, uint64_t key) {
+  const uint64_t M0 = 0xD2E7470EE14C6C93ull, M1 = 0xCA5A826395121157ull;
+  const uint64_t W0 = 0x9E3779B97F4A7C15ull, W1 = 0xBB67AE8584CAA73Bull;
+  uint64_t c0 = ctr, c1 = 0, c2 = 0, c3 = 0, k0 = key, k1 = 0;
+#pragma unroll
+  for (int r = 0; r < 10; r++) {
+    const uint64_t hi0 = __umul64hi(c0, M0), lo0 = c0 * M0;
+    const uint64_t hi1 = __umul64hi(c2, M1), lo1 = c2 * M1;
+    const uint64_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += W0;
+    k1 += W1;
+  }
+  return c0;
+}
+
 __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
-    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int snap, int row_cap,
-    const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
+    const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int snap, int sample, uint64_t seed,
+    int row_cap, const int32_t* __restrict__ slot_expert, const uint32_t* __restrict__ slot_weight,
     const uint32_t* __restrict__ remote_weight, const int32_t* __restrict__ remote_replicas,
     int32_t* __restrict__ expert_counts, uint32_t* __restrict__ cum_counts, int32_t* __restrict__ slot_counts,
     int32_t* __restrict__ slot_offsets, int32_t* __restrict__ pair_row, int32_t* __restrict__ row_token,
     uint32_t* __restrict__ hdr, int timing, uint64_t* __restrict__ t0, uint64_t* __restrict__ t1) {
   constexpr int NW = kSmallWaves, BD = NW * 64;
-  // dynamic LDS: peer masks [NW][E] (u64), run[E], first[E], remote_replicas[E],
-  // remote_weight[E], wavefront counts wc[NW][E]
+  // pairs are ranked by a key: the expert (split), or the sampled slot
+  const int KW = sample ? S : E;
+  // dynamic LDS: peer masks [NW][KW] (u64), run[E], first[E], remote_replicas[E],
+  // remote_weight[E], row weight W[E] (sampling), wavefront counts wc[NW][KW]
   extern __shared__ uint64_t dyn64[];
   uint64_t* masks = dyn64;
-  int32_t* run = reinterpret_cast<int32_t*>(dyn64 + NW * E);
+  int32_t* run = reinterpret_cast<int32_t*>(dyn64 + NW * KW);
   int32_t* first = run + E;
   int32_t* s_rr = run + 2 * E;
   uint32_t* s_rw = reinterpret_cast<uint32_t*>(run + 3 * E);
-  int32_t* wc = run + 4 * E;
+  uint32_t* s_W = reinterpret_cast<uint32_t*>(run + 4 * E);
+  int32_t* wc = run + 5 * E;
   __shared__ SlotLds L;
   __shared__ int32_t s_next[kMaxS];
   __shared__ int32_t s_se[kMaxS];
   __shared__ uint32_t s_sw[kMaxS];
   __shared__ uint32_t s_w[kMaxS];
+  __shared__ uint32_t s_effw[kMaxS];  // sampling: the slot's weight after the zero-sum fallback
+  __shared__ int32_t s_cnt[kMaxS];    // sampling: pairs drawn per slot
   __shared__ int s_tmp[64];
   __shared__ uint32_t s_err, s_sticky;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -676,7 +707,7 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
     const int p = pw + r * 64;
     e[r] = (r < R && p < Pv) ? ids[p] : -1;
   }
-  for (int i = tid; i < NW * E; i += BD) {
+  for (int i = tid; i < NW * KW; i += BD) {
     masks[i] = 0;
     wc[i] = 0;
   }
@@ -691,6 +722,8 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
   if (tid < E) {
     s_rr[tid] = rr_in;
     s_rw[tid] = rw_in;
+    run[tid] = 0;
+    first[tid] = 0x7fffffff;
   }
   int bad = 0;
 #pragma unroll
@@ -701,50 +734,166 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
     }
   }
   __syncthreads();
+  // the rank key of every pair: its expert, or the slot its draw picks
+  int key[kSmallRounds];
+#pragma unroll
+  for (int r = 0; r < kSmallRounds; r++) key[r] = e[r];
+  if (sample) {
+    // per slot: the weight after the zero-sum fallback and the next slot of
+    // its expert; per expert: the row weight W and the first local slot
+    if (tid < S) {
+      const int ex = s_se[tid];
+      if (ex >= 0 && ex < E) {
+        uint64_t Wloc = 0;
+        int nloc = 0, nbefore = 0, nx = -1;
+        for (int s2 = 0; s2 < S; s2++)
+          if (s_se[s2] == ex) {
+            Wloc += s_sw[s2];
+            nloc++;
+            if (s2 < tid) nbefore++;
+            if (s2 > tid && nx < 0) nx = s2;
+          }
+        const int rr = s_rr[ex];
+        const uint32_t rw = s_rw[ex];
+        const bool has_remote = rw > 0u || rr > 0;
+        uint64_t W = Wloc + (has_remote ? rw : 0u);
+        uint32_t mine = s_sw[tid];
+        if (W >= (1ull << 32)) atomicOr(&s_err, TEMPO_DERR_WEIGHT_OVERFLOW);
+        if (W == 0 || W >= (1ull << 32)) {
+          W = (uint64_t)nloc + (has_remote && rr > 0 ? (uint64_t)rr : 0ull);
+          mine = 1;
+        }
+        s_effw[tid] = mine;
+        s_next[tid] = nx;
+        if (nbefore == 0) {
+          first[ex] = tid;
+          s_W[ex] = (uint32_t)W;
+        }
+      } else {
+        atomicOr(&s_err, TEMPO_DERR_BAD_SLOT_EXPERT);
+        s_next[tid] = -1;
+      }
+    }
+    __syncthreads();
+    // one draw per pair: Philox-4x64-10 word 0 at counter (p, 0, 0, 0), key
+    // (seed, 0); u = floor(hi32 * W / 2^32); the first entry with u < C_j
+    // (the local slots in order, then the remote share)
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; r++) {
+      int k = -1;
+      if (e[r] >= 0) {
+        atomicAdd(&run[e[r]], 1);
+        const int s0 = first[e[r]];
+        if (s0 < S) {
+          const uint64_t u = ((philox4x64_10_w0((uint64_t)(pw + r * 64), seed) >> 32) * (uint64_t)s_W[e[r]]) >> 32;
+          uint64_t C = 0;
+          for (int s2 = s0; s2 >= 0 && s2 < S; s2 = s_next[s2]) {
+            C += s_effw[s2];
+            if (u < C) {
+              k = s2;
+              break;
+            }
+          }
+        }
+      }
+      key[r] = k;
+    }
+  }
   // ranks within the wavefront's run
-  int32_t* const mine = wc + w * E;
-  uint64_t* const mk = masks + w * E;
+  int32_t* const mine = wc + w * KW;
+  uint64_t* const mk = masks + w * KW;
   const uint64_t below = (1ull << lane) - 1ull;
   int rk[kSmallRounds];
 #pragma unroll
   for (int r = 0; r < kSmallRounds; r++) {
     rk[r] = -1;
-    const int ex = e[r];
-    if (r < R && ex >= 0) {
-      atomicOr(reinterpret_cast<unsigned long long*>(&mk[ex]), 1ull << lane);
+    const int kx = key[r];
+    if (r < R && kx >= 0) {
+      atomicOr(reinterpret_cast<unsigned long long*>(&mk[kx]), 1ull << lane);
       // (one LDS instruction for the whole wavefront: every lane's bit is in
       // before any lane reads the mask, and every read is done before the
       // first lane's clear)
-      const uint64_t peers = mk[ex];
+      const uint64_t peers = mk[kx];
       const int rw = __popcll(peers & below);
-      const int cnt = mine[ex];
+      const int cnt = mine[kx];
       rk[r] = cnt + rw;
       if (rw == 0) {
-        mine[ex] = cnt + __popcll(peers);
-        mk[ex] = 0;
+        mine[kx] = cnt + __popcll(peers);
+        mk[kx] = 0;
       }
     }
   }
   if (bad) atomicOr(&s_err, TEMPO_DERR_BAD_ID);
   __syncthreads();
-  // per expert: exclusive prefix over the wavefronts (in place) and n_e
-  for (int ex = tid; ex < E; ex += BD) {
+  // per key: exclusive prefix over the wavefronts (in place) and the total
+  // (n_e when ranking by expert, the slot's count when sampling)
+  for (int kx = tid; kx < KW; kx += BD) {
     int acc = 0;
 #pragma unroll
     for (int w2 = 0; w2 < NW; w2++) {
-      const int v = wc[w2 * E + ex];
-      wc[w2 * E + ex] = acc;
+      const int v = wc[w2 * KW + kx];
+      wc[w2 * KW + kx] = acc;
       acc += v;
     }
-    run[ex] = acc;
-    expert_counts[ex] = acc;
-    if (cum_counts) cum_counts[ex] = cum_counts[ex] + (uint32_t)acc;
-    first[ex] = 0x7fffffff;
+    if (sample) s_cnt[kx] = acc;
+    else run[kx] = acc;
   }
   __syncthreads();
+  for (int ex = tid; ex < E; ex += BD) {
+    const int n = run[ex];
+    expert_counts[ex] = n;
+    if (cum_counts) cum_counts[ex] = cum_counts[ex] + (uint32_t)n;
+  }
 #pragma unroll
   for (int r = 0; r < kSmallRounds; r++)
-    if (e[r] >= 0) rk[r] += mine[e[r]];
+    if (key[r] >= 0) rk[r] += mine[key[r]];
+  if (sample) {
+    // padded sizes, offsets and the header from the drawn counts
+    const int c = tid < S ? s_cnt[tid] : 0;
+    const int Pz = (c + M - 1) / M * M;
+    int total = 0;
+    const int off = block_exclusive_scan<NW>(Pz, s_tmp, &total);
+    if (tid < S) {
+      L.off[tid] = off;
+      L.c[tid] = c;
+      slot_counts[tid] = c;
+      slot_offsets[tid] = off;
+      if (timing) {
+        t0[tid] = ~0ull;
+        t1[tid] = 0ull;
+      }
+    }
+    if (tid == 0) {
+      L.off[S] = total;
+      slot_offsets[S] = total;
+    }
+    block_exclusive_scan<NW>(Pz / M, s_tmp, &total);
+    const int ntiles = total;
+    block_exclusive_scan<NW>(c > 0 ? 1 : 0, s_tmp, &total);
+    const int G = total;
+    block_exclusive_scan<NW>(c, s_tmp, &total);
+    if (tid == 0) {
+      hdr[kHdrTiles] = (uint32_t)ntiles;
+      hdr[kHdrActive] = (uint32_t)G;
+      hdr[kHdrPairs] = (uint32_t)total;
+      hdr[kHdrLastErr] = s_err;
+      hdr[kHdrSticky] = s_sticky | s_err;
+    }
+    __syncthreads();
+    for (int s2 = w; s2 < S; s2 += NW)
+      for (int r = L.off[s2] + L.c[s2] + lane; r < L.off[s2 + 1]; r += 64) row_token[r] = -1;
+#pragma unroll
+    for (int r = 0; r < kSmallRounds; r++) {
+      const int p = pw + r * 64;
+      if (r < R && p < P) {
+        const int row = key[r] >= 0 ? L.off[key[r]] + rk[r] : -1;
+        pair_row[p] = row;
+        if (row >= 0) row_token[row] = (int)(((float)p + 0.5f) * invK);  // p / K exactly (as below)
+      }
+    }
+    for (int p = R * BD + tid; p < P; p += BD) pair_row[p] = -1;
+    return;
+  }
   if (S <= 64) {
     if (tid < 64)
       plan_slots_wave(run, E, S, M, snap, s_se, s_sw, s_rw, s_rr, L, first, s_next, true, slot_counts, slot_offsets,
@@ -809,13 +958,52 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
   for (int p = R * BD + tid; p < P; p += BD) pair_row[p] = -1;
 }
 
+// Row copies after k_dispatch_small: the token rows into x_perm (when asked)
+// and, for fp8, their activation scales into x_perm_scale (block-major), for
+// the rows in use (slot_offsets[S]); one wavefront per row.
+template <int ESIZE>
+__global__ __launch_bounds__(256) void k_gather_rows(const int32_t* __restrict__ row_token,
+                                                     const int32_t* __restrict__ slot_offsets, int S, int H, int row_cap,
+                                                     int gather_rows, const uint8_t* __restrict__ x,
+                                                     const float* __restrict__ x_scale, uint8_t* __restrict__ x_perm,
+                                                     float* __restrict__ x_perm_scale) {
+  const int lane = threadIdx.x & 63;
+  const int used = min(slot_offsets[S], row_cap);
+  const int nch = H * ESIZE / 16;
+  for (int row = blockIdx.x * 4 + (threadIdx.x >> 6); row < used; row += gridDim.x * 4) {
+    const int tok = row_token[row];
+    if (tok < 0) continue;
+    if (ESIZE == 1) {
+      const int ns = H / 128;
+      for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)i * row_cap + row] = x_scale[(size_t)tok * ns + i];
+    }
+    if (!gather_rows) continue;
+    const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x) + (size_t)tok * nch;
+    uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm) + (size_t)row * nch;
+    constexpr int U = 8;
+    for (int c0 = lane; c0 < nch; c0 += 64 * U) {
+      uint4 v[U];
+#pragma unroll
+      for (int u = 0; u < U; u++) v[u] = src[min(c0 + u * 64, nch - 1)];
+#pragma unroll
+      for (int u = 0; u < U; u++)
+        if (c0 + u * 64 < nch) dst[c0 + u * 64] = v[u];
+    }
+  }
+}
+
 }  // namespace
+
+bool dispatch_sample_supported(const tempo_moe_shape& s) {
+  return s.T * s.K <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE && s.S <= kMaxS;
+}
 
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids, const void* x,
                            const float* x_scale, const tempo_dispatch_out& out, char* ws, const Layout& L,
                            bool timing, bool gather_rows, hipStream_t st) {
   const int P = s.T * s.K, Pv = s.T_valid * s.K;
   const int snap = (plan.flags & TEMPO_PLAN_SNAP_TILES) ? 1 : 0;
+  const int sample = (plan.flags & TEMPO_PLAN_SAMPLE) ? 1 : 0;
   int ebits = 0;
   while ((1 << ebits) < s.E) ebits++;
   int32_t* blk_hist = reinterpret_cast<int32_t*>(ws + L.blk_hist);
@@ -825,12 +1013,29 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
-  if (s.dtype == TEMPO_BF16 && !gather_rows && P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE) {
-    const size_t lds = (size_t)kSmallWaves * s.E * 8 + (size_t)(kSmallWaves + 4) * s.E * sizeof(int32_t);
+  // one workgroup for decode-sized bf16 batches whose rows stage 2 gathers;
+  // sampled replicas always take this path (then a row-copy launch when
+  // x_perm or the fp8 scales are needed)
+  const bool small = P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE;
+  if (sample && !dispatch_sample_supported(s)) return hipErrorNotSupported;
+  if (sample || (small && s.dtype == TEMPO_BF16 && !gather_rows)) {
+    const int KW = sample ? s.S : s.E;
+    const size_t lds = (size_t)kSmallWaves * KW * 8 + (size_t)(kSmallWaves * KW + 5 * s.E) * sizeof(int32_t);
     hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
-                       s.m_tile, snap, L.row_cap, plan.slot_expert,
+                       s.m_tile, snap, sample, plan.seed, L.row_cap, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, hdr, timing ? 1 : 0, t0, t1);
+    if (gather_rows || s.dtype != TEMPO_BF16) {
+      const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
+      if (s.dtype == TEMPO_BF16)
+        hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
+                           L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                           static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+      else
+        hipLaunchKernelGGL(k_gather_rows<1>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
+                           L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                           static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+    }
     return hipGetLastError();
   }
 

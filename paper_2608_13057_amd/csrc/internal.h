@@ -55,6 +55,9 @@ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 // ---- launchers (stream-ordered, no synchronisation) ----
 // gather_rows = false leaves x_perm unwritten (stage 2 then gathers through
 // row_token; x_perm_scale is still written for fp8).
+// Whether sampled replicas (TEMPO_PLAN_SAMPLE) are available for this shape.
+bool dispatch_sample_supported(const tempo_moe_shape& s);
+
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids,
                            const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
                            const Layout& L, bool timing, bool gather_rows, hipStream_t st);

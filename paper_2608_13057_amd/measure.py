@@ -211,14 +211,16 @@ def _snap(args):
     from . import moe, synth
     from .moe import to_device as td
 
-    lines = [f"# Tile-aware split (TEMPO_PLAN_SNAP_TILES) against the plain split", "",
+    title = ("Tile-aware split (TEMPO_PLAN_SNAP_TILES)" if args.variant == "snap" else
+             f"Sampled replicas (TEMPO_PLAN_SAMPLE, generator key {args.key})")
+    lines = [f"# {title} against the plain split", "",
              "Command (repo root, MI355X):", "", "```", args.command or "python -m paper_2608_13057_amd.measure snap",
              "```", "",
-             "Tiles = sum over slots of ceil(c_s / M) as stage 1 placed them on the GPU; extra = plain / snapped - 1 "
-             "(the padded tiles the plain split adds).  Block = one forward (stages 1-3), median of "
+             "Tiles = sum over slots of ceil(c_s / M) as stage 1 placed them on the GPU; extra = plain / variant - 1.  "
+             "Block = one forward (stages 1-3), median of "
              f"{args.calls} event-timed calls, the two splits alternating call by call.", "",
-             "| workload | T | plan | M | G plain / snap | N plain / snap | tiles plain / snap | extra tiles | "
-             "block plain us | block snap us | block change |", "|---|---|---|---|---|---|---|---|---|---|---|"]
+             "| workload | T | plan | M | G plain / variant | N plain / variant | tiles plain / variant | extra tiles | "
+             "block plain us | block variant us | block change |", "|---|---|---|---|---|---|---|---|---|---|---|"]
     for spec in args.cases:
         name, T, M, timed = spec.split(":")
         T, M, timed = int(T), int(M), timed == "t"
@@ -236,7 +238,9 @@ def _snap(args):
                 # (a prepared forward holds device pointers only: every tensor
                 # it reads stays referenced here until the timing is done)
                 keep = dict(plan=moe.PlanTensors(td(wl.placement.slot_expert), td(plan.slot_weight),
-                                                 td(plan.remote_weight), td(plan.remote_replicas), snap_tiles=snap),
+                                                 td(plan.remote_weight), td(plan.remote_replicas),
+                                                 snap_tiles=snap and args.variant == "snap",
+                                                 sample_seed=args.key if snap and args.variant == "sample" else None),
                             ids=td(wl.topk_ids), w=td(wl.topk_w), x=td(x), xs=None if xs is None else td(xs),
                             ws=moe.Workspace(shape))
                 keep["disp"] = moe.DispatchBuffers.allocate(shape, keep["ws"].row_cap)
@@ -306,7 +310,9 @@ def main(argv=None):
     s.add_argument("--title", default="")
     s.add_argument("--command", default="")
     s.add_argument("--note", default="")
-    n = sub.add_parser("snap")
+    n = sub.add_parser("snap", help="the tile-aware split or sampled replicas against the plain split")
+    n.add_argument("--variant", choices=("snap", "sample"), default="snap")
+    n.add_argument("--key", type=int, default=12345, help="generator key of the sampled variant")
     n.add_argument("--cases", nargs="+", default=[
         "qwen3_decode_fp8:1024:128:t", "qwen3_prefill_bf16:2048:128:n", "qwen3_prefill_bf16:4096:128:n",
         "qwen3_prefill_bf16:8192:128:t", "qwen3_prefill_bf16:8192:256:t", "qwen3_prefill_bf16:16384:128:n",

@@ -139,10 +139,13 @@ class PlanTensors:
     remote_weight: torch.Tensor  # [E] int32 (uint32 bits)
     remote_replicas: torch.Tensor  # [E] int32
     snap_tiles: bool = False  # tile-aware split (TEMPO_PLAN_SNAP_TILES)
+    sample_seed: int | None = None  # sampled replicas with this generator key (TEMPO_PLAN_SAMPLE)
 
     def c(self) -> Plan:
+        flags = (_lib.TEMPO_PLAN_SNAP_TILES if self.snap_tiles else 0) | (
+            0 if self.sample_seed is None else _lib.TEMPO_PLAN_SAMPLE)
         return Plan(_ptr(self.slot_expert), _ptr(self.slot_weight), _ptr(self.remote_weight),
-                    _ptr(self.remote_replicas), _lib.TEMPO_PLAN_SNAP_TILES if self.snap_tiles else 0)
+                    _ptr(self.remote_replicas), flags, 0 if self.sample_seed is None else int(self.sample_seed))
 
 
 @dataclass
@@ -329,3 +332,17 @@ def device_error(ws: Workspace, stream=None) -> int:
     bits = ctypes.c_uint32(0)
     check(_lib.load().tempo_moe_device_error(ws.ptr, _stream(stream), ctypes.byref(bits)), "tempo_moe_device_error")
     return int(bits.value)
+
+
+def counter_window(before, after):
+    """Per-expert pair counts of a window from two snapshots of the
+    cumulative counters (cum_counts, uint32, wrapping modulo 2^32): the
+    wrap-safe difference (after - before) mod 2^32 (Sec. 4.4: a persistent
+    cumulative counter needs no zeroing kernel; the reader recovers windows by
+    differencing).  Exact while a window adds fewer than 2^32 pairs per
+    expert.  Accepts numpy arrays or CPU tensors of int32 / uint32 bits."""
+    import numpy as np
+
+    b = np.asarray(before.cpu() if hasattr(before, "cpu") else before).view(np.uint32)
+    a = np.asarray(after.cpu() if hasattr(after, "cpu") else after).view(np.uint32)
+    return (a.astype(np.uint64) - b.astype(np.uint64)) % (1 << 32)

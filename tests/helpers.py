@@ -34,7 +34,7 @@ class Case:
     """Everything one forward needs, on host (numpy) and device (torch)."""
 
     def __init__(self, wl: synth.Workload, plan_name: str, m_tile: int = 128, weights=True, device="cuda",
-                 T_valid=None, snap=False):
+                 T_valid=None, snap=False, sample_seed=None):
         from paper_2608_13057_amd import moe
 
         self.wl = wl
@@ -42,6 +42,7 @@ class Case:
         self.dtype = wl.dtype
         self.m_tile = m_tile
         self.snap = snap
+        self.sample_seed = sample_seed
         self.T_valid = wl.T_valid if T_valid is None else T_valid
         self.shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=m_tile, dtype=wl.dtype,
                                   T_valid=self.T_valid)
@@ -56,7 +57,8 @@ class Case:
         self.d_xs = None if self.xs is None else to_dev(self.xs, device)
         self.d_plan = moe.PlanTensors(to_dev(wl.placement.slot_expert, device), to_dev(self.plan.slot_weight, device),
                                       to_dev(self.plan.remote_weight, device),
-                                      to_dev(self.plan.remote_replicas, device), snap_tiles=snap)
+                                      to_dev(self.plan.remote_replicas, device), snap_tiles=snap,
+                                      sample_seed=sample_seed)
         if weights:
             natural = moe.WeightTensors(to_dev(self.w13, device), to_dev(self.w2, device),
                                         None if self.s13 is None else to_dev(self.s13, device),
@@ -71,7 +73,7 @@ class Case:
 
         return oracle.dispatch(self.wl.topk_ids, self.T_valid, self.wl.E, self.m_tile, self.wl.placement.slot_expert,
                                self.plan.slot_weight, self.plan.remote_weight, self.plan.remote_replicas,
-                               snap=self.snap)
+                               snap=self.snap, sample_seed=self.sample_seed)
 
 
 def rel_err_rows(y: np.ndarray, ref: np.ndarray, rows: np.ndarray) -> float:

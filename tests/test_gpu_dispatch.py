@@ -215,8 +215,55 @@ def test_snap_flag_validated():
     wl = synth.make_workload("tiny")
     c = Case(wl, "uniform", 64, weights=False)
     pl = c.d_plan.c()
-    pl.flags = 2
+    pl.flags = 4  # no such flag
     sh, do = c.shape.c(), c.disp.c()
     rc = _lib.load().tempo_moe_dispatch(moe.ctypes.byref(sh), moe.ctypes.byref(pl), moe._ptr(c.d_ids), moe._ptr(c.d_x),
                                         None, moe.ctypes.byref(do), c.ws.ptr, c.ws.nbytes, None)
     assert rc == _lib.TEMPO_EINVAL  # refused on the host, nothing launched
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_sampled_dispatch_bit_exact(seed):
+    """Sampled replicas (TEMPO_PLAN_SAMPLE, the deployed semantics) against
+    the oracle's sampled mode: the dispatch entry point (rows gathered into
+    x_perm by the row-copy launch) and the forward; bf16 and fp8; ragged
+    batches, padding tokens, zero-weight rows, remote shares."""
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(1100 + seed)
+    T = int(rng.choice([1, 37, 300, 1024]))
+    K = int(rng.integers(1, 9))
+    E = int(rng.integers(K, 200))
+    S = int(rng.choice([3, 30, 90]))
+    wl = _random_workload(rng, T, K, E, S, "bf16" if seed % 2 == 0 else "fp8")
+    T_valid = int(rng.integers(0, T + 1)) if seed % 3 else T
+    m_tile = (64, 128, 192, 256)[seed % 4]
+    key = int(rng.integers(0, 2**63))
+    print(f"[sample] seed={seed} T={T} K={K} E={E} S={S} Tv={T_valid} M={m_tile} {wl.dtype} key={key}", flush=True)
+    c = Case(wl, "rand", m_tile, T_valid=T_valid, sample_seed=key)
+    ref = c.oracle_dispatch()
+    moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    _compare(c, ref)
+    assert moe.device_error(c.ws) == ref["err"]
+    _forward(c)
+    _compare(c, ref, check_rows=False)
+
+
+def test_sampled_dispatch_limits():
+    """Sampling is offered up to 8192 pairs and 256 experts; beyond that the
+    call is refused on the host; snapping and sampling together are invalid."""
+    from paper_2608_13057_amd import _lib, moe
+
+    rng = np.random.default_rng(7)
+    wl = _random_workload(rng, 2048, 8, 64, 8)  # 16384 pairs
+    c = Case(wl, "rand", 64, weights=False, sample_seed=1)
+    with pytest.raises(_lib.TempoError) as ex:
+        moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    assert ex.value.code == _lib.TEMPO_EUNSUPPORTED
+    c2 = Case(_random_workload(rng, 64, 2, 10, 4), "rand", 64, weights=False, sample_seed=1)
+    pl = c2.d_plan.c()
+    pl.flags = _lib.TEMPO_PLAN_SAMPLE | _lib.TEMPO_PLAN_SNAP_TILES
+    sh, do = c2.shape.c(), c2.disp.c()
+    rc = _lib.load().tempo_moe_dispatch(moe.ctypes.byref(sh), moe.ctypes.byref(pl), moe._ptr(c2.d_ids),
+                                        moe._ptr(c2.d_x), None, moe.ctypes.byref(do), c2.ws.ptr, c2.ws.nbytes, None)
+    assert rc == _lib.TEMPO_EINVAL
