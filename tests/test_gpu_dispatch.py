@@ -267,3 +267,31 @@ def test_sampled_dispatch_limits():
     rc = _lib.load().tempo_moe_dispatch(moe.ctypes.byref(sh), moe.ctypes.byref(pl), moe._ptr(c2.d_ids),
                                         moe._ptr(c2.d_x), None, moe.ctypes.byref(do), c2.ws.ptr, c2.ws.nbytes, None)
     assert rc == _lib.TEMPO_EINVAL
+
+
+@pytest.mark.parametrize("name", ["qwen3_decode_bf16", "dsv3_decode_fp8"])
+def test_counts_solver_plan_loop(name):
+    """counts -> plan -> kernel: stage 1 on the GPU collects n_e; the
+    tempo_fast solver splits them over an 8-GPU placement in which GPU 0
+    holds this workload's slots; the plan it emits for GPU 0, run through
+    stage 1 on the GPU again, places exactly the solver's shares."""
+    import torch
+    from paper_2608_13057_amd import moe, solver, synth
+
+    wl = synth.make_workload(name)
+    c = Case(wl, next(iter(wl.plans)), 64, weights=False)
+    moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    n = to_host(c.disp.expert_counts).astype(np.int64)
+    se = wl.placement.slot_expert
+    R = np.zeros((wl.E, 8), bool)
+    R[se, 0] = True
+    R[np.arange(wl.E), 1 + np.arange(wl.E) % 7] = True
+    x = solver.tempo_fast(n, R, solver.CostModel(41.6, 5.61, 14.1, 0.1122))
+    sw, rw, rr = solver.plan_for_gpu(x, se, 0)
+    c.d_plan = moe.PlanTensors(to_dev(se), to_dev(sw), to_dev(rw), to_dev(rr))
+    moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    torch.cuda.synchronize()
+    sc = to_host(c.disp.slot_counts)
+    for e in np.unique(se):
+        assert sc[se == e].sum() == x[e, 0], e
+    assert sc.sum() == x[:, 0].sum()
