@@ -151,9 +151,9 @@ def moe(x, topk_w, pslot, w13, w2, dtype: str, mode: str = "exact", x_scale=None
     S, I2, H2 = w13.shape
     I = I2 // 2
     assert H2 == H and w2.shape == (S, H, I)
-    dt = {"bf16": 0, "fp8": 1}[dtype]
+    dt = {"bf16": 0, "fp8": 1, "fp8mx": 2}[dtype]
     md = {"exact": 0, "mirror": 1}[mode]
-    if dt == 1:
+    if dt != 0:
         assert x_scale is not None and w13_scale is not None and w2_scale is not None
         xs = np.ascontiguousarray(x_scale, np.float32)
         s13 = np.ascontiguousarray(w13_scale, np.float32)
@@ -185,7 +185,7 @@ def ffn_rows(x, tok, slot, w13, w2, dtype: str, mode: str = "exact", x_scale=Non
     slot = np.ascontiguousarray(slot, np.int32)
     R = len(tok)
     out = np.zeros((R, H), np.float64)
-    dt = {"bf16": 0, "fp8": 1}[dtype]
+    dt = {"bf16": 0, "fp8": 1, "fp8mx": 2}[dtype]
     md = {"exact": 0, "mirror": 1}[mode]
     keep = [np.ascontiguousarray(a, np.float32) if a is not None else None for a in (x_scale, w13_scale, w2_scale)]
     w13c, w2c = np.ascontiguousarray(w13), np.ascontiguousarray(w2)

@@ -333,6 +333,9 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
 /* ------------------------------------------------------------------ */
 
 /* dtype: 0 = bf16 (uint16 storage), 1 = fp8 e4m3 (uint8 storage) with
+ * scales, 2 = fp8 e4m3 whose scales are powers of two (UE8M0; the paper's
+ * note that newer hardware requires them, Sec. 7): the same values, only the
+ * re-quantisation of h picks its scale differently (below); 1 or 2
  * fp32 scales: activations 1 x 128 along the contraction, weights 128 x 128
  * blocks (the gate/up matrix [2I, H] is blocked as one matrix). */
 static double x_at(int dtype, const void* x, const float* xs, int H, int t, int h) {
@@ -367,11 +370,17 @@ static void ffn_one(int H, int I, int dtype, int mode, const double* xv, int s, 
     if (dtype == 0) {
       for (int i = 0; i < I; i++) hv[i] = round_bf16(hv[i]);
     } else {
-      /* 1 x 128 block quantisation: scale = amax / 448, q = e4m3(h / scale) */
+      /* 1 x 128 block quantisation: scale = amax / 448 (dtype 2: the
+       * smallest power of two at least amax / 448), q = e4m3(h / scale) */
       for (int b = 0; b < I / 128; b++) {
         double amax = 0.0;
         for (int i = b * 128; i < b * 128 + 128; i++) amax = fmax(amax, fabs(hv[i]));
         double sc = amax > 0.0 ? amax / 448.0 : 1.0;
+        if (dtype == 2 && amax > 0.0) {
+          int ex;
+          const double f = frexp(sc, &ex); /* sc = f 2^ex, f in [0.5, 1) */
+          sc = ldexp(1.0, f == 0.5 ? ex - 1 : ex);
+        }
         for (int i = b * 128; i < b * 128 + 128; i++) hv[i] = round_e4m3(hv[i] / sc) * sc;
       }
     }

@@ -25,7 +25,8 @@ Sec. 3.2):
   copies of their expert's weights;
 * bf16 = round-to-nearest-even of the fp32 sample; fp8 = e4m3 (RNE,
   saturating at 448) with fp32 scales amax/448: 1 x 128 blocks along the
-  hidden dimension for x, 128 x 128 blocks for weights.
+  hidden dimension for x, 128 x 128 blocks for weights; fp8mx = the same
+  with every scale rounded up to a power of two (UE8M0).
 
 Independent streams: numpy SeedSequence([seed, stream]) with stream 0 for
 logits, 1 for activations and 2 + e for the weights of logical expert e.
@@ -79,22 +80,34 @@ def to_e4m3_codes(v: np.ndarray) -> np.ndarray:
     return code.astype(np.uint8) | sign
 
 
-def quant_rows_1x128(x: np.ndarray):
-    """[R, C] fp32 -> (e4m3 codes [R, C], fp32 scales [R, C/128])."""
+def _pow2_ceil(v: np.ndarray) -> np.ndarray:
+    """Smallest power of two >= v (fp32, v > 0): UE8M0 scales."""
+    m, e = np.frexp(v.astype(np.float64))
+    return np.ldexp(1.0, np.where(m == 0.5, e - 1, e)).astype(np.float32)
+
+
+def quant_rows_1x128(x: np.ndarray, pow2: bool = False):
+    """[R, C] fp32 -> (e4m3 codes [R, C], fp32 scales [R, C/128]); pow2:
+    scales rounded up to powers of two."""
     R, C = x.shape
     xb = x.reshape(R, C // 128, 128).astype(np.float32)
     amax = np.abs(xb).max(axis=2)
     sc = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
+    if pow2:
+        sc = _pow2_ceil(sc)
     q = to_e4m3_codes(xb / sc[:, :, None])
     return q.reshape(R, C), sc
 
 
-def quant_blocks_128x128(w: np.ndarray):
-    """[R, C] fp32 -> (e4m3 codes [R, C], fp32 scales [R/128, C/128])."""
+def quant_blocks_128x128(w: np.ndarray, pow2: bool = False):
+    """[R, C] fp32 -> (e4m3 codes [R, C], fp32 scales [R/128, C/128]); pow2:
+    scales rounded up to powers of two."""
     R, C = w.shape
     wb = w.reshape(R // 128, 128, C // 128, 128).astype(np.float32)
     amax = np.abs(wb).max(axis=3).max(axis=1)
     sc = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
+    if pow2:
+        sc = _pow2_ceil(sc)
     q = to_e4m3_codes(wb / sc[:, None, :, None])
     return q.reshape(R, C), sc
 
@@ -261,7 +274,7 @@ def activations(T: int, H: int, seed: int, dtype: str):
     x = _rng(seed, 1).standard_normal((T, H), dtype=np.float32)
     if dtype == "bf16":
         return to_bf16_bits(x), None
-    return quant_rows_1x128(x)
+    return quant_rows_1x128(x, pow2=dtype == "fp8mx")
 
 
 def expert_weights(e: int, H: int, I: int, seed: int, dtype: str, std: float = 0.02):
@@ -272,8 +285,8 @@ def expert_weights(e: int, H: int, I: int, seed: int, dtype: str, std: float = 0
     w2 = r.standard_normal((H, I), dtype=np.float32) * np.float32(std)
     if dtype == "bf16":
         return to_bf16_bits(w13), None, to_bf16_bits(w2), None
-    q13, s13 = quant_blocks_128x128(w13)
-    q2, s2 = quant_blocks_128x128(w2)
+    q13, s13 = quant_blocks_128x128(w13, pow2=dtype == "fp8mx")
+    q2, s2 = quant_blocks_128x128(w2, pow2=dtype == "fp8mx")
     return q13, s13, q2, s2
 
 
@@ -285,7 +298,7 @@ def slot_weights(slot_expert: np.ndarray, H: int, I: int, seed: int, dtype: str)
     w13 = np.empty((S, 2 * I, H), edt)
     w2 = np.empty((S, H, I), edt)
     s13 = s2 = None
-    if dtype == "fp8":
+    if dtype != "bf16":
         s13 = np.empty((S, 2 * I // 128, H // 128), np.float32)
         s2 = np.empty((S, H // 128, I // 128), np.float32)
     from concurrent.futures import ThreadPoolExecutor
@@ -297,7 +310,7 @@ def slot_weights(slot_expert: np.ndarray, H: int, I: int, seed: int, dtype: str)
         a, sa, b, sb = cache[e]
         w13[s] = a
         w2[s] = b
-        if dtype == "fp8":
+        if dtype != "bf16":
             s13[s] = sa
             s2[s] = sb
     return w13, s13, w2, s2
@@ -339,6 +352,10 @@ WORKLOADS = {
     "dsv3_decode_fp8": ("fp8", 256, 8, 256, 7168, 2048, 0.8, ("remote_hot", 4), ("uniform",)),
     "qwen3_prefill_bf16": ("bf16", 8192, 8, 128, 4096, 1536, 1.0, ("remote_hot", 2), ("uniform",)),
     "qwen3_prefill_fp8": ("fp8", 8192, 8, 128, 4096, 1536, 1.0, ("remote_hot", 2), ("uniform",)),
+    # fp8 with power-of-two (UE8M0) scales
+    "tiny_fp8mx": ("fp8mx", 96, 2, 6, 256, 512, 1.2, ("local_hot", 6, 2), ("uniform",)),
+    "qwen3_decode_fp8mx": ("fp8mx", 1024, 8, 128, 4096, 1536, 1.2, ("local_hot_strided", 16, 2), ("uniform",)),
+    "qwen3_prefill_fp8mx": ("fp8mx", 8192, 8, 128, 4096, 1536, 1.0, ("remote_hot", 2), ("uniform",)),
 }
 
 

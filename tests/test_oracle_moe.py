@@ -95,7 +95,7 @@ def _dense_numpy(x, xs, w13, s13, w2, s2, ids_slot, w, dtype):
     return y
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "fp8"])
+@pytest.mark.parametrize("dtype", ["bf16", "fp8", "fp8mx"])
 def test_moe_matches_dense_numpy(dtype):
     ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem(dtype)
     E, S = 3, len(se)
@@ -165,3 +165,35 @@ def test_nonlocal_and_padding_tokens_are_zero():
     d = oracle.dispatch(ids, 6, 3, 8, se, np.ones(4, np.uint32), np.zeros(3, np.uint32), np.zeros(3, np.int32))
     y = oracle.moe(x, w, oracle.pair_slot(d), w13, w2, "bf16")
     assert np.all(y[6:] == 0)
+
+
+def test_pow2_scales_are_minimal_powers_of_two():
+    """fp8mx inputs: every scale is a power of two, the block's amax / scale
+    is within e4m3's range and halving the scale would leave it."""
+    x = np.random.default_rng(1).standard_normal((40, 512)).astype(np.float32) * 3
+    x[3, :128] = 0
+    q, sc = synth.quant_rows_1x128(x, pow2=True)
+    m, _ = np.frexp(sc.astype(np.float64))
+    assert np.all(m == 0.5)
+    amax = np.abs(x.reshape(40, 4, 128)).max(axis=2)
+    nz = amax > 0
+    assert np.all(amax[nz] / sc[nz] <= 448.0) and np.all(amax[nz] / (sc[nz] / 2) > 448.0)
+    assert sc[3, 0] == 1.0
+
+
+def test_mirror_mode_pow2_h_quantisation():
+    """fp8mx mirror mode: h re-quantised with power-of-two block scales; the
+    output stays close to the exact mode and differs from fp8's mirror mode
+    (different h scales) while the exact modes agree (same codes, same
+    scales read the same way)."""
+    ids, w, se, x, xs, w13, s13, w2, s2 = _small_problem("fp8mx")
+    d = oracle.dispatch(ids, ids.shape[0], 3, 16, se, np.ones(4, np.uint32), np.zeros(3, np.uint32),
+                        np.zeros(3, np.int32))
+    ps = oracle.pair_slot(d)
+    ye = oracle.moe(x, w, ps, w13, w2, "fp8mx", "exact", xs, s13, s2)
+    ye8 = oracle.moe(x, w, ps, w13, w2, "fp8", "exact", xs, s13, s2)
+    assert np.array_equal(ye, ye8)
+    ym = oracle.moe(x, w, ps, w13, w2, "fp8mx", "mirror", xs, s13, s2)
+    ym8 = oracle.moe(x, w, ps, w13, w2, "fp8", "mirror", xs, s13, s2)
+    assert not np.array_equal(ym, ym8)
+    assert 0 < np.max(np.abs(ym - ye)) / np.max(np.abs(ye)) < 0.1
