@@ -29,7 +29,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
-MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}  # dense
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0, "fp8mx": 5000.0}  # dense
 
 
 def log(msg):
@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="qwen3_decode_bf16")
     ap.add_argument("--plan", default=None)
-    ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, else 128")
+    ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, 128 above, 256 for bf16 beyond 128 rows per expert")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copies", type=int, default=0, help="weight copies rotated per step (0 = auto)")
     ap.add_argument("--no-cpu-baseline", action="store_true")

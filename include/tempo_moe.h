@@ -65,6 +65,12 @@ extern "C" {
 
 #define TEMPO_BF16 0
 #define TEMPO_FP8_E4M3 1
+/* fp8 e4m3 whose scales (x_scale, w13_scale, w2_scale) are powers of two
+ * (UE8M0): stage 2 applies them in the MFMA's hardware block scaling instead
+ * of scaling every step's partial sums, and re-quantises h with the smallest
+ * power of two >= amax / 448.  Scales that are not powers of two give wrong
+ * results (their mantissas are dropped). */
+#define TEMPO_FP8_E4M3_UE8M0 2
 
 /*
  * Problem shape.
@@ -78,7 +84,7 @@ extern "C" {
  *   H, I     hidden and expert-intermediate sizes, multiples of 128
  *   m_tile   M-tile: every activated slot's rows are padded to a multiple of
  *            it (Sec. 2.2, Eq. 2); 64, 128, 192 or 256
- *   dtype    TEMPO_BF16 or TEMPO_FP8_E4M3 (activations and weights)
+ *   dtype    TEMPO_BF16, TEMPO_FP8_E4M3 or TEMPO_FP8_E4M3_UE8M0 (activations and weights)
  */
 typedef struct tempo_moe_shape {
   int32_t T, T_valid, K, E, S, H, I, m_tile, dtype;

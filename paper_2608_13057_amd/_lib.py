@@ -23,6 +23,7 @@ TEMPO_PLAN_SAMPLE = 2
 
 TEMPO_BF16 = 0
 TEMPO_FP8_E4M3 = 1
+TEMPO_FP8_E4M3_UE8M0 = 2
 
 SYMBOLS = ("tempo_moe_query", "tempo_moe_pack_weights", "tempo_moe_dispatch", "tempo_moe_experts", "tempo_moe_combine",
            "tempo_moe_forward", "tempo_moe_device_error", "tempo_moe_strerror")

@@ -78,7 +78,7 @@ static int check_shape(const tempo_moe_shape* s) {
   if (s->K > kMaxK || s->K > s->E || s->E > kMaxE || s->S > kMaxS) return TEMPO_EINVAL;
   if (s->H % 128 || s->I % 128) return TEMPO_EINVAL;
   if (s->m_tile != 64 && s->m_tile != 128 && s->m_tile != 192 && s->m_tile != 256) return TEMPO_EINVAL;
-  if (s->dtype != TEMPO_BF16 && s->dtype != TEMPO_FP8_E4M3) return TEMPO_EINVAL;
+  if (s->dtype != TEMPO_BF16 && s->dtype != TEMPO_FP8_E4M3 && s->dtype != TEMPO_FP8_E4M3_UE8M0) return TEMPO_EINVAL;
   // row indices and element offsets stay within int32 / the addressable range
   const long long P = (long long)s->T * s->K;
   const long long cap = P + (long long)s->S * (s->m_tile - 1);
@@ -96,13 +96,13 @@ static int check_plan(const tempo_plan* p) {
 static int check_disp(const tempo_moe_shape* s, const tempo_dispatch_out* d, bool need_index_outputs) {
   if (!d || !d->slot_counts || !d->slot_offsets || !d->x_perm) return TEMPO_EINVAL;
   if (need_index_outputs && (!d->expert_counts || !d->row_token || !d->pair_row)) return TEMPO_EINVAL;
-  if (s->dtype == TEMPO_FP8_E4M3 && !d->x_perm_scale) return TEMPO_EINVAL;
+  if (s->dtype != TEMPO_BF16 && !d->x_perm_scale) return TEMPO_EINVAL;
   return TEMPO_OK;
 }
 
 static int check_weights(const tempo_moe_shape* s, const tempo_expert_weights* w) {
   if (!w || !w->w13 || !w->w2) return TEMPO_EINVAL;
-  if (s->dtype == TEMPO_FP8_E4M3 && (!w->w13_scale || !w->w2_scale)) return TEMPO_EINVAL;
+  if (s->dtype != TEMPO_BF16 && (!w->w13_scale || !w->w2_scale)) return TEMPO_EINVAL;
   return TEMPO_OK;
 }
 
@@ -129,7 +129,7 @@ int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weig
   int rc = check_shape(shape);
   if (rc) return rc;
   if (!natural || !packed || !natural->w13 || !natural->w2 || !packed->w13 || !packed->w2) return TEMPO_EINVAL;
-  if (shape->dtype == TEMPO_FP8_E4M3 &&
+  if (shape->dtype != TEMPO_BF16 &&
       (!natural->w13_scale || !natural->w2_scale || !packed->w13_scale || !packed->w2_scale))
     return TEMPO_EINVAL;
   const size_t es = shape->dtype == TEMPO_BF16 ? 2 : 1;
@@ -142,7 +142,7 @@ int tempo_moe_pack_weights(const tempo_moe_shape* shape, const tempo_expert_weig
       overlap(natural->w13, b13, packed->w2, b2) || overlap(natural->w2, b2, packed->w13, b13) ||
       overlap(packed->w13, b13, packed->w2, b2))
     return TEMPO_EINVAL;
-  if (shape->dtype == TEMPO_FP8_E4M3) {
+  if (shape->dtype != TEMPO_BF16) {
     const size_t kb = shape->H / 128, ib = shape->I / 128;
     const size_t n13 = (size_t)shape->S * 2 * ib * kb * 4, n2 = (size_t)shape->S * kb * ib * 4;
     const size_t p13 = (size_t)shape->S * (shape->I / 64) * kb * 16, p2 = (size_t)shape->S * kb * ib * 16;
@@ -165,7 +165,7 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
   if (rc) return rc;
   if ((rc = check_plan(plan)) || (rc = check_disp(shape, out, true))) return rc;
   if ((plan->flags & TEMPO_PLAN_SAMPLE) && !dispatch_sample_supported(*shape)) return TEMPO_EUNSUPPORTED;
-  if (!topk_ids || !x || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale)) return TEMPO_EINVAL;
+  if (!topk_ids || !x || !workspace || (shape->dtype != TEMPO_BF16 && !x_scale)) return TEMPO_EINVAL;
   const Layout L = make_layout(*shape);
   if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
   return dev_status(launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *out, static_cast<char*>(workspace), L,
@@ -209,7 +209,7 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   if ((rc = check_plan(plan)) || (rc = check_disp(shape, disp, true)) || (rc = check_weights(shape, weights)))
     return rc;
   if ((plan->flags & TEMPO_PLAN_SAMPLE) && !dispatch_sample_supported(*shape)) return TEMPO_EUNSUPPORTED;
-  if (!topk_ids || !topk_w || !x || !y || !workspace || (shape->dtype == TEMPO_FP8_E4M3 && !x_scale))
+  if (!topk_ids || !topk_w || !x || !y || !workspace || (shape->dtype != TEMPO_BF16 && !x_scale))
     return TEMPO_EINVAL;
   const Layout L = make_layout(*shape);
   if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;

@@ -3,7 +3,9 @@
 // the contraction, weights 128 x 128), the DeepSeek-V3 / Qwen3-FP8 convention
 // the paper's fp8 grouped GEMM runs (Sec. 2.2).
 //   gate/up:  h = silu(g) * u with g, u = sum_kb (A_kb W_kb^T) * sA[row,kb] * sW[blk,kb]
-//   requant:  h -> e4m3 with per-row 1 x 128 scales amax / 448 (saturating)
+//   requant:  h -> e4m3 with per-row 1 x 128 scales amax / 448 (saturating;
+//             rounded up to a power of two for the UE8M0 variant, whose GEMMs
+//             apply the scales in the MFMA's block scaling)
 //   down:     y_perm = sum_kb (h_kb W2_kb^T) * sh[row,kb] * sW2[blk,kb]  -> bf16
 // One pipeline step is one 128-element scale block of the contraction.
 #include <algorithm>
@@ -19,6 +21,9 @@ using namespace gemm;
 // scale = amax / 448 (1 if the block is all zero), q = e4m3(h / scale) with
 // round-to-nearest-even, magnitudes saturated at 448.  One wavefront per row,
 // two columns per lane per block.  Scales are stored block-major.
+// MX: the scale is rounded up to a power of two (UE8M0), the smallest one at
+// least amax / 448.
+template <bool MX>
 __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, int I, int row_cap,
                                                  const int32_t* __restrict__ row_token,
                                                  const int32_t* __restrict__ slot_offsets, int S,
@@ -37,7 +42,12 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
       float m = fmaxf(fabsf(v.x), fabsf(v.y));
 #pragma unroll
       for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d));
-      const float sc = m > 0.f ? m / 448.0f : 1.0f;
+      float sc = m > 0.f ? m / 448.0f : 1.0f;
+      if (MX && m > 0.f) {
+        uint32_t bits = __float_as_uint(sc);
+        if (bits & 0x7FFFFFu) bits = (bits & 0xFF800000u) + 0x800000u;  // next power of two up
+        sc = __uint_as_float(bits);
+      }
       const float q0 = fminf(fmaxf(v.x / sc, -448.f), 448.f), q1 = fminf(fmaxf(v.y / sc, -448.f), 448.f);
       dst[b * 64 + lane] = (uint16_t)(__builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false) & 0xFFFF);
       if (lane == 0) h_scale[(size_t)b * row_cap + row] = sc;
@@ -45,7 +55,7 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
   }
 }
 
-template <int BM>
+template <int BM, bool MX>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                      const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                      hipStream_t st) {
@@ -79,10 +89,10 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.Kd = s.H;
   gu.Nout = s.I;
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
-  hipLaunchKernelGGL((k_gemm<true, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
+  hipLaunchKernelGGL((k_gemm<true, BM, true, MX>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
   if (!mark(0)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
-  hipLaunchKernelGGL(k_quant_h, dim3(std::min(ceil_div(L.row_cap, 4), persistent_grid(8))), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
+  hipLaunchKernelGGL(k_quant_h<MX>, dim3(std::min(ceil_div(L.row_cap, 4), persistent_grid(8))), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
   if (!mark(1)) return hipErrorLaunchFailure;
 
@@ -97,7 +107,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.C = y_perm;
   dn.Kd = s.I;
   dn.Nout = s.H;
-  hipLaunchKernelGGL((k_gemm<true, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
+  hipLaunchKernelGGL((k_gemm<true, BM, false, MX>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
   if (!mark(2)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
@@ -110,10 +120,17 @@ bool experts_supported(const tempo_moe_shape&) { return true; }
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                               hipStream_t st) {
-  if (s.m_tile == 128) return launch_bm<128>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 64) return launch_bm<64>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 256) return launch_bm<256>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 192) return launch_bm<192>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.dtype == TEMPO_FP8_E4M3_UE8M0) {
+    if (s.m_tile == 128) return launch_bm<128, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 64) return launch_bm<64, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 256) return launch_bm<256, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 192) return launch_bm<192, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    return hipErrorInvalidValue;
+  }
+  if (s.m_tile == 128) return launch_bm<128, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 64) return launch_bm<64, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 256) return launch_bm<256, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 192) return launch_bm<192, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   return hipErrorInvalidValue;
 }
 

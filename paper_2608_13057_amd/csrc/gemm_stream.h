@@ -255,7 +255,10 @@ __device__ __forceinline__ void static_for(F&& f) {
 
 constexpr int GEMM_THREADS = 256;
 
-template <bool FP8, int BM, bool GATEUP>
+// MX (fp8 only): the scales are powers of two and go to the MFMA as per-lane
+// UE8M0 exponents (each lane supplies the activation row and the weight column
+// it holds), so the products accumulate straight into the running sums.
+template <bool FP8, int BM, bool GATEUP, bool MX = false>
 __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   constexpr int MI = BM / 32;               // row blocks of 32
   constexpr int AG = BM / 32;               // activation 8-row groups per wavefront
@@ -527,9 +530,24 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
                                wr[d][1][0], wr[d][1][1], wr[d][1][2], wr[d][1][3]};
       const i32x8 b1 = (i32x8){wr[d][2][0], wr[d][2][1], wr[d][2][2], wr[d][2][3],
                                wr[d][3][0], wr[d][3][1], wr[d][3][2], wr[d][3][3]};
+      // MX: the exponent byte of a power-of-two fp32 scale is its UE8M0 code
+      const int eb = MX ? (int)((__float_as_uint(sw) >> 23) & 0xFF) : 127;
 #pragma unroll
       for (int mi = 0; mi < MI; mi++) {
-        if (mi < live) {
+        if (MX && mi < live) {
+          const int r = mi * 32 + bcol;
+          i32x8 a[2];
+#pragma unroll
+          for (int h = 0; h < 2; h++) {
+            const int c = 4 * h + 2 * (lane >> 5);
+            const i32x4 lo = *reinterpret_cast<const i32x4*>(st + swz(r, c));
+            const i32x4 hi = *reinterpret_cast<const i32x4*>(st + swz(r, c + 1));
+            a[h] = (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          }
+          const int ea = (int)((__float_as_uint(sa_lds[r]) >> 23) & 0xFF);  // this lane's activation row
+          acc[mi] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[0], b0, acc[mi], 0, 0, 0, ea, 0, eb);
+          acc[mi] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[1], b1, acc[mi], 0, 0, 0, ea, 0, eb);
+        } else if (!MX && mi < live) {
           const int r = mi * 32 + bcol;
           i32x8 a[2];
 #pragma unroll

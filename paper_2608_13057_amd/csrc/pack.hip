@@ -89,7 +89,7 @@ hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& nat
                      static_cast<uint4*>(const_cast<void*>(pk.w13)), s.S, 2 * s.I, rc13, 1, s.I, es == 1);
   hipLaunchKernelGGL(k_pack, dim3(g2), dim3(256), 0, st, static_cast<const uint4*>(nat.w2),
                      static_cast<uint4*>(const_cast<void*>(pk.w2)), s.S, s.H, rc2, 0, 0, es == 1);
-  if (s.dtype == TEMPO_FP8_E4M3) {
+  if (s.dtype != TEMPO_BF16) {
     // gate/up: I/64 output blocks x H/128 steps; down: H/128 blocks x I/128 steps
     const size_t m13 = (size_t)s.S * (s.I / 64) * (s.H / 128), m2 = (size_t)s.S * (s.H / 128) * (s.I / 128);
     hipLaunchKernelGGL(k_pack_scales, dim3((int)((m13 + 255) / 256 < 65536 ? (m13 + 255) / 256 : 65536)), dim3(256), 0,

@@ -16,7 +16,7 @@ import torch
 from . import _lib
 from ._lib import DispatchOut, ExpertWeights, Plan, Shape, check
 
-DTYPES = {"bf16": _lib.TEMPO_BF16, "fp8": _lib.TEMPO_FP8_E4M3}
+DTYPES = {"bf16": _lib.TEMPO_BF16, "fp8": _lib.TEMPO_FP8_E4M3, "fp8mx": _lib.TEMPO_FP8_E4M3_UE8M0}
 
 
 def to_device(a, device="cuda") -> torch.Tensor:
@@ -122,7 +122,7 @@ class DispatchBuffers:
             pair_row=torch.empty(shape.T, shape.K, **i32),
             x_perm=torch.empty(row_cap, shape.H, dtype=shape.elem, device=device),
             x_perm_scale=(torch.empty(shape.H // 128, row_cap, dtype=torch.float32, device=device)
-                          if shape.dtype == "fp8" else None),
+                          if shape.dtype != "bf16" else None),
             cum_counts=torch.zeros(shape.E, dtype=torch.int32, device=device) if cum_counts else None,
         )
 
@@ -165,7 +165,7 @@ def pack_weights(shape: MoEShape, natural: WeightTensors, stream=None) -> Weight
     scales ([S, I/64, H/128, 4] and [S, H/128, I/128, 4] fp32)."""
     _check_weights(shape, natural)
     s13 = s2 = None
-    if shape.dtype == "fp8":
+    if shape.dtype != "bf16":
         dev = natural.w13.device
         s13 = torch.empty(shape.S, shape.I // 64, shape.H // 128, 4, dtype=torch.float32, device=dev)
         s2 = torch.empty(shape.S, shape.H // 128, shape.I // 128, 4, dtype=torch.float32, device=dev)
@@ -179,7 +179,7 @@ def pack_weights(shape: MoEShape, natural: WeightTensors, stream=None) -> Weight
 def _check_inputs(shape, topk_ids, x, x_scale):
     _need(topk_ids, torch.int32, (shape.T, shape.K), "topk_ids")
     _need(x, shape.elem, (shape.T, shape.H), "x")
-    if shape.dtype == "fp8":
+    if shape.dtype != "bf16":
         _need(x_scale, torch.float32, (shape.T, shape.H // 128), "x_scale")
 
 
@@ -193,7 +193,7 @@ def _check_plan(shape, plan):
 def _check_weights(shape, w, packed=False):
     _need(w.w13, shape.elem, (shape.S, 2 * shape.I, shape.H), "w13")
     _need(w.w2, shape.elem, (shape.S, shape.H, shape.I), "w2")
-    if shape.dtype == "fp8":
+    if shape.dtype != "bf16":
         if packed:
             _need(w.w13_scale, torch.float32, (shape.S, shape.I // 64, shape.H // 128, 4), "packed w13_scale")
             _need(w.w2_scale, torch.float32, (shape.S, shape.H // 128, shape.I // 128, 4), "packed w2_scale")
@@ -212,7 +212,7 @@ def _check_disp(shape, d, row_cap):
         _need(d.row_token, torch.int32, (row_cap,), "row_token")
     if d.pair_row is not None:
         _need(d.pair_row, torch.int32, (shape.T, shape.K), "pair_row")
-    if shape.dtype == "fp8":
+    if shape.dtype != "bf16":
         _need(d.x_perm_scale, torch.float32, (shape.H // 128, row_cap), "x_perm_scale")
     if d.cum_counts is not None:
         _need(d.cum_counts, torch.int32, (shape.E,), "cum_counts")
