@@ -130,7 +130,11 @@ def _mean_counter(rows, counter: str, match):
 
 
 def _is_gateup(name: str) -> bool:
-    return "k_gemm<" in name and name.replace(" ", "").split("(")[0].endswith(",true>")
+    """The stream-K GEMM instance with GATEUP (its third template argument)."""
+    if "k_gemm<" not in name:
+        return False
+    args = name.replace(" ", "").split("k_gemm<", 1)[1].split(">", 1)[0].split(",")
+    return len(args) >= 3 and args[2] == "true"
 
 
 def _is_copy(name: str) -> bool:
