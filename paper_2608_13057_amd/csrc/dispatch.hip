@@ -460,7 +460,7 @@ __global__ __launch_bounds__(256) void k_scan(const int32_t* __restrict__ blk_hi
 template <int ESIZE, int CHUNK>
 __global__ __launch_bounds__(256) void k_place(
     const int32_t* __restrict__ ids, int P, int Pv, int K, int E, int S, int M, int snap, int H, int row_cap, int nblk,
-    int gather_rows, const int32_t* __restrict__ blk_hist, const int32_t* __restrict__ blk_pre,
+    int copies, const int32_t* __restrict__ blk_hist, const int32_t* __restrict__ blk_pre,
     const uint32_t* __restrict__ blk_err,
     const int32_t* __restrict__ local_rank, const int32_t* __restrict__ slot_expert,
     const uint32_t* __restrict__ slot_weight, const uint32_t* __restrict__ remote_weight,
@@ -598,12 +598,12 @@ __global__ __launch_bounds__(256) void k_place(
   const int R = s_nplaced;
   const int nch = H * ESIZE / 16;
   for (int j = w; j < R; j += 4) {
-    if (ESIZE == 1) {  // scales are stored block-major: [H/128][row_cap]
+    if (ESIZE == 1 && (copies & 2)) {  // scales are stored block-major: [H/128][row_cap]
       const int ns = H / 128;
       for (int i = lane; i < ns; i += 64)
         x_perm_scale[(size_t)i * row_cap + s_prow[j]] = x_scale[(size_t)s_ptok[j] * ns + i];
     }
-    if (!gather_rows) continue;
+    if (!(copies & 1)) continue;
     const uint4* __restrict__ src = reinterpret_cast<const uint4*>(x) + (size_t)s_ptok[j] * nch;
     uint4* __restrict__ dst = reinterpret_cast<uint4*>(x_perm) + (size_t)s_prow[j] * nch;
     constexpr int U = 8;
@@ -1050,10 +1050,14 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   }
   const bool large = blk_pre != nullptr;
   const int nb = ceil_div(P, large ? kPlaceChunkLarge : kPlaceChunk);
+  // row and scale copies: inside k_place for small batches; for large ones a
+  // row-parallel launch after it (a placing block holds a few dozen rows, too
+  // few loads in flight)
+  const int copies = large ? 0 : (gather_rows ? 1 : 0) | (s.dtype != TEMPO_BF16 ? 2 : 0);
   const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
   auto launch = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, snap, s.H, L.row_cap,
-                       L.nblk, gather_rows ? 1 : 0, blk_hist, blk_pre, blk_err, local_rank, plan.slot_expert,
+                       L.nblk, copies, blk_hist, blk_pre, blk_err, local_rank, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, static_cast<const uint8_t*>(x),
                        x_scale, static_cast<uint8_t*>(out.x_perm), out.x_perm_scale, hdr, timing ? 1 : 0, t0, t1);
@@ -1064,6 +1068,17 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   } else {
     if (large) launch(k_place<1, kPlaceChunkLarge>);
     else launch(k_place<1, kPlaceChunk>);
+  }
+  if (large && (gather_rows || s.dtype != TEMPO_BF16)) {
+    const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
+    if (s.dtype == TEMPO_BF16)
+      hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
+                         L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                         static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+    else
+      hipLaunchKernelGGL(k_gather_rows<1>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
+                         L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                         static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
   }
   return hipGetLastError();
 }

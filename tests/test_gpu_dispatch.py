@@ -31,7 +31,7 @@ def _compare(case, d_ref, check_rows=True):
 
 
 @pytest.mark.parametrize("name", ["tiny", "qwen3_decode_bf16", "qwen3_decode_fp8", "dsv3_decode_fp8",
-                                  "qwen3_prefill_bf16"])
+                                  "qwen3_prefill_bf16", "qwen3_prefill_fp8"])
 @pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
 def test_dispatch_workloads_bit_exact(name, m_tile):
     from paper_2608_13057_amd import moe, synth
