@@ -158,8 +158,8 @@ def cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, m_tile, budget_s):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs one GPU's share of the EP MoE block on one GPU only; multi-GPU runs (dispatch/"
-              "combine all-to-all over xGMI) are not part of this build.", file=sys.stderr)
+        print("bench.py runs one GPU's share of the EP MoE block on one GPU only; the library has no multi-GPU "
+              "path (dispatch / combine all-to-all over xGMI), so --gpus must be 1.", file=sys.stderr)
         return 2
 
     import torch
