@@ -295,3 +295,28 @@ def test_counts_solver_plan_loop(name):
     for e in np.unique(se):
         assert sc[se == e].sum() == x[e, 0], e
     assert sc.sum() == x[:, 0].sum()
+
+
+def test_dispatch_at_the_limits():
+    """The kernels' size limits: 1024 experts, 256 slots and top-32 routing
+    through the multi-block stage 1 (scanned prefixes, the block-wide plan);
+    exactly 8192 pairs with 256 experts and 256 slots through the single
+    workgroup, in the split and the sampled modes, via the dispatch entry
+    point and the forward."""
+    from paper_2608_13057_amd import moe
+
+    rng = np.random.default_rng(2024)
+    wl = _random_workload(rng, 300, 32, 1024, 256)
+    c = Case(wl, "rand", 256, weights=False)
+    print("[limits] E=1024 S=256 K=32 T=300 M=256", flush=True)
+    moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+    _compare(c, c.oracle_dispatch())
+    wl = _random_workload(rng, 256, 32, 256, 256)
+    for key in (None, 77):
+        print(f"[limits] E=256 S=256 K=32 T=256 M=64 sample={key}", flush=True)
+        c = Case(wl, "rand", 64, sample_seed=key)
+        ref = c.oracle_dispatch()
+        moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
+        _compare(c, ref)
+        _forward(c)
+        _compare(c, ref, check_rows=False)
