@@ -4,15 +4,20 @@
 A step is one pass of the whole block -- stage 1 dispatch (counts, plan split,
 M-tile padded permute), stage 2 grouped expert FFN (gate/up + SwiGLU, down)
 and stage 3 combine -- over one synthetic batch already resident in HBM.
-Default workload: the Qwen3-235B-shaped decode share (18 local slots = 16 home
-experts of 128 + 2 replicas of the hottest, H 4096, I 1536, bf16, 512
-tokens, top-8, Zipf(1.0) popularity, token-balancing plan).
+Default workload: the Qwen3-235B-shaped prefill share (18 local slots = 16
+home experts of 128 + 2 replicas of the hottest experts homed elsewhere,
+H 4096, I 1536, bf16, 8192 tokens, top-8, Zipf(1.0) popularity, uniform
+plan), the largest configuration; almost every slot is in the linear
+(compute-bound) regime of the cost model.
 
-Prints ONE JSON line with the block time (us/batch, lower is better), the
-roofline of the dominant kernel (the gate/up GEMM, HBM-bound in decode),
+Prints ONE JSON line: the block time (us/batch, lower is better), the
+roofline of the dominant kernel (the gate/up GEMM: MFMA-bound at prefill,
+HBM-bound at decode), the same for the flat-regime decode share
+(`roofline_flat`: 512 tokens, the weight-streaming regime), the fitted
+max-affine profile (a, b, c, beta, n*) of the headline's dtype and M-tile,
 per-stage times, and the CPU oracle timed on the host cores as a baseline.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME] [--no-flat]
 """
 from __future__ import annotations
 
@@ -41,7 +46,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3_decode_bf16")
+    ap.add_argument("--workload", default="qwen3_prefill_bf16")
+    ap.add_argument("--flat-workload", default="qwen3_decode_bf16",
+                    help="the weight-streaming (decode) share measured beside the headline for roofline_flat")
+    ap.add_argument("--no-flat", action="store_true")
     ap.add_argument("--plan", default=None)
     ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, 128 above, 256 for bf16 beyond 128 rows per expert")
     ap.add_argument("--seed", type=int, default=0)
@@ -155,68 +163,65 @@ def cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, m_tile, budget_s):
     }
 
 
-def main():
-    args = parse()
-    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs one GPU's share of the EP MoE block on one GPU only; the library has no multi-GPU "
-              "path (dispatch / combine all-to-all over xGMI), so --gpus must be 1.", file=sys.stderr)
-        return 2
+class Measured:
+    """Timings of one workload's block on the GPU (see measure_workload)."""
 
-    import torch
 
-    from paper_2608_13057_amd import moe, synth
+def measure_workload(torch, name, m_tile, plan_name, steps, warmup, seed, copies_arg, spin):
+    """Build a workload's inputs in HBM, then time K back-to-back HIP-graph
+    replays of the whole block (the headline) and K eager steps with HIP
+    events between the stages and around the two GEMM kernels, recorded on
+    the stream the kernels run on."""
+    from paper_2608_13057_amd import measure, moe, synth
     from paper_2608_13057_amd.moe import to_device as to_dev
 
-    from paper_2608_13057_amd import measure
-
-    wl = synth.make_workload(args.workload, seed=args.seed)
-    args.m_tile = args.m_tile or measure.auto_m_tile(wl)
-    plan_name = args.plan or next(iter(wl.plans))
-    plan = wl.plans[plan_name]
-    log(f"workload {args.workload} plan {plan_name} T={wl.T} K={wl.K} E={wl.E} S={wl.S} H={wl.H} I={wl.I}")
+    m = Measured()
+    wl = synth.make_workload(name, seed=seed)
+    m.wl, m.name = wl, name
+    m.m_tile = m_tile or measure.auto_m_tile(wl)
+    m.plan_name = plan_name or next(iter(wl.plans))
+    plan = m.plan = wl.plans[m.plan_name]
+    log(f"workload {name} plan {m.plan_name} T={wl.T} K={wl.K} E={wl.E} S={wl.S} H={wl.H} I={wl.I} M={m.m_tile}")
     t0 = time.perf_counter()
-    x, xs = synth.activations(wl.T, wl.H, wl.seed, wl.dtype)
-    w13, s13, w2, s2 = synth.slot_weights(wl.placement.slot_expert, wl.H, wl.I, wl.seed, wl.dtype)
+    m.x, m.xs = synth.activations(wl.T, wl.H, wl.seed, wl.dtype)
+    m.w13, m.s13, m.w2, m.s2 = synth.slot_weights(wl.placement.slot_expert, wl.H, wl.I, wl.seed, wl.dtype)
     log(f"generated inputs in {time.perf_counter() - t0:.1f} s")
 
     dev = "cuda"
-    shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=args.m_tile, dtype=wl.dtype)
-    d_ids, d_w, d_x = to_dev(wl.topk_ids), to_dev(wl.topk_w), to_dev(x)
-    d_xs = None if xs is None else to_dev(xs)
+    shape = moe.MoEShape(T=wl.T, K=wl.K, E=wl.E, S=wl.S, H=wl.H, I=wl.I, m_tile=m.m_tile, dtype=wl.dtype)
+    d_ids, d_w, d_x = to_dev(wl.topk_ids), to_dev(wl.topk_w), to_dev(m.x)
+    d_xs = None if m.xs is None else to_dev(m.xs)
     d_plan = moe.PlanTensors(to_dev(wl.placement.slot_expert), to_dev(plan.slot_weight),
                              to_dev(plan.remote_weight), to_dev(plan.remote_replicas))
-    natural = moe.WeightTensors(to_dev(w13), to_dev(w2), None if s13 is None else to_dev(s13),
-                                None if s2 is None else to_dev(s2))
+    natural = moe.WeightTensors(to_dev(m.w13), to_dev(m.w2), None if m.s13 is None else to_dev(m.s13),
+                                None if m.s2 is None else to_dev(m.s2))
     weights0 = moe.pack_weights(shape, natural)  # one-time re-layout, outside the timed region
     del natural
     wbytes = weights0.w13.numel() * weights0.w13.element_size() + weights0.w2.numel() * weights0.w2.element_size()
     # rotate weight copies so that one cycle streams > 2 x the 256 MB Infinity Cache
-    copies = args.copies or max(2, math.ceil(1.0e9 / wbytes))
+    copies = m.copies = copies_arg or max(2, math.ceil(1.0e9 / wbytes))
     wsets = [weights0] + [moe.WeightTensors(*(None if t is None else t.clone() for t in
                                               (weights0.w13, weights0.w2, weights0.w13_scale, weights0.w2_scale)))
                           for _ in range(copies - 1)]
     ws = moe.Workspace(shape, dev)
     disp = moe.DispatchBuffers.allocate(shape, ws.row_cap, dev)
     y = torch.empty(wl.T, wl.H, dtype=torch.int16, device=dev)
-
     fwd = [moe.PreparedForward(shape, d_plan, d_ids, d_w, d_x, d_xs, wsets[i], disp, y, ws) for i in range(copies)]
 
-    for i in range(args.warmup):
+    for i in range(warmup):
         fwd[i % copies]()
     torch.cuda.synchronize()
     if moe.device_error(ws) != 0:
         raise RuntimeError("device reported a data error")
     sc = disp.slot_counts.cpu().numpy()
-    G, N = int((sc > 0).sum()), int(sc.sum())
-    tiles = int(sum(-(-int(c) // args.m_tile) for c in sc))
-    log(f"G={G} N={N} tiles={tiles} slot_counts={sc.tolist()}")
+    m.G, m.N = int((sc > 0).sum()), int(sc.sum())
+    m.tiles = int(sum(-(-int(c) // m.m_tile) for c in sc))
+    log(f"G={m.G} N={m.N} tiles={m.tiles} slot_counts={sc.tolist()}")
+    K = steps
 
-    # The host enqueues a whole timed loop while the GPU spins on a short
-    # kernel, so launch overhead never shows up between steps.
-    spin = calibrate_spin(torch)
-    K = args.steps
-
-    # (1) headline: K back-to-back replays of HIP graphs of the whole block
+    # (1) headline: K back-to-back replays of HIP graphs of the whole block;
+    # the host enqueues the whole loop while the GPU spins on a short kernel,
+    # so launch overhead never shows up between steps
     graphs = []
     for i in range(copies):
         g = torch.cuda.CUDAGraph()
@@ -228,15 +233,13 @@ def main():
     torch.cuda.synchronize()
     ev_a, ev_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t_wall = time.perf_counter()
     torch.cuda._sleep(spin)
     ev_a.record()
     for i in range(K):
         graphs[i % copies].replay()
     ev_b.record()
     torch.cuda.synchronize()
-    t_wall = time.perf_counter() - t_wall
-    ms_per_step = ev_a.elapsed_time(ev_b) / K
+    m.ms_per_step = ev_a.elapsed_time(ev_b) / K
 
     # (2) per-kernel times: K eager steps with HIP events between the stages
     # and around the two GEMM kernels, all on the stream the kernels run on
@@ -251,41 +254,86 @@ def main():
         fwd[i % copies](stage_events=evs[i])
     torch.cuda.synchronize()
     at = np.array([[evs[i][0].elapsed_time(evs[i][j]) for j in range(NE)] for i in range(K)]) * 1e3  # us
-    eager_ms = evs[0][0].elapsed_time(evs[K - 1][NE - 1]) / K
-    stage_us = {
+    m.eager_ms = evs[0][0].elapsed_time(evs[K - 1][NE - 1]) / K
+    m.stage_us = {
         "dispatch": float(np.mean(at[:, 1])),
         "gate_up": float(np.mean(at[:, 3] - at[:, 1])),
         "down": float(np.mean(at[:, 5] - at[:, 3])),
         "combine": float(np.mean(at[:, 6] - at[:, 5])),
     }
-    kernel_us = {"gate_up_gemm": float(np.mean(at[:, 2] - at[:, 1])), "down_gemm": float(np.mean(at[:, 4] - at[:, 3]))}
-    log(f"graph ms/step {ms_per_step:.4f} eager(events) ms/step {eager_ms:.4f} stages_us {stage_us} kernels_us {kernel_us}")
+    m.kernel_us = {"gate_up_gemm": float(np.mean(at[:, 2] - at[:, 1])),
+                   "down_gemm": float(np.mean(at[:, 4] - at[:, 3]))}
+    log(f"{name}: graph ms/step {m.ms_per_step:.4f} eager(events) ms/step {m.eager_ms:.4f} "
+        f"stages_us {m.stage_us} kernels_us {m.kernel_us}")
+    del graphs, fwd, wsets, weights0, ws, disp, y
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return m
+
+
+def roofline(m):
+    """Roofline of the dominant kernel, the gate/up GEMM launch: MFMA-bound
+    (useful flops 2 N H 2I per launch against the dense peak of the dtype)
+    when the path runs the large-tile kernel or most pairs sit in slots past
+    the MFMA/HBM balance point, otherwise HBM-bound (weights of the G
+    activated slots once + the N real activation rows in and h rows out)."""
+    from paper_2608_13057_amd import measure
+
+    wl = m.wl
+    gu_s = m.kernel_us["gate_up_gemm"] * 1e-6
+    kernel = measure.gateup_kernel_name(wl.dtype, m.m_tile, wl.H)
+    traffic, traffic_current = measure.committed_traffic(m.name, m.m_tile)
+    common = {"traffic": traffic if traffic_current else None, "kernel": kernel + " (gate/up)",
+              "launch_us": m.kernel_us["gate_up_gemm"], "G": m.G, "N": m.N}
+    # pairs per activated slot against the ideal balance point e P / (2 BW) ~ 312
+    linear = measure.uses_big_kernel(wl.dtype, m.m_tile, wl.H) or m.N / max(1, m.G) > 312
+    if linear:
+        fl = gemm_flops(wl, m.N, "gateup")
+        peak = MFMA_PEAK_TFLOPS[wl.dtype]
+        ach = fl / gu_s / 1e12
+        return {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+                **common, "flops_per_launch": fl}
+    b = gemm_bytes(wl, wl.dtype, m.G, m.N, "gateup")
+    ach = b / gu_s / 1e9
+    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+            **common, "bytes_per_launch": b}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs one GPU's share of the EP MoE block on one GPU only; the library has no multi-GPU "
+              "path (dispatch / combine all-to-all over xGMI), so --gpus must be 1.", file=sys.stderr)
+        return 2
+
+    import torch
+
+    from paper_2608_13057_amd import measure, synth
+
+    spin = calibrate_spin(torch)
+    m = measure_workload(torch, args.workload, args.m_tile, args.plan, args.steps, args.warmup, args.seed,
+                         args.copies, spin)
+    wl = m.wl
     copy_gbs = attainable_copy_gbs(torch, spin)
     log(f"attainable copy bandwidth {copy_gbs:.0f} GB/s")
-
-    gu_s = kernel_us["gate_up_gemm"] * 1e-6
-    dn_s = kernel_us["down_gemm"] * 1e-6
-    gu_bytes = gemm_bytes(wl, wl.dtype, G, N, "gateup")
-    dn_bytes = gemm_bytes(wl, wl.dtype, G, N, "down")
-    traffic, traffic_current = measure.committed_traffic(args.workload, args.m_tile)
-    roof = {"bound": "hbm", "achieved": gu_bytes / gu_s / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gu_bytes / gu_s / 1e9 / HBM_PEAK_GBS,
-            "traffic": traffic if traffic_current else None,
-            "kernel": f"tempo::gemm::k_gemm<{'true' if wl.dtype != 'bf16' else 'false'}, {args.m_tile}, true> (gate/up)",
-            "bytes_per_launch": gu_bytes, "launch_us": kernel_us["gate_up_gemm"]}
+    gu_s, dn_s = m.kernel_us["gate_up_gemm"] * 1e-6, m.kernel_us["down_gemm"] * 1e-6
+    gu_bytes = gemm_bytes(wl, wl.dtype, m.G, m.N, "gateup")
+    dn_bytes = gemm_bytes(wl, wl.dtype, m.G, m.N, "down")
     mfma = {
-        "gate_up_tflops": gemm_flops(wl, N, "gateup") / gu_s / 1e12,
-        "down_tflops": gemm_flops(wl, N, "down") / dn_s / 1e12,
+        "gate_up_tflops": gemm_flops(wl, m.N, "gateup") / gu_s / 1e12,
+        "down_tflops": gemm_flops(wl, m.N, "down") / dn_s / 1e12,
+        "stage2_tflops": (gemm_flops(wl, m.N, "gateup") + gemm_flops(wl, m.N, "down")) / (gu_s + dn_s) / 1e12,
         "peak_tflops": MFMA_PEAK_TFLOPS[wl.dtype],
     }
+    shape_name = "dsv3" if wl.H == 7168 else "qwen3"
     out = {
         "metric": "per-GPU MoE block us/batch",
-        "value": ms_per_step * 1e3,
+        "value": m.ms_per_step * 1e3,
         "unit": "us/batch",
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": m.ms_per_step,
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
@@ -293,23 +341,30 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": args.workload,
-            "description": synth.describe(args.workload, plan_name),
-            "m_tile": args.m_tile,
-            "plan": plan_name,
-            "G": G, "N": N, "tiles": tiles,
-            "weight_copies_rotated": copies,
+            "description": synth.describe(args.workload, m.plan_name),
+            "m_tile": m.m_tile,
+            "plan": m.plan_name,
+            "G": m.G, "N": m.N, "tiles": m.tiles,
+            "weight_copies_rotated": m.copies,
         },
-        "roofline": roof,
-        "stages_us": stage_us,
-        "kernels_us": kernel_us,
-        "eager_ms_per_step": eager_ms,
+        "roofline": roofline(m),
+        "stages_us": m.stage_us,
+        "kernels_us": m.kernel_us,
+        "eager_ms_per_step": m.eager_ms,
         "attainable_copy_gbs": copy_gbs,
         "stage2_hbm_gbs": (gu_bytes + dn_bytes) / (gu_s + dn_s) / 1e9,
         "mfma": mfma,
+        "fit": measure.committed_fit(shape_name, wl.dtype, m.m_tile),
     }
+    if not args.no_flat and args.flat_workload != args.workload:
+        f = measure_workload(torch, args.flat_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
+        out["roofline_flat"] = {**roofline(f), "workload": args.flat_workload, "m_tile": f.m_tile,
+                                "block_us": f.ms_per_step * 1e3, "stages_us": f.stage_us,
+                                "fit": measure.committed_fit(shape_name, f.wl.dtype, f.m_tile)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
-        out["cpu_baseline"] = cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, args.m_tile, args.cpu_budget_s)
+        out["cpu_baseline"] = cpu_baseline(wl, m.plan, m.x, m.xs, m.w13, m.s13, m.w2, m.s2, m.m_tile,
+                                           args.cpu_budget_s)
     print(json.dumps(out), flush=True)
     return 0
 

@@ -236,9 +236,13 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
  * Stage 2 (Sec. 2.1 "gate/up, activation, down"; Sec. 2.2 weight streaming).
  * For every slot with c_s > 0: h = silu(x_perm W_gate^T) * (x_perm W_up^T)
  * with silu(z) = z / (1 + e^-z), then y_perm = h W2^T.  Slots with c_s = 0
- * read no weights.  Reads slot_counts / slot_offsets / x_perm (and
- * x_perm_scale) of a stage-1 result from device memory, so no host round
- * trip is needed.  y_perm [row_cap, H] bf16 device: real rows written,
+ * read no weights.  Reads slot_counts, slot_offsets, row_token and x_perm
+ * (and x_perm_scale) of a stage-1 result from device memory, so no host
+ * round trip is needed; expert_counts and pair_row may be NULL.  The number
+ * of M-tiles comes from slot_offsets[S] / m_tile (capped at row_cap /
+ * m_tile), so the workspace need not be the one stage 1 used: any
+ * workspace of tempo_moe_query's size serves.
+ * y_perm [row_cap, H] bf16 device: real rows written,
  * padding rows not.  Accumulation is fp32; h is rounded to bf16 (bf16 path)
  * or quantised to e4m3 with 1 x 128 fp32 scales amax/448, round to nearest
  * even, saturating at 448 (fp8 path; the fp8 contraction applies the

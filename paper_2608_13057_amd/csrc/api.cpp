@@ -94,8 +94,8 @@ static int check_plan(const tempo_plan* p) {
 }
 
 static int check_disp(const tempo_moe_shape* s, const tempo_dispatch_out* d, bool need_index_outputs) {
-  if (!d || !d->slot_counts || !d->slot_offsets || !d->x_perm) return TEMPO_EINVAL;
-  if (need_index_outputs && (!d->expert_counts || !d->row_token || !d->pair_row)) return TEMPO_EINVAL;
+  if (!d || !d->slot_counts || !d->slot_offsets || !d->row_token || !d->x_perm) return TEMPO_EINVAL;
+  if (need_index_outputs && (!d->expert_counts || !d->pair_row)) return TEMPO_EINVAL;
   if (s->dtype != TEMPO_BF16 && !d->x_perm_scale) return TEMPO_EINVAL;
   return TEMPO_OK;
 }

@@ -21,7 +21,6 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   a.slot_offsets = d.slot_offsets;
   a.S = s.S;
   a.max_tiles = L.row_cap / BM;
-  a.hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
   a.t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   a.t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   a.timing = timing ? 1 : 0;

@@ -64,10 +64,10 @@ __host__ __device__ constexpr size_t packed_tile_bytes(int K) { return (size_t)B
 // 32b + (l & 31), chunk 2w + (l >> 5), and the stores fill 1 KB each.
 __global__ __launch_bounds__(256) void k_pack_rows(const char* __restrict__ A, int gather,
                                                    const int32_t* __restrict__ row_token,
-                                                   const uint32_t* __restrict__ hdr, int max_tiles, int K,
-                                                   char* __restrict__ out) {
+                                                   const int32_t* __restrict__ slot_offsets, int S, int max_tiles,
+                                                   int K, char* __restrict__ out) {
   const int KT = K / 64;
-  const int blocks = min((int)hdr[kHdrTiles], max_tiles) * KT;
+  const int blocks = max(0, min(slot_offsets[S] / BIG_M, max_tiles)) * KT;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const size_t row_bytes = (size_t)K * 2;
 #pragma unroll 1
@@ -96,7 +96,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
   constexpr int wm = WV & 1, wn = WV >> 1;           // this wavefront's 128-row and 128-weight-row halves
   const int lane = threadIdx.x & 63;
 
-  const int NT = __builtin_amdgcn_readfirstlane(min((int)p.hdr[kHdrTiles], p.max_tiles));
+  const int NT = __builtin_amdgcn_readfirstlane(max(0, min(s_off[p.S] / BIG_M, p.max_tiles)));
   const int KT = p.Kd / 64;        // steps of 64 bf16
   const int NU = 4 * KT;           // sub-steps per item
   const int NBT = p.Nout / NCOLS;  // items per M-tile
@@ -360,19 +360,17 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
                               const hipEvent_t* ev, hipStream_t st) {
   const int grid = persistent_grid(1);
   const int max_tiles = L.row_cap / BIG_M;
-  const uint32_t* hdr = reinterpret_cast<const uint32_t*>(ws + L.header);
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
 
   const char* src = static_cast<const char*>(x_rows ? x_rows : d.x_perm);
   hipLaunchKernelGGL(k_pack_rows, dim3(persistent_grid(4)), dim3(256), 0, st, src, x_rows ? 1 : 0,
-                     d.row_token, hdr, max_tiles, s.H, ws + L.apack);
+                     d.row_token, d.slot_offsets, s.S, max_tiles, s.H, ws + L.apack);
 
   GemmArgs a{};
   a.slot_counts = d.slot_counts;
   a.slot_offsets = d.slot_offsets;
   a.S = s.S;
   a.max_tiles = max_tiles;
-  a.hdr = hdr;
   a.t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
   a.t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   a.timing = timing ? 1 : 0;

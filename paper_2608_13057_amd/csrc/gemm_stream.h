@@ -98,7 +98,6 @@ struct GemmArgs {
   const int32_t* slot_counts;
   const int32_t* slot_offsets;
   int S, Kd, Nout, max_tiles;
-  const uint32_t* hdr;
   uint64_t* t0;
   uint64_t* t1;
   int timing;
@@ -286,14 +285,14 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
-  // the independent loads of the set-up first, together
-  const int nt_hdr = (int)p.hdr[kHdrTiles];
   for (int s = tid; s <= p.S; s += GEMM_THREADS) s_off[s] = p.slot_offsets[s];
   for (int s = tid; s < p.S; s += GEMM_THREADS) s_cnt[s] = p.slot_counts[s];
   __syncthreads();
   build_slot_weights<BM>(s_off, s_cnt, s_sw, p.S);
 
-  const int NT = __builtin_amdgcn_readfirstlane(min(nt_hdr, p.max_tiles));
+  // M-tiles in use, from the stage-1 offsets themselves (every P_s is a
+  // multiple of BM), bounded by what the row buffers hold
+  const int NT = __builtin_amdgcn_readfirstlane(max(0, min(s_off[p.S] / BM, p.max_tiles)));
   const Geo g = make_geo<BM>(p.Kd / BK, p.Nout / NCOLS, NT, blockIdx.x, gridDim.x, s_off, s_cnt, s_sw, p.S);
   if (g.q0 >= g.q1) {  // uniform: the whole workgroup leaves
     if (tid == 0) p.fix[(size_t)blockIdx.x * FIX_WORDS] = -1;

@@ -57,8 +57,54 @@ def auto_m_tile(wl) -> int:
     return 256
 
 
+def uses_big_kernel(dtype: str, m_tile: int, H: int) -> bool:
+    """Whether stage 2 runs the 256 x 256-item large-tile GEMM (bf16 with
+    256-row tiles and H a multiple of 256) rather than the stream-K one."""
+    return dtype == "bf16" and m_tile == 256 and H % 256 == 0
+
+
+def gateup_kernel_name(dtype: str, m_tile: int, H: int) -> str:
+    """Symbol (as rocprofv3 prints it) of the gate/up GEMM kernel a forward
+    launches."""
+    if uses_big_kernel(dtype, m_tile, H):
+        return "tempo::(anonymous namespace)::k_gemm_big<true>"
+    fp8 = "false" if dtype == "bf16" else "true"
+    mx = "true" if dtype == "fp8mx" else "false"
+    return f"tempo::gemm::k_gemm<{fp8}, {m_tile}, true, {mx}>"
+
+
 def traffic_path(workload: str, m_tile: int) -> str:
     return os.path.join(ROOT, "profiles", f"k_gemm_gateup_{workload}_m{m_tile}_traffic.md")
+
+
+def fit_path(shape: str, dtype: str, m_tile: int) -> str:
+    return os.path.join(ROOT, "profiles", f"stage4_{shape}_{dtype}_m{m_tile}.md")
+
+
+def committed_fit(shape: str, dtype: str, m_tile: int, scope: str = "gemm"):
+    """The Eq. 1 fit (a, b, c, beta, n*) of a committed stage-4 profile for
+    one scope, or None: from its `fit_json:` line, else from the Eq. 1 row of
+    the scope's table."""
+    path = fit_path(shape, dtype, m_tile)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        text = fh.read()
+    for line in text.splitlines():
+        if line.startswith("fit_json: "):
+            d = json.loads(line[len("fit_json: "):])
+            if d.get("scope") == scope:
+                return d
+    sec = text.split(f"scope `{scope}`", 1)
+    if len(sec) < 2:
+        return None
+    for line in sec[1].splitlines():
+        if line.startswith("| Eq. 1 |"):
+            c = [x.strip() for x in line.strip("|").split("|")]
+            return {"scope": scope, "model": "Eq. 1", "a": float(c[1]), "b": float(c[2]), "c": float(c[3]),
+                    "beta": float(c[4]), "n_star": float(c[6]), "err_mean": float(c[7]), "err_max": float(c[8]),
+                    "source": os.path.relpath(path, ROOT)}
+    return None
 
 
 def committed_traffic(workload: str, m_tile: int):
@@ -130,7 +176,10 @@ def _mean_counter(rows, counter: str, match):
 
 
 def _is_gateup(name: str) -> bool:
-    """The stream-K GEMM instance with GATEUP (its third template argument)."""
+    """The gate/up GEMM: the large-tile kernel k_gemm_big<true>, or the
+    stream-K instance with GATEUP (its third template argument)."""
+    if "k_gemm_big<true>" in name.replace(" ", ""):
+        return True
     if "k_gemm<" not in name:
         return False
     args = name.replace(" ", "").split("k_gemm<", 1)[1].split(">", 1)[0].split(",")

@@ -208,8 +208,7 @@ def _check_disp(shape, d, row_cap):
     _need(d.x_perm, shape.elem, (row_cap, shape.H), "x_perm")
     if d.expert_counts is not None:
         _need(d.expert_counts, torch.int32, (shape.E,), "expert_counts")
-    if d.row_token is not None:
-        _need(d.row_token, torch.int32, (row_cap,), "row_token")
+    _need(d.row_token, torch.int32, (row_cap,), "row_token")
     if d.pair_row is not None:
         _need(d.pair_row, torch.int32, (shape.T, shape.K), "pair_row")
     if shape.dtype != "bf16":

@@ -83,3 +83,35 @@ def rel_err_rows(y: np.ndarray, ref: np.ndarray, rows: np.ndarray) -> float:
     d = np.abs(y[rows] - ref[rows]).max(axis=1)
     n = np.abs(ref[rows]).max(axis=1)
     return float(np.max(d / np.maximum(n, 1e-30)))
+
+
+def tile_sample(d: dict, m_tile: int, rng) -> np.ndarray:
+    """Tokens of a stage-1 result stratified by M-tile: for every activated
+    slot, one random real row of each of its M-tiles and its last real row;
+    returns the sorted distinct tokens of those rows."""
+    so, sc, rt = d["slot_offsets"], d["slot_counts"], d["row_token"]
+    toks = set()
+    for s in range(len(sc)):
+        c = int(sc[s])
+        for lo in range(0, c, m_tile):
+            toks.add(int(rt[so[s] + rng.integers(lo, min(c, lo + m_tile))]))
+        if c > 0:
+            toks.add(int(rt[so[s] + c - 1]))
+    return np.array(sorted(toks), np.int64)
+
+
+def bf16_ulp(v: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 values at |v| (8 significant bits); 2^-133 at 0."""
+    a = np.abs(v)
+    e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    return np.where(a > 0, 2.0 ** (e - 7), 2.0 ** -133)
+
+
+def mirror_stats(got: np.ndarray, ref: np.ndarray) -> str:
+    """Element-wise agreement with a reference that rounds where the GPU
+    rounds: the share of elements that are identical and the largest
+    difference in bf16 ulps of the reference element."""
+    diff = np.abs(got - ref)
+    same = float(np.mean(diff == 0))
+    ulps = float(np.max(diff / bf16_ulp(ref))) if diff.size else 0.0
+    return f"identical={same:.4f} max_ulps={ulps:.1f}"

@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
-from helpers import Case, bf16_to_f64, rel_err_rows, to_dev, to_host
+from helpers import Case, bf16_to_f64, mirror_stats, rel_err_rows, tile_sample, to_dev, to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -41,10 +41,14 @@ def _local_rows(d_ref, T_valid):
     return np.nonzero(has)[0], np.nonzero(~has)[0]
 
 
+@pytest.mark.parametrize("fresh_ws", [False, True])
 @pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8", "tiny_fp8mx"])
-def test_experts_stage_tiny(m_tile, name):
-    """Stage 2 alone: y_perm real rows against the oracle's per-row FFN."""
+def test_experts_stage_tiny(m_tile, name, fresh_ws):
+    """Stage 2 alone: y_perm real rows against the oracle's per-row FFN.
+    fresh_ws: stage 2 runs on a second, never-used workspace (it takes the
+    tile count from slot_offsets, not from anything stage 1 left in the
+    workspace)."""
     import torch
     from paper_2608_13057_amd import moe, synth
 
@@ -52,7 +56,7 @@ def test_experts_stage_tiny(m_tile, name):
     c = Case(wl, "uniform", m_tile)
     moe.dispatch(c.shape, c.d_plan, c.d_ids, c.d_x, c.d_xs, c.disp, c.ws)
     y_perm = torch.empty(c.ws.row_cap, wl.H, dtype=torch.int16, device="cuda")
-    moe.experts(c.shape, c.disp, c.d_weights, y_perm, c.ws)
+    moe.experts(c.shape, c.disp, c.d_weights, y_perm, moe.Workspace(c.shape) if fresh_ws else c.ws)
     torch.cuda.synchronize()
     d = c.oracle_dispatch()
     rt = d["row_token"]
@@ -62,7 +66,7 @@ def test_experts_stage_tiny(m_tile, name):
     for mode, tol in (("exact", TOL_EXACT[wl.dtype]), ("mirror", TOL_MIRROR[wl.dtype])):
         ref = oracle.ffn_rows(c.x, rt[real], slot, c.w13, c.w2, wl.dtype, mode, c.xs, c.s13, c.s2)
         err = rel_err_rows(got, ref, np.arange(len(real)))
-        print(f"[experts {name} M={m_tile}] {mode} err={err:.2e}")
+        print(f"[experts {name} M={m_tile}] {mode} err={err:.2e} {mirror_stats(got, ref)}")
         assert err <= tol
 
 
@@ -104,7 +108,7 @@ def test_forward_tiny(m_tile, name):
     for mode in ("exact", "mirror"):
         ref = _oracle_y(c, d, mode)
         err = rel_err_rows(got, ref, loc)
-        print(f"[forward {name} M={m_tile}] {mode} err={err:.2e}")
+        print(f"[forward {name} M={m_tile}] {mode} err={err:.2e} {mirror_stats(got[loc], ref[loc])}")
         assert err <= (TOL_EXACT if mode == "exact" else TOL_MIRROR)[wl.dtype]
     assert np.all(y[none] == 0)
     sc = d["slot_counts"]
@@ -181,6 +185,41 @@ def test_forward_full_size_sampled(name, plan, m_tile):
     print(f"[forward {name}] sampled {len(pick)} tokens err={err:.2e}")
     assert err <= TOL_EXACT[wl.dtype]
     assert np.all(y[none] == 0)
+    assert np.all((st > 0) == (d["slot_counts"] > 0))
+
+
+@pytest.mark.parametrize("name,m_tile", [("qwen3_prefill_bf16", 256), ("qwen3_prefill_fp8", 128),
+                                         ("qwen3_prefill_fp8mx", 128), ("qwen3_prefill_fp8", 256),
+                                         ("qwen3_prefill_bf16", 128)])
+def test_forward_prefill_tile_sampled(name, m_tile):
+    """The prefill share (8192 tokens, top-8 of 128, 18 slots) at full size:
+    stage 1 bit-exact inside the forward, and y on a token sample stratified
+    by M-tile -- one random row of every M-tile of every activated slot (the
+    second and later tiles of multi-tile slots included) plus each slot's
+    last real row (its ragged tail) -- against the fp64 oracle; tokens with
+    no local pair exactly zero."""
+    from paper_2608_13057_amd import synth
+
+    wl = synth.make_workload(name)
+    c = Case(wl, "uniform", m_tile)
+    print(f"[prefill {name} M={m_tile}] running", flush=True)
+    y, st = _run_forward(c, timing=True)
+    d = c.oracle_dispatch()
+    assert np.array_equal(to_host(c.disp.slot_counts), d["slot_counts"])
+    assert np.array_equal(to_host(c.disp.slot_offsets), d["slot_offsets"])
+    assert np.array_equal(to_host(c.disp.pair_row), d["pair_row"])
+    assert np.array_equal(to_host(c.disp.row_token)[: d["slot_offsets"][-1]], d["row_token"])
+    loc, none = _local_rows(d, c.T_valid)
+    assert np.all(y[none] == 0)
+    pick = tile_sample(d, m_tile, np.random.default_rng(1))
+    ntiles = int(sum(-(-int(n) // m_tile) for n in d["slot_counts"]))
+    assert int((d["slot_counts"] > m_tile).sum()) >= 2  # slots spanning several tiles are covered
+    sel = np.zeros(wl.T, np.uint8)
+    sel[pick] = 1
+    ref = _oracle_y(c, d, "exact", sel)
+    err = rel_err_rows(bf16_to_f64(y), ref, pick)
+    print(f"[prefill {name} M={m_tile}] {ntiles} tiles, sampled {len(pick)} tokens err={err:.2e}")
+    assert err <= TOL_EXACT[wl.dtype]
     assert np.all((st > 0) == (d["slot_counts"] > 0))
 
 

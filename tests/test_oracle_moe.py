@@ -197,3 +197,71 @@ def test_mirror_mode_pow2_h_quantisation():
     ym8 = oracle.moe(x, w, ps, w13, w2, "fp8", "mirror", xs, s13, s2)
     assert not np.array_equal(ym, ym8)
     assert 0 < np.max(np.abs(ym - ye)) / np.max(np.abs(ye)) < 0.1
+
+
+# ---- stage 3 alone: oracle.combine (Sec. 2.1, routing-weighted combine) ----
+
+def _combine_problem(T=37, K=5, H=128, R=120, T_valid=31, seed=11):
+    rng = np.random.default_rng(seed)
+    yp = synth.to_bf16_bits(rng.standard_normal((R, H)).astype(np.float32))
+    pr = rng.integers(-1, R, size=(T, K)).astype(np.int32)
+    w = rng.random((T, K)).astype(np.float32)
+    return pr, w, yp, T_valid
+
+
+def test_combine_matches_gathered_einsum():
+    """y = sum_k w[t,k] * Y_perm[pair_row[t,k]] over pairs with a row, for
+    t < T_valid, as one numpy gather + einsum over a 0/1 mask (torch's bf16
+    decoding for the rows): an independent vectorised statement of the same
+    definition."""
+    pr, w, yp, Tv = _combine_problem()
+    rows = torch.from_numpy(yp.view(np.int16)).view(torch.bfloat16).double().numpy()
+    mask = (pr >= 0).astype(np.float64)
+    mask[Tv:] = 0.0
+    g = rows[np.maximum(pr, 0)]  # [T, K, H]
+    ref = np.einsum("tk,tk,tkh->th", w.astype(np.float64), mask, g)
+    got = oracle.combine(pr, w, yp, Tv)
+    assert np.allclose(got, ref, rtol=1e-13, atol=1e-13)
+    assert np.all(got[Tv:] == 0)
+
+
+def test_combine_one_hot_is_row_copy():
+    """K = 1, w = 1: each token's output is exactly its row's bf16 value
+    (a permutation of the rows); a token whose pair has no row is zero."""
+    rng = np.random.default_rng(3)
+    T, H = 50, 256
+    yp = synth.to_bf16_bits(rng.standard_normal((T, H)).astype(np.float32))
+    perm = rng.permutation(T).astype(np.int32)
+    pr = perm.reshape(T, 1).copy()
+    pr[7, 0] = -1
+    got = oracle.combine(pr, np.ones((T, 1), np.float32), yp, T)
+    vals = synth.bf16_bits_to_f32(yp).astype(np.float64)
+    for t in range(T):
+        if t == 7:
+            assert np.all(got[t] == 0)
+        else:
+            assert np.array_equal(got[t], vals[perm[t]])
+
+
+def test_combine_linear_and_order_free():
+    """Linear in the routing weights (scaling w by a power of two scales y
+    exactly), and permuting a token's k-columns together with their rows
+    leaves y unchanged up to fp64 summation order."""
+    pr, w, yp, Tv = _combine_problem(seed=12)
+    y1 = oracle.combine(pr, w, yp, Tv)
+    y2 = oracle.combine(pr, (w * 4.0).astype(np.float32), yp, Tv)
+    assert np.array_equal(y2, 4.0 * y1)
+    perm = np.random.default_rng(0).permutation(pr.shape[1])
+    y3 = oracle.combine(pr[:, perm], w[:, perm], yp, Tv)
+    assert np.allclose(y3, y1, rtol=1e-14, atol=1e-14)
+
+
+def test_combine_hand_worked():
+    """Two tokens, K = 2, rows of exactly representable values."""
+    vals = np.array([[1.0, -2.0], [0.5, 4.0], [3.0, 0.25]], np.float32)
+    yp = synth.to_bf16_bits(vals)
+    pr = np.array([[2, 0], [-1, 1]], np.int32)
+    w = np.array([[0.5, 0.25], [0.75, 2.0]], np.float32)
+    got = oracle.combine(pr, w, yp, 2)
+    assert np.array_equal(got, np.array([[0.5 * 3.0 + 0.25 * 1.0, 0.5 * 0.25 + 0.25 * -2.0], [1.0, 8.0]]))
+    assert np.all(oracle.combine(pr, w, yp, 1)[1] == 0)  # the second token is graph padding
