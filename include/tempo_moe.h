@@ -288,6 +288,32 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
                       void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * tempo_moe_forward with the library's own static scratch array as the
+ * workspace, so the call takes no workspace argument and allocates nothing.
+ * Arguments, outputs and errors are those of tempo_moe_forward, except:
+ *   - the shape's workspace (tempo_moe_query) must fit in
+ *     TEMPO_STATIC_SCRATCH_BYTES, else TEMPO_EWORKSPACE is returned before
+ *     anything is enqueued (decode-sized shapes fit: e.g. 18 slots of
+ *     H 4096 / I 1536 with 512 tokens, top-8, m_tile 64);
+ *   - every GPU holds one copy of the array from the first call on it until
+ *     the process ends, and every call on that GPU uses it: calls that
+ *     overlap on one GPU (concurrent streams, or a second call enqueued
+ *     before the first has run on another stream) race on it, so serialise
+ *     them on one stream;
+ *   - the array keeps the last call's contents; nothing in it needs to start
+ *     at zero, and the sticky device error word it holds cannot be read
+ *     (data errors are still handled: offending pairs are dropped).
+ * TEMPO_EDEVICE if the array's device address cannot be looked up.
+ */
+#define TEMPO_STATIC_SCRATCH_BYTES (128u << 20)
+int tempo_moe_forward_static(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
+                             const float* topk_w, const void* x, const float* x_scale,
+                             const tempo_expert_weights* weights, const tempo_dispatch_out* disp, void* y,
+                             uint64_t* slot_time_ns, void* const* stage_events, void* stream);
+
+/*
  * Synchronises `stream`, returns the sticky device error word (OR of the
  * TEMPO_DERR_* bits seen by every dispatch since the last read) in *bits and
  * clears it.  Returns TEMPO_EDEVICE if the synchronisation fails.

@@ -25,8 +25,10 @@ TEMPO_BF16 = 0
 TEMPO_FP8_E4M3 = 1
 TEMPO_FP8_E4M3_UE8M0 = 2
 
+TEMPO_STATIC_SCRATCH_BYTES = 128 << 20
+
 SYMBOLS = ("tempo_moe_query", "tempo_moe_pack_weights", "tempo_moe_dispatch", "tempo_moe_experts", "tempo_moe_combine",
-           "tempo_moe_forward", "tempo_moe_device_error", "tempo_moe_strerror")
+           "tempo_moe_forward", "tempo_moe_forward_static", "tempo_moe_device_error", "tempo_moe_strerror")
 
 _P = ctypes.c_void_p
 
@@ -75,6 +77,8 @@ def load() -> ctypes.CDLL:
     lib.tempo_moe_combine.argtypes = [SP, _P, _P, _P, _P, _P]
     lib.tempo_moe_forward.argtypes = [SP, ctypes.POINTER(Plan), _P, _P, _P, _P, ctypes.POINTER(ExpertWeights),
                                       ctypes.POINTER(DispatchOut), _P, _P, _P, _P, ctypes.c_size_t, _P]
+    lib.tempo_moe_forward_static.argtypes = [SP, ctypes.POINTER(Plan), _P, _P, _P, _P, ctypes.POINTER(ExpertWeights),
+                                             ctypes.POINTER(DispatchOut), _P, _P, _P, _P]
     lib.tempo_moe_device_error.argtypes = [_P, _P, ctypes.POINTER(ctypes.c_uint32)]
     lib.tempo_moe_strerror.argtypes = [ctypes.c_int]
     lib.tempo_moe_strerror.restype = ctypes.c_char_p

@@ -287,6 +287,29 @@ def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, we
     return y
 
 
+def forward_static(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, weights: WeightTensors,
+                   disp: DispatchBuffers, y, slot_time_ns=None, stream=None):
+    """tempo_moe_forward_static: forward() on the library's static scratch
+    array instead of a workspace (allocates nothing; the shape's workspace
+    must fit in TEMPO_STATIC_SCRATCH_BYTES).  Calls that overlap on one GPU
+    race on the array."""
+    _check_inputs(shape, topk_ids, x, x_scale)
+    _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
+    _check_plan(shape, plan)
+    _check_weights(shape, weights, packed=True)
+    _, row_cap = query(shape)
+    _check_disp(shape, disp, row_cap)
+    _need(y, torch.int16, (shape.T, shape.H), "y")
+    if slot_time_ns is not None:
+        _need(slot_time_ns, torch.int64, (shape.S,), "slot_time_ns")
+    sh, pl, w, do = shape.c(), plan.c(), weights.c(), disp.c()
+    check(_lib.load().tempo_moe_forward_static(ctypes.byref(sh), ctypes.byref(pl), _ptr(topk_ids), _ptr(topk_w),
+                                               _ptr(x), _ptr(x_scale), ctypes.byref(w), ctypes.byref(do), _ptr(y),
+                                               _ptr(slot_time_ns), None, _stream(stream)),
+          "tempo_moe_forward_static")
+    return y
+
+
 class PreparedForward:
     """A validated tempo_moe_forward call whose ctypes arguments are built
     once; calling it re-issues the same launch sequence on the current (or a

@@ -73,3 +73,20 @@ def test_struct_layouts_match_the_header(tmp_path):
         assert got[(cname, "size")] == ctypes.sizeof(py), cname
         for f, _ in py._fields_:
             assert got[(cname, f)] == getattr(py, f).offset, (cname, f)
+
+
+def test_static_forward_refuses_shapes_beyond_its_scratch():
+    """tempo_moe_forward_static checks the shape's workspace against
+    TEMPO_STATIC_SCRATCH_BYTES before touching the device (so this runs
+    without a GPU): the prefill share does not fit, and a bad shape is
+    EINVAL."""
+    lib = _lib.load()
+    big = moe.MoEShape(T=8192, K=8, E=128, S=18, H=4096, I=1536, m_tile=256).c()
+    assert moe.query(moe.MoEShape(T=8192, K=8, E=128, S=18, H=4096, I=1536, m_tile=256))[0] > \
+        _lib.TEMPO_STATIC_SCRATCH_BYTES
+    args = [None] * 11
+    assert lib.tempo_moe_forward_static(ctypes.byref(big), *args) == _lib.TEMPO_EWORKSPACE
+    bad = moe.MoEShape(T=8, K=2, E=4, S=2, H=256, I=256, m_tile=96).c()
+    assert lib.tempo_moe_forward_static(ctypes.byref(bad), *args) == _lib.TEMPO_EINVAL
+    small = moe.MoEShape(T=512, K=8, E=128, S=18, H=4096, I=1536, m_tile=64)
+    assert moe.query(small)[0] <= _lib.TEMPO_STATIC_SCRATCH_BYTES
