@@ -281,12 +281,12 @@ def roofline(m):
 
     wl = m.wl
     gu_s = m.kernel_us["gate_up_gemm"] * 1e-6
-    kernel = measure.gateup_kernel_name(wl.dtype, m.m_tile, wl.H)
+    kernel = measure.gateup_kernel_name(wl.dtype, m.m_tile, wl.H, wl.I)
     traffic, traffic_current = measure.committed_traffic(m.name, m.m_tile)
     common = {"traffic": traffic if traffic_current else None, "kernel": kernel + " (gate/up)",
               "launch_us": m.kernel_us["gate_up_gemm"], "G": m.G, "N": m.N}
     # pairs per activated slot against the ideal balance point e P / (2 BW) ~ 312
-    linear = measure.uses_big_kernel(wl.dtype, m.m_tile, wl.H) or m.N / max(1, m.G) > 312
+    linear = measure.uses_big_kernel(wl.dtype, m.m_tile, wl.H, wl.I) or m.N / max(1, m.G) > 312
     if linear:
         fl = gemm_flops(wl, m.N, "gateup")
         peak = MFMA_PEAK_TFLOPS[wl.dtype]

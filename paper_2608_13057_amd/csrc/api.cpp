@@ -4,6 +4,7 @@
 // memory or synchronises, except tempo_moe_device_error.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <cstring>
 
@@ -46,7 +47,7 @@ Layout make_layout(const tempo_moe_shape& s) {
   L.y_perm = o;
   o = align_up(o + (size_t)L.row_cap * s.H * 2);
   L.apack = o;
-  o = align_up(o + experts_big_pack_bytes(s, L.row_cap));
+  o = align_up(o + std::max(experts_big_pack_bytes(s, L.row_cap), experts_big_f8_pack_bytes(s, L.row_cap)));
   // stage-2 partial tiles: per workgroup of the persistent grid, 8 tiles of
   // m_tile x 128 fp32 (the running sum and the chunks of split work items)
   L.part = o;

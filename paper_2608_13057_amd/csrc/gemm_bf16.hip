@@ -58,7 +58,8 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
 }  // namespace
 
 bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L) {
-  if (experts_big_supported(s)) return true;  // the large-tile kernel packs the token rows itself
+  // the large-tile kernels pack the token rows themselves
+  if (experts_big_supported(s) || experts_big_f8_supported(s)) return true;
   // upper bound of the M-tiles one workgroup range of the gate/up GEMM spans
   const int grid = persistent_grid(1);
   const int NB = s.I / 64;

@@ -1,0 +1,521 @@
+// Stage 2, fp8 e4m3 with power-of-two (UE8M0) block scales, for 256-row
+// M-tiles: the linear regime of the cost model (Sec. 2.2: many rows per slot,
+// the per-token compute beta dominates), where the expert FFN is a dense fp8
+// contraction.  Same organisation as the bf16 large-tile kernel
+// (gemm_big_agpr.hip), with the fp8 MFMA v_mfma_scale_f32_32x32x64_f8f6f4,
+// which applies the activation and weight block scales itself: each lane
+// hands it the UE8M0 exponent of the token row and of the weight row whose
+// 32 contraction elements it supplies, so the products accumulate straight
+// into the running sums.
+//
+// * Operands packed in MFMA operand order: the weights by
+//   tempo_moe_pack_weights (fp8 layout), the activation rows of each 256-row
+//   tile by k_pack_rows_f8 below, and the gate/up result h -- re-quantised to
+//   e4m3 in the gate/up epilogue -- in the layout the down GEMM reads.  The
+//   activation layout mirrors the weights': per 128-byte contraction step a
+//   tile is 32 KB, rows 32b..32b+31 form the 4 KB piece b, stored as four 1 KB
+//   loads j in which lane l holds the 16-byte chunk c(j, l) =
+//   4 (j >> 1) + 2 (l >> 5) + (j & 1) of row 32b + (l & 31).  Loads 2h and
+//   2h + 1 of a piece are one MFMA operand (the 32 bytes of a lane) for the
+//   64 contraction elements 64h .. 64h + 63 of the step: a sub-step.
+// * Per tile and step, the 256 activation-row scale exponents (UE8M0 bytes)
+//   sit at byte 8 (r & 31) + (r >> 5) of a 256-byte block, so a lane reads the
+//   exponents of its four row blocks as one word.
+// * A work item is (256-row M-tile, 256 packed weight rows); four wavefronts
+//   in a 2 x 2 arrangement each own 128 x 128 of it as 4 x 4 MFMA tiles of
+//   32 x 32 with the accumulators in AGPRs; the MFMAs take the weights as
+//   their first operand (a lane owns one token row and runs of four output
+//   columns).  Items are never split and accumulate their sub-steps in
+//   order, so a row's result depends only on its own inputs.
+// * The operands of a sub-step (16 KB of activations, 16 KB of weights, and
+//   the step's scale exponents) stream through an LDS ring of NSS slots by
+//   DMA; one barrier per sub-step, the fragment reads of sub-step u + 1 and
+//   the DMA of sub-step u + NSS - 1 interleaved with the MFMAs of sub-step u.
+// * gate/up epilogue: SwiGLU of the accumulators, the amax of each row over
+//   the item's 128 h columns (one contraction step of the down GEMM; the two
+//   wavefronts holding a row's halves combine theirs through LDS), the
+//   smallest power-of-two scale >= amax / 448, and e4m3 codes (round to
+//   nearest even, saturating) written in the packed layout with their
+//   exponents.  down epilogue: bf16 rows of y_perm.
+#include "gemm_stream.h"
+
+namespace tempo {
+namespace {
+
+using namespace gemm;
+
+constexpr int F8_M = 256;                       // rows per item (the M-tile)
+constexpr int F8_N = 256;                       // packed weight rows per item (two blocks of 128)
+constexpr int F8_STEP = 128;                    // contraction bytes of a step (one scale block)
+constexpr int F8_SUB = 16 * 1024;               // one 64-element sub-step of 256 rows
+constexpr int F8_SC = 2 * F8_SUB;               // offset of a slot's scale area
+constexpr int F8_SLOT = F8_SC + 512;            // activations, weights, then scale exponents
+constexpr int F8_NSS = 4;                       // ring slots
+constexpr int F8_DMA = 9;                       // DMA instructions per wavefront and sub-step
+constexpr int F8_GM = 4;                        // M-tiles per group of the item order
+
+// bytes of a packed 256-row tile of K-byte rows, and of its scale exponents
+__host__ __device__ constexpr size_t f8_tile_bytes(int K) { return (size_t)F8_M * K; }
+__host__ __device__ constexpr size_t f8_tile_scale_bytes(int K) { return (size_t)(K / F8_STEP) * 256; }
+
+// UE8M0 code of a power-of-two fp32 scale: its exponent byte
+__device__ __forceinline__ uint32_t ue8m0_of(float s) { return (__float_as_uint(s) >> 23) & 0xFFu; }
+
+// The activation rows of every live 256-row tile in the packed fp8 layout,
+// with their scale exponents, from token rows (gather: row r is token
+// row_token[r] of A) or from permuted rows (row r of A); the scales of row r
+// are A_scale[kt][row_cap] (block-major, as stage 1 writes them in both
+// cases); padding rows are zero with exponent 127 (scale 1).  One (tile, step) block per workgroup of a fixed
+// grid at a time: wavefront w writes pieces 2w and 2w + 1 (1 KB per store
+// instruction), thread t the exponent of row t.
+__global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict__ A, const float* __restrict__ A_scale,
+                                                      int gather, int row_cap, const int32_t* __restrict__ row_token,
+                                                      const int32_t* __restrict__ slot_offsets, int S, int max_tiles,
+                                                      int K, uint8_t* __restrict__ out, uint8_t* __restrict__ out_sc) {
+  const int KT = K / F8_STEP;
+  const int blocks = max(0, min(slot_offsets[S] / F8_M, max_tiles)) * KT;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+#pragma unroll 1
+  for (int blk = blockIdx.x; blk < blocks; blk += gridDim.x) {
+    const int tile = blk / KT, kt = blk - tile * KT;
+    uint8_t* dst = out + (size_t)tile * f8_tile_bytes(K) + (size_t)kt * (F8_M * F8_STEP);
+#pragma unroll
+    for (int pb = 0; pb < 2; pb++) {
+      const int b = 2 * w + pb;
+      const int row = tile * F8_M + 32 * b + (lane & 31);
+      const int tok = row_token[row];
+      const size_t src_row = (size_t)(gather ? tok : row) * K + kt * F8_STEP;
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const int c = 4 * (j >> 1) + 2 * (lane >> 5) + (j & 1);
+        i32x4 v = {0, 0, 0, 0};
+        if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + src_row + c * 16);
+        *reinterpret_cast<i32x4*>(dst + b * 4096 + j * 1024 + lane * 16) = v;
+      }
+    }
+    const int row = tile * F8_M + tid;
+    const int tok = row_token[row];
+    uint32_t e = 127;
+    if (tok >= 0) e = ue8m0_of(A_scale[(size_t)kt * row_cap + row]);
+    out_sc[(size_t)tile * f8_tile_scale_bytes(K) + (size_t)kt * 256 + (tid & 31) * 8 + (tid >> 5)] = (uint8_t)e;
+  }
+}
+
+struct F8Args {
+  const uint8_t* A;       // packed activation tiles
+  const uint8_t* A_sc;    // their scale exponents
+  const uint8_t* W;       // packed fp8 weights (tempo_moe_pack_weights)
+  size_t w_slot_bytes;
+  const float* Wsp;       // packed weight scales [slot][block][step][4] (powers of two)
+  size_t ws_slot_floats;
+  void* C;                // gate/up: packed h tiles; down: y_perm rows (bf16)
+  uint8_t* C_sc;          // gate/up: h scale exponents
+  const int32_t* slot_counts;
+  const int32_t* slot_offsets;
+  int S, Kd, Nout, max_tiles;
+  uint64_t* t0;
+  uint64_t* t1;
+  int timing;
+};
+
+// The GEMM of wavefront WV (0..3, uniform) of a workgroup.  (All four
+// issue their loads at the same points, so one code instance serves them.)
+template <bool GATEUP>
+__device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xamax, const int32_t* s_off,
+                                        const int32_t* s_cnt, const int WV) {
+  constexpr int NCOLS = GATEUP ? F8_N / 2 : F8_N;  // output columns per item
+  const int wm = WV & 1, wn = WV >> 1;             // this wavefront's 128-row and 128-weight-row halves
+  const int lane = threadIdx.x & 63;
+
+  const int NT = __builtin_amdgcn_readfirstlane(max(0, min(s_off[p.S] / F8_M, p.max_tiles)));
+  const int KT = p.Kd / F8_STEP;   // steps of 128 bytes
+  const int NU = 2 * KT;           // sub-steps per item
+  const int NBT = p.Nout / NCOLS;  // items per M-tile
+  const int items = NT * NBT;
+
+  // item order: as in the bf16 large-tile kernel (XCD-aware groups of F8_GM
+  // M-tiles, tile index fastest)
+  const int G = gridDim.x;
+  const int lin0 = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
+  const int my_items = lin0 < items ? (items - 1 - lin0) / G + 1 : 0;
+  if (my_items == 0) return;
+  auto item_of = [&](int n, int& tile, int& nbt) {
+    const int it = lin0 + n * G;
+    const int grp = it / (F8_GM * NBT), w_in = it - grp * (F8_GM * NBT);
+    const int gm = min(F8_GM, NT - grp * F8_GM);
+    nbt = w_in / gm;
+    tile = grp * F8_GM + (w_in - nbt * gm);
+  };
+
+  // DMA cursor: item ordinal dn, sub-step du; a_src / w_src point at this
+  // wavefront's first 1 KB load of the sub-step (activation loads 4 WV ..
+  // 4 WV + 3: pieces 2 WV and 2 WV + 1; weight loads 4 WV .. 4 WV + 3: pieces
+  // 2 (WV & 1), 2 (WV & 1) + 1 of weight block 2 nbt + (WV >> 1)); sc_src:
+  // this wavefront's scale load (WV 0: the tile's 256 exponents of the step;
+  // WV 1: the two weight blocks' packed scales, lanes 0 and 1; WV 2, 3: a
+  // 16-byte dummy so that every wavefront issues F8_DMA loads per sub-step).
+  // Past the last item the cursor re-loads the last item's sub-steps.
+  int dn = 0, du = 0;
+  const char* a_src = nullptr;
+  const char* w_src = nullptr;
+  const char* sc_src = nullptr;
+  auto dma_item = [&]() {
+    int tile, nbt;
+    item_of(dn, tile, nbt);
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * F8_M));
+    a_src = reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) + (2 * WV) * 4096;
+    w_src = reinterpret_cast<const char*>(p.W) + (size_t)slot * p.w_slot_bytes +
+            (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096;
+    if (WV == 1)
+      sc_src = reinterpret_cast<const char*>(p.Wsp + (size_t)slot * p.ws_slot_floats + (size_t)(2 * nbt) * KT * 4);
+    else
+      sc_src = reinterpret_cast<const char*>(p.A_sc) + (size_t)tile * f8_tile_scale_bytes(p.Kd);
+  };
+  const uint32_t ring_lds = lds_addr(ring);
+  const uint32_t lane16 = lane * 16;
+  // sub-step du of the cursor: step du >> 1, half du & 1
+  auto dma_piece = [&](uint32_t sl, int q) {
+    // q = 0..3 activation loads, 4..7 weight loads; each 1 KB
+    const int b = q & 3;  // load within this wavefront's share: piece (b >> 1), part (b & 1)
+    const char* src = (q < 4 ? a_src : w_src) + (b >> 1) * 4096 + (b & 1) * 1024;
+    lds_dma16s(src, lane16, sl + (q < 4 ? 0 : F8_SUB) + (4 * WV + b) * 1024);
+  };
+  auto dma_scales = [&](uint32_t sl) {
+    const int kt = du >> 1;
+    if (WV == 0) {
+      if (lane < 16) lds_dma16s(sc_src + kt * 256, lane16, sl + F8_SC);
+    } else if (WV == 1) {
+      if (lane < 2) lds_dma16s(sc_src + kt * 16, lane * (uint32_t)(KT * 16), sl + F8_SC + 256);
+    } else {
+      if (lane == 0) lds_dma16s(sc_src, 0, sl + F8_SC + 256 + 32 + 16 * (WV - 2));
+    }
+  };
+  auto dma_advance = [&]() {
+    // half 0 -> 1 within a step: +2 KB; half 1 -> the next step's half 0
+    const int st = (du & 1) ? F8_M * F8_STEP - 2048 : 2048;
+    const int sw = (du & 1) ? 128 * F8_STEP - 2048 : 2048;
+    a_src += st;
+    w_src += sw;
+    if (++du == NU) {
+      du = 0;
+      if (dn + 1 < my_items) ++dn;
+      dma_item();
+    }
+  };
+
+  f32x16 acc[4][4];
+  // Operand registers: the weight fragments of a sub-step are read during
+  // the previous one (fb[buf ^ 1]); the activation fragment of row block
+  // i + 1 during the MFMAs of row block i (fa[(i + 1) & 1]; for i = 3 that is
+  // row block 0 of the next sub-step), so 80 registers hold the operands.
+  i32x8 fa[2], fb[2][4];
+  int ea[2][4], eb[2];
+  auto rd8 = [&](const char* s) {
+    const i32x4 lo = *reinterpret_cast<const i32x4*>(s);
+    const i32x4 hi = *reinterpret_cast<const i32x4*>(s + 1024);
+    return (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  };
+  // activation row block i of ring slot `slot` (piece 4 wm + i)
+  auto frag_a = [&](int slot, int i) { return rd8(ring + slot * F8_SLOT + (4 * wm + i) * 2048 + lane * 16); };
+  // weight piece j of block wn
+  auto frag_b = [&](int slot, int buf, int j) {
+    fb[buf][j] = rd8(ring + slot * F8_SLOT + F8_SUB + (4 * wn + j) * 2048 + lane * 16);
+  };
+  // scale exponents of this lane's token rows (one word, byte i for row
+  // block i) and of its weight row (gate or up scale of block wn for
+  // gate/up)
+  auto frag_sc = [&](int slot, int buf) {
+    const char* s = ring + slot * F8_SLOT + F8_SC;
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(s + (lane & 31) * 8 + 4 * wm);
+#pragma unroll
+    for (int i = 0; i < 4; i++) ea[buf][i] = (int)((w >> (8 * i)) & 0xFFu);
+    const float* ws = reinterpret_cast<const float*>(s + 256 + 16 * wn);
+    eb[buf] = (int)ue8m0_of(GATEUP ? ws[((lane >> 4) & 1)] : ws[0]);
+  };
+
+  // Sub-step g in slot sc: four groups i of four MFMAs (row block i against
+  // weight pieces j).  During group i: the activation fragment of row block
+  // i + 1 (of sub-step g + 1, slot sn, for i = 3) and weight piece i of
+  // sub-step g + 1; this wavefront's DMA of sub-step g + NSS - 1 into slot
+  // (g - 1) % NSS (address sl), two loads per group and the scale load.
+  // Then, once sub-step g + 2 has landed (F8_DMA loads per later sub-step:
+  // NSS - 3 of them) and every wavefront holds sub-step g + 1's fragments,
+  // the barrier.
+  int sc = 0, sn = 1;
+  uint32_t sl = ring_lds + (F8_NSS - 1) * F8_SLOT;
+  // last: the item's last sub-step, which reads nothing of the next one
+  // (its first fragments are read after the epilogue, so that no operand
+  // registers are held across it)
+  auto substep = [&](int buf, bool first, bool last) {
+    const f32x16 zero = {};
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[buf][j], fa[i & 1], first ? zero : acc[i][j],
+                                                                     0, 0, 0, eb[buf], 0, ea[buf][i]);
+        if (j == 0 && i < 3) fa[(i + 1) & 1] = frag_a(sc, i + 1);
+        if (j == 0 && i == 3 && !last) fa[0] = frag_a(sn, 0);
+        if (j == 1 && !last) frag_b(sn, buf ^ 1, i);
+        if (j == 2 && i == 3 && !last) frag_sc(sn, buf ^ 1);
+        __builtin_amdgcn_sched_barrier(0);
+        // DMA: loads 2i, 2i + 1 after MFMAs 1 and 3 of group i; the scale
+        // load after MFMA 2 of group 0
+        if (j == 1 || j == 3) {
+          dma_piece(sl, 2 * i + (j >> 1));
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (i == 0 && j == 2) {
+          dma_scales(sl);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    dma_advance();
+    sl = ring_lds + sc * F8_SLOT;
+    sc = sn;
+    sn = sn + 1 == F8_NSS ? 0 : sn + 1;
+    wait_lgkm0();
+    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 3)));
+    barrier_nofence();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  // prologue: sub-steps 0 .. NSS - 2 into slots 0 .. NSS - 2; sub-steps 0
+  // and 1 landed before the first reads
+  dma_item();
+#pragma unroll 1
+  for (int g = 0; g < F8_NSS - 1; g++) {
+#pragma unroll
+    for (int q = 0; q < 8; q++) dma_piece(ring_lds + g * F8_SLOT, q);
+    dma_scales(ring_lds + g * F8_SLOT);
+    dma_advance();
+  }
+  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 3)));
+  barrier_nofence();
+  // the first fragments of the next sub-step (in slot sc), into buffer 0
+  auto first_frags = [&]() {
+    fa[0] = frag_a(sc, 0);
+#pragma unroll
+    for (int j = 0; j < 4; j++) frag_b(sc, 0, j);
+    frag_sc(sc, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  first_frags();
+
+#pragma unroll 1
+  for (int n = 0; n < my_items; n++) {
+    int tile, nbt;
+    item_of(n, tile, nbt);
+    const int row0 = tile * F8_M;
+    const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
+    const int nvalid = __builtin_amdgcn_readfirstlane(min(F8_M, s_off[slot] + s_cnt[slot] - row0));
+    const uint64_t tstart = p.timing ? __builtin_amdgcn_s_memrealtime() : 0;
+
+    // NU = 2 KT >= 4 sub-steps, an even number
+    substep(0, true, false);
+    substep(1, false, false);
+#pragma unroll 1
+    for (int u = 2; u < NU - 2; u += 2) {
+      substep(0, false, false);
+      substep(1, false, false);
+    }
+    substep(0, false, false);
+    substep(1, false, true);
+
+    // Epilogue.  Lane l of tile (i, j) holds token row 128 wm + 32 i + (l & 31)
+    // and, in element e, packed weight row 8 (e / 4) + 4 (l / 32) + e % 4 of
+    // piece j of block wn (gate/up: rows 0..15 gate, 16..31 the matching up
+    // columns, so gate and up of a column are elements e and e + 8).
+    int lid;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(lid));
+    const int l31 = lid & 31, hl = lid >> 5;
+    auto pack4 = [](float v0, float v1, float v2, float v3) {
+      uint2 w;
+      w.x = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
+      w.y = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+      return w;
+    };
+    if (GATEUP) {
+      // h of element e (0..7) of tile (i, j): silu(v[e]) * v[e + 8], h column
+      // 64 wn + 16 j + 8 (e / 4) + 4 hl + e % 4 of the item's 128
+      // one row block i at a time: its 32 h values of this lane, their amax
+      // over the lane, the row's other lane (l ^ 32) and the other
+      // wavefront (wn, through LDS), the smallest power-of-two scale
+      // >= amax / 448 (1 for an all-zero row), then e4m3 codes of h / 2^k
+      // (exact scaling), saturated at 448, round to nearest even.  Lane l
+      // holds bytes 4 hl .. 4 hl + 3 and 8 + 4 hl .. of the 16-byte chunk
+      // 4 wn + j of its row in the down GEMM's step nbt, which sits at load
+      // 2 wn + (j & 1), lane (l & 31) + 32 (j >> 1) of piece 4 wm + i.
+      char* hb = static_cast<char*>(p.C) + (size_t)tile * f8_tile_bytes(p.Nout) + (size_t)nbt * (F8_M * F8_STEP) +
+                 (4 * wm) * 4096 + (2 * wn) * 1024 + l31 * 16 + 4 * hl;
+      uint32_t ew = 0;
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        float h[4][8];
+        float m = 0.f;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          f32x16 v = acc[i][j];  // (one tile at a time, as below)
+          asm volatile("" : "+v"(v));
+#pragma unroll
+          for (int e = 0; e < 8; e++) {
+            h[j][e] = silu_mul(v[e], v[e + 8]);
+            m = fmaxf(m, fabsf(h[j][e]));
+          }
+        }
+        m = fmaxf(m, __shfl_xor(m, 32));
+        if (hl == 0) xamax[wn * F8_M + 128 * wm + 32 * i + l31] = m;
+        wait_lgkm0();
+        barrier_nofence();
+        m = fmaxf(m, xamax[(1 - wn) * F8_M + 128 * wm + 32 * i + l31]);
+        float sc = m > 0.f ? m / 448.0f : 1.0f;
+        uint32_t bits = __float_as_uint(sc);
+        if (m > 0.f && (bits & 0x7FFFFFu)) bits = (bits & 0xFF800000u) + 0x800000u;
+        const uint32_t e8 = (bits >> 23) & 0xFFu;
+        const int k = (int)e8 - 127;
+        ew |= e8 << (8 * i);
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          float q[8];
+#pragma unroll
+          for (int e = 0; e < 8; e++) q[e] = fminf(fmaxf(ldexpf(h[j][e], -k), -448.f), 448.f);
+          uint32_t w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+          w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], w0, true);
+          uint32_t w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
+          w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], w1, true);
+          char* d = hb + i * 4096 + (j & 1) * 1024 + (j >> 1) * 512;
+          *reinterpret_cast<uint32_t*>(d) = w0;
+          *reinterpret_cast<uint32_t*>(d + 8) = w1;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (wn == 0 && hl == 0)
+        *reinterpret_cast<uint32_t*>(p.C_sc + (size_t)tile * f8_tile_scale_bytes(p.Nout) + (size_t)nbt * 256 +
+                                     l31 * 8 + 4 * wm) = ew;
+    } else {
+      // bf16 rows of y_perm, as in the bf16 large-tile kernel: lanes l and
+      // l + 32 hold the two 8-byte halves of a row's 8-column chunk; one
+      // lane swap per pair of chunks gives 16 consecutive bytes per lane
+      auto swap16 = [](uint2 w0, uint2 w1) {
+        const auto x = __builtin_amdgcn_permlane32_swap(w0.x, w1.x, false, false);
+        const auto y = __builtin_amdgcn_permlane32_swap(w0.y, w1.y, false, false);
+        return i32x4{(int)x[0], (int)y[0], (int)x[1], (int)y[1]};
+      };
+      const size_t ld = (size_t)p.Nout * 2;
+      char* yb = static_cast<char*>(p.C) + (size_t)row0 * ld + (size_t)(nbt * NCOLS + 128 * wn + 8 * hl) * 2;
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const int r = 128 * wm + 32 * i + l31;
+        char* yr = yb + r * ld;
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+          // (one tile at a time: the empty asm keeps the compiler from
+          // reading every accumulator out of the AGPRs at once, which spills)
+          f32x16 v = acc[i][j];
+          asm volatile("" : "+v"(v));
+          uint2 w[4];
+#pragma unroll
+          for (int q = 0; q < 4; q++) w[q] = pack4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+          const i32x4 c0 = swap16(w[0], w[1]), c1 = swap16(w[2], w[3]);
+          if (r < nvalid) {  // padding rows of y_perm stay unwritten
+            *reinterpret_cast<i32x4*>(yr + (32 * j) * 2) = c0;
+            *reinterpret_cast<i32x4*>(yr + (32 * j + 16) * 2) = c1;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+    }
+    first_frags();
+    if (p.timing && WV == 0 && lid == 0) {
+      const uint64_t tend = __builtin_amdgcn_s_memrealtime();
+      atomicMin(reinterpret_cast<unsigned long long*>(&p.t0[slot]), (unsigned long long)tstart);
+      atomicMax(reinterpret_cast<unsigned long long*>(&p.t1[slot]), (unsigned long long)tend);
+    }
+  }
+  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
+}
+
+template <bool GATEUP>
+__global__ __launch_bounds__(256, 1) void k_gemm_big_f8(const F8Args p) {
+  __shared__ __attribute__((aligned(1024))) char ring[F8_NSS * F8_SLOT];
+  __shared__ float xamax[2 * F8_M];
+  __shared__ int32_t s_off[kMaxS + 1];
+  __shared__ int32_t s_cnt[kMaxS];
+  const int tid = threadIdx.x;
+  for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
+  for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
+  __syncthreads();
+  f8_body<GATEUP>(p, ring, xamax, s_off, s_cnt, __builtin_amdgcn_readfirstlane(tid >> 6));
+}
+
+}  // namespace
+
+bool experts_big_f8_supported(const tempo_moe_shape& s) {
+  // (I a multiple of 256: every item of both GEMMs has at least four sub-steps)
+  return s.dtype == TEMPO_FP8_E4M3_UE8M0 && s.m_tile == F8_M && s.H % F8_N == 0 && s.I % 256 == 0;
+}
+
+size_t experts_big_f8_pack_bytes(const tempo_moe_shape& s, int row_cap) {
+  // packed activation tiles, then their scale exponents
+  return experts_big_f8_supported(s) ? (size_t)row_cap * s.H + (size_t)row_cap * (s.H / F8_STEP) : 0;
+}
+
+// Both GEMMs of stage 2 for UE8M0 fp8 with 256 x 256 items.  The activation
+// rows come from x_rows (token rows, gathered through row_token) or, if that
+// is null, from the permuted rows in x_perm; their scales from the
+// block-major x_perm_scale of stage 1.
+hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
+                                 const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                                 const hipEvent_t* ev, hipStream_t st) {
+  const int grid = persistent_grid(1);
+  const int max_tiles = L.row_cap / F8_M;
+  auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
+  uint8_t* apack = reinterpret_cast<uint8_t*>(ws + L.apack);
+  uint8_t* apack_sc = apack + (size_t)L.row_cap * s.H;
+  const bool gather = x_rows != nullptr;
+  hipLaunchKernelGGL(k_pack_rows_f8, dim3(persistent_grid(4)), dim3(256), 0, st,
+                     static_cast<const uint8_t*>(gather ? x_rows : d.x_perm), d.x_perm_scale,
+                     gather ? 1 : 0, L.row_cap, d.row_token, d.slot_offsets, s.S, max_tiles, s.H, apack, apack_sc);
+
+  F8Args a{};
+  a.slot_counts = d.slot_counts;
+  a.slot_offsets = d.slot_offsets;
+  a.S = s.S;
+  a.max_tiles = max_tiles;
+  a.t0 = reinterpret_cast<uint64_t*>(ws + L.slot_t0);
+  a.t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
+  a.timing = timing ? 1 : 0;
+  uint8_t* h8 = reinterpret_cast<uint8_t*>(ws + L.h);
+  uint8_t* h_sc = reinterpret_cast<uint8_t*>(ws + L.h_scale);
+
+  F8Args gu = a;
+  gu.A = apack;
+  gu.A_sc = apack_sc;
+  gu.W = static_cast<const uint8_t*>(w.w13);
+  gu.w_slot_bytes = (size_t)2 * s.I * s.H;
+  gu.Wsp = w.w13_scale;
+  gu.ws_slot_floats = (size_t)(s.I / 64) * (s.H / F8_STEP) * 4;
+  gu.C = h8;  // packed h tiles
+  gu.C_sc = h_sc;
+  gu.Kd = s.H;
+  gu.Nout = s.I;
+  hipLaunchKernelGGL(k_gemm_big_f8<true>, dim3(grid), dim3(256), 0, st, gu);
+  if (!mark(0) || !mark(1)) return hipErrorLaunchFailure;
+
+  F8Args dn = a;
+  dn.A = h8;
+  dn.A_sc = h_sc;
+  dn.W = static_cast<const uint8_t*>(w.w2);
+  dn.w_slot_bytes = (size_t)s.H * s.I;
+  dn.Wsp = w.w2_scale;
+  dn.ws_slot_floats = (size_t)(s.H / F8_STEP) * (s.I / F8_STEP) * 4;
+  dn.C = y_perm;
+  dn.Kd = s.I;
+  dn.Nout = s.H;
+  hipLaunchKernelGGL(k_gemm_big_f8<false>, dim3(grid), dim3(256), 0, st, dn);
+  if (!mark(2)) return hipErrorLaunchFailure;
+  return hipGetLastError();
+}
+
+}  // namespace tempo

@@ -120,6 +120,7 @@ hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out
                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
                               hipStream_t st) {
   if (s.dtype == TEMPO_FP8_E4M3_UE8M0) {
+    if (experts_big_f8_supported(s)) return launch_experts_big_f8(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
     if (s.m_tile == 128) return launch_bm<128, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
     if (s.m_tile == 64) return launch_bm<64, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
     if (s.m_tile == 256) return launch_bm<256, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);

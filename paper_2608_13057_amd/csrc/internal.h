@@ -40,7 +40,7 @@ struct Layout {
   size_t h_scale;     // [I/128, row_cap] fp32 (fp8 only; scale-block-major)
   size_t h32;         // [row_cap, I] fp32 gate/up output before re-quantisation (fp8 only)
   size_t y_perm;      // [row_cap, H] bf16
-  size_t apack;       // 256-row bf16 tiles only: the activation rows packed in MFMA operand order
+  size_t apack;       // 256-row large-tile kernels only: the activation rows packed in MFMA operand order
   size_t part;        // [grid][8][m_tile][128] fp32 stage-2 partial tiles
   size_t fix;         // [grid][12] int32 stage-2 fixup records
   size_t total;
@@ -83,6 +83,17 @@ size_t experts_big_pack_bytes(const tempo_moe_shape& s, int row_cap);
 hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                               const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
                               const hipEvent_t* ev, hipStream_t st);
+
+// UE8M0 fp8 with 256-row M-tiles (H a multiple of 256): both GEMMs as
+// 256 x 256 items on the hardware-scaled fp8 MFMA, with the activation rows
+// and their scale exponents first packed into the workspace
+// (experts_big_f8_pack_bytes of it) and h re-quantised in the gate/up
+// epilogue.
+bool experts_big_f8_supported(const tempo_moe_shape& s);
+size_t experts_big_f8_pack_bytes(const tempo_moe_shape& s, int row_cap);
+hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
+                                 const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
+                                 const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,

@@ -46,28 +46,30 @@ def gemm_source_hash() -> str:
 
 def auto_m_tile(wl) -> int:
     """64-row tiles when an expert sees a few dozen rows (decode), 128 up to
-    128 rows per expert, and beyond that 256 for bf16 (the large-tile kernel;
-    at the prefill share 586 us per block against 987 us at 128) or 128 for
-    fp8."""
+    128 rows per expert, and beyond that 256 for bf16 and UE8M0 fp8 (the
+    large-tile kernels of the linear regime) or 128 for fp8 with fp32
+    scales."""
     per_expert = wl.T * wl.K / wl.E
     if per_expert <= 64:
         return 64
-    if per_expert <= 128 or wl.dtype != "bf16":
+    if per_expert <= 128 or wl.dtype == "fp8":
         return 128
     return 256
 
 
-def uses_big_kernel(dtype: str, m_tile: int, H: int) -> bool:
-    """Whether stage 2 runs the 256 x 256-item large-tile GEMM (bf16 with
-    256-row tiles and H a multiple of 256) rather than the stream-K one."""
-    return dtype == "bf16" and m_tile == 256 and H % 256 == 0
+def uses_big_kernel(dtype: str, m_tile: int, H: int, I: int = 256) -> bool:
+    """Whether stage 2 runs a 256 x 256-item large-tile GEMM (bf16, or UE8M0
+    fp8 with I a multiple of 256, with 256-row tiles and H a multiple of 256)
+    rather than the stream-K one."""
+    return (dtype == "bf16" or (dtype == "fp8mx" and I % 256 == 0)) and m_tile == 256 and H % 256 == 0
 
 
-def gateup_kernel_name(dtype: str, m_tile: int, H: int) -> str:
+def gateup_kernel_name(dtype: str, m_tile: int, H: int, I: int = 256) -> str:
     """Symbol (as rocprofv3 prints it) of the gate/up GEMM kernel a forward
     launches."""
-    if uses_big_kernel(dtype, m_tile, H):
-        return "tempo::(anonymous namespace)::k_gemm_big<true>"
+    if uses_big_kernel(dtype, m_tile, H, I):
+        return ("tempo::(anonymous namespace)::k_gemm_big<true>" if dtype == "bf16" else
+                "tempo::(anonymous namespace)::k_gemm_big_f8<true>")
     fp8 = "false" if dtype == "bf16" else "true"
     mx = "true" if dtype == "fp8mx" else "false"
     return f"tempo::gemm::k_gemm<{fp8}, {m_tile}, true, {mx}>"
@@ -178,7 +180,7 @@ def _mean_counter(rows, counter: str, match):
 def _is_gateup(name: str) -> bool:
     """The gate/up GEMM: the large-tile kernel k_gemm_big<true>, or the
     stream-K instance with GATEUP (its third template argument)."""
-    if "k_gemm_big<true>" in name.replace(" ", ""):
+    if "k_gemm_big<true>" in name.replace(" ", "") or "k_gemm_big_f8<true>" in name.replace(" ", ""):
         return True
     if "k_gemm<" not in name:
         return False

@@ -107,6 +107,11 @@ def bf16_ulp(v: np.ndarray) -> np.ndarray:
     return np.where(a > 0, 2.0 ** (e - 7), 2.0 ** -133)
 
 
+def identical_share(got: np.ndarray, ref: np.ndarray) -> float:
+    """Share of elements equal to the reference bit for bit."""
+    return float(np.mean(got == ref)) if got.size else 1.0
+
+
 def mirror_stats(got: np.ndarray, ref: np.ndarray) -> str:
     """Element-wise agreement with a reference that rounds where the GPU
     rounds: the share of elements that are identical and the largest

@@ -4,19 +4,27 @@ Tolerances: outputs are compared per token row as
   err = max_t ||y_t - r_t||_inf / ||r_t||_inf
 over rows with at least one local pair; rows without one must be exactly
 zero.  Against the fp64 oracle in its exact mode the bar is 1e-2 for bf16
-and 5e-2 for fp8; against its mirror mode (rounding h, o and y where the
-datapath stores them) a tighter bar shows the residual is fp32 accumulation
-order only."""
+and 5e-2 for fp8.  Against its mirror mode (which rounds h, o and y where
+the datapath stores them, with the dot products still in fp64) the residual
+comes only from the fp32 accumulation order moving a value across a rounding
+boundary, so most elements must be bit-identical and the rest differ by such
+flips: bf16 at least 99.9% identical and err <= 1e-3 (an h flip is one bf16
+ulp of one of I terms of an output; measured 1e-4 .. 3e-4); fp8 at least 85%
+identical and err <= 2e-2 (an e4m3 flip of one h element moves every output
+of its row by up to 2^-4 of that term; measured 6e-3 .. 1.3e-2, 92%
+identical)."""
 import numpy as np
 import pytest
 
 import oracle
-from helpers import Case, bf16_to_f64, mirror_stats, rel_err_rows, tile_sample, to_dev, to_host
+from helpers import (Case, bf16_to_f64, identical_share, mirror_stats, rel_err_rows, tile_sample, to_dev,
+                     to_host)
 
 pytestmark = pytest.mark.gpu
 
 TOL_EXACT = {"bf16": 1e-2, "fp8": 5e-2, "fp8mx": 5e-2}
-TOL_MIRROR = {"bf16": 8e-3, "fp8": 2e-2, "fp8mx": 2e-2}
+TOL_MIRROR = {"bf16": 1e-3, "fp8": 2e-2, "fp8mx": 2e-2}
+MIRROR_IDENTICAL = {"bf16": 0.999, "fp8": 0.85, "fp8mx": 0.85}
 
 
 def _run_forward(c, timing=False):
@@ -68,6 +76,8 @@ def test_experts_stage_tiny(m_tile, name, fresh_ws):
         err = rel_err_rows(got, ref, np.arange(len(real)))
         print(f"[experts {name} M={m_tile}] {mode} err={err:.2e} {mirror_stats(got, ref)}")
         assert err <= tol
+        if mode == "mirror":
+            assert identical_share(got, ref) >= MIRROR_IDENTICAL[wl.dtype]
 
 
 def test_combine_stage():
@@ -110,6 +120,8 @@ def test_forward_tiny(m_tile, name):
         err = rel_err_rows(got, ref, loc)
         print(f"[forward {name} M={m_tile}] {mode} err={err:.2e} {mirror_stats(got[loc], ref[loc])}")
         assert err <= (TOL_EXACT if mode == "exact" else TOL_MIRROR)[wl.dtype]
+        if mode == "mirror":
+            assert identical_share(got[loc], ref[loc]) >= MIRROR_IDENTICAL[wl.dtype]
     assert np.all(y[none] == 0)
     sc = d["slot_counts"]
     assert np.all((st > 0) == (sc > 0))
@@ -119,10 +131,10 @@ def test_forward_tiny(m_tile, name):
 def test_forward_split_invariance_bit_exact(name):
     """The same batch under different splits of the replicated experts over
     their two local slots gives bit-identical y for every M-tile; across
-    M-tiles served by the stream-K kernel (64 / 128 / 192, and 256 for fp8)
-    y is bit-identical too (its chunk boundaries do not depend on the tile).
-    bf16 256-row tiles run the large-tile kernel, whose summation order is a
-    different fixed one."""
+    M-tiles served by the stream-K kernel (64 / 128 / 192, and 256 for fp8
+    with fp32 scales) y is bit-identical too (its chunk boundaries do not
+    depend on the tile).  bf16 and UE8M0 fp8 256-row tiles run the large-tile
+    kernels, whose summation order is a different fixed one."""
     from paper_2608_13057_amd import synth
 
     wl = synth.make_workload(name)
@@ -136,7 +148,7 @@ def test_forward_split_invariance_bit_exact(name):
     for m_tile, os_ in outs.items():
         for o in os_[1:]:
             assert np.array_equal(o, os_[0]), f"plan changed y at M={m_tile}"
-    same = (64, 128, 192, 256) if wl.dtype != "bf16" else (64, 128, 192)
+    same = (64, 128, 192, 256) if wl.dtype == "fp8" else (64, 128, 192)
     for m_tile in same[1:]:
         assert np.array_equal(outs[m_tile][0], outs[same[0]][0]), f"M={m_tile} differs from M={same[0]}"
 
@@ -189,8 +201,8 @@ def test_forward_full_size_sampled(name, plan, m_tile):
 
 
 @pytest.mark.parametrize("name,m_tile", [("qwen3_prefill_bf16", 256), ("qwen3_prefill_fp8", 128),
-                                         ("qwen3_prefill_fp8mx", 128), ("qwen3_prefill_fp8", 256),
-                                         ("qwen3_prefill_bf16", 128)])
+                                         ("qwen3_prefill_fp8mx", 256), ("qwen3_prefill_fp8mx", 128),
+                                         ("qwen3_prefill_fp8", 256), ("qwen3_prefill_bf16", 128)])
 def test_forward_prefill_tile_sampled(name, m_tile):
     """The prefill share (8192 tokens, top-8 of 128, 18 slots) at full size:
     stage 1 bit-exact inside the forward, and y on a token sample stratified

@@ -1,5 +1,6 @@
-"""Register and LDS budget of the large-tile stage-2 GEMM, from the compiler's
-kernel metadata (CPU only: hipcc cross-compiles for gfx950).
+"""Register and LDS budget of the large-tile stage-2 GEMMs (bf16 and UE8M0
+fp8), from the compiler's kernel metadata (CPU only: hipcc cross-compiles for
+gfx950).
 
 The kernel streams its operands with LDS DMA issued from inline assembly,
 which the compiler does not track; a register spill makes it wait for every
@@ -16,10 +17,10 @@ import pytest
 
 from paper_2608_13057_amd import build
 
-SRC = os.path.join(build.CSRC, "gemm_big_agpr.hip")
+SOURCES = {"bf16": os.path.join(build.CSRC, "gemm_big_agpr.hip"), "fp8": os.path.join(build.CSRC, "gemm_big_f8_agpr.hip")}
 
 
-def _metadata(tmp_path):
+def _metadata(tmp_path, SRC):
     if not os.path.exists(build.HIPCC) and shutil.which("hipcc") is None:
         pytest.skip("hipcc not available")
     out = tmp_path / "big.s"
@@ -36,12 +37,15 @@ def _metadata(tmp_path):
     return kernels
 
 
-def test_large_tile_gemm_has_no_spills_and_fits_lds(tmp_path):
-    kernels = _metadata(tmp_path)
+@pytest.mark.parametrize("which", sorted(SOURCES))
+def test_large_tile_gemm_has_no_spills_and_fits_lds(tmp_path, which):
+    kernels = _metadata(tmp_path, SOURCES[which])
     big = {n: f for n, f in kernels.items() if "k_gemm_big" in n}
     assert len(big) == 2, sorted(kernels)  # gate/up and down
     for name, f in big.items():
         assert f["vgpr_spill_count"] == 0, (name, f)
-        assert f["sgpr_spill_count"] == 0, (name, f)
+        # scalar spills go to lanes of a VGPR (v_writelane / v_readlane), no
+        # memory access; the bf16 kernel has none, the fp8 one a few dozen
+        assert f["sgpr_spill_count"] <= (0 if which == "bf16" else 64), (name, f)
         assert f["group_segment_fixed_size"] <= 160 * 1024, (name, f)
         assert f.get("private_segment_fixed_size", 0) == 0, (name, f)
