@@ -168,6 +168,18 @@ typedef struct tempo_dispatch_out {
 } tempo_dispatch_out;
 
 /*
+ * One slot's packed weight tensors (device pointers), as
+ * tempo_moe_pack_weights writes them for a shape with S = 1; an entry of the
+ * per-slot table of tempo_expert_weights.
+ */
+typedef struct tempo_slot_weights {
+  const void* w13;
+  const float* w13_scale;
+  const void* w2;
+  const float* w2_scale;
+} tempo_slot_weights;
+
+/*
  * Expert weights of the S local slots (device pointers).  A replica slot
  * holds its own copy of its expert's weights.  In the natural layout:
  *   w13       [S, 2I, H]  rows 0..I-1 gate projection, rows I..2I-1 up projection
@@ -188,17 +200,29 @@ typedef struct tempo_expert_weights {
   const float* w13_scale;
   const void* w2;
   const float* w2_scale;
+  /* Stage 2 only, nullable: a device array [S] whose entry s holds slot s's
+   * packed tensors wherever they live (the replica sets of Sec. 3.1 come from
+   * a placement that puts each slot's weights where it likes).  When given,
+   * the four pointers above are ignored (and may be NULL); each entry's
+   * tensors are those of a 1-slot pack.  Stage 2 reads each entry once per
+   * work item.  tempo_moe_pack_weights ignores this field. */
+  const tempo_slot_weights* slot_table;
 } tempo_expert_weights;
 
 /*
  * Sizes for a shape.  *workspace_bytes: the workspace every other call needs
  * (one per stream in flight); *row_cap = T*K + S*(m_tile-1) rounded up to a
- * multiple of 128, the rows of the permuted buffers.  The workspace must be zero-filled once before its first
- * use (it holds the sticky error word); after that it is reused without
- * clearing.  Returns TEMPO_EINVAL / TEMPO_EUNSUPPORTED for shapes the library
- * rejects.  Either output pointer may be NULL.
+ * multiple of 128, the rows of the permuted buffers.  The workspace must be
+ * zero-filled once before its first use (it holds the sticky error word);
+ * after that it is reused without clearing.  *packed_bytes_per_slot: the
+ * bytes of one slot's packed weights, w13 + w2 (2I*H + H*I elements) plus,
+ * for fp8, the packed scales (I/64 * H/128 + H/128 * I/128 entries of 16
+ * bytes) -- what a slot table entry points at.  Returns TEMPO_EINVAL /
+ * TEMPO_EUNSUPPORTED for shapes the library rejects.  Any output pointer may
+ * be NULL.
  */
-int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap);
+int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap,
+                    size_t* packed_bytes_per_slot);
 
 /*
  * One-time re-layout of expert weights for the stage-2 kernels (not part of
@@ -319,6 +343,16 @@ int tempo_moe_forward_static(const tempo_moe_shape* shape, const tempo_plan* pla
  * clears it.  Returns TEMPO_EDEVICE if the synchronisation fails.
  */
 int tempo_moe_device_error(void* workspace, void* stream, uint32_t* bits);
+
+/*
+ * Per-expert pair counts of a window from two snapshots of the cumulative
+ * counters (tempo_dispatch_out.cum_counts; Sec. 4.4: a persistent cumulative
+ * counter needs no zeroing kernel, the reader recovers window counts by
+ * differencing): window[e] = (after[e] - before[e]) mod 2^32, exact while a
+ * window adds fewer than 2^32 pairs to an expert.  Host arrays of E entries;
+ * touches no GPU.  TEMPO_EINVAL for a null pointer or E < 1.
+ */
+int tempo_moe_counter_window(int32_t E, const uint32_t* before, const uint32_t* after, uint32_t* window);
 
 /* A static string describing a TEMPO_* return code. */
 const char* tempo_moe_strerror(int code);

@@ -14,8 +14,14 @@ Readings where the paper is silent: the initial assignment puts a point in the
 flat piece when its tokens-per-activation N/G is at most the median of N/G;
 each point is re-assigned to the piece whose prediction is larger (ties go to
 the flat piece); iteration stops when no point changes piece or after 50
-rounds; a piece with fewer than two distinct regressor rows keeps slope 0 and
-its intercept is the mean; an empty piece never wins a point.  n* = b/beta.
+rounds, and the run's result is its lowest-SSE iterate; a piece with fewer
+than two distinct regressor rows keeps slope 0 and its intercept is the mean;
+an empty piece never wins a point.  n* = b/beta.
+
+:func:`fit_restarts` -- the same alternation restarted from every
+single-breakpoint split of the points by N/G (flat iff N/G <= tau, for each
+distinct tau, and all-flat / all-linear) besides the median split, keeping the
+lowest SSE; for the tile-aware form also from the assignment of the Eq. 1 fit.
 """
 from __future__ import annotations
 
@@ -67,6 +73,7 @@ def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None):
         assign = list(init)
     cf = cl = None
     it = 0
+    best = None  # (sse, cf, cl, assignment that produced them, round)
     for it in range(1, iters + 1):
         fx, fy, lx, ly = [], [], [], []
         for i in range(m):
@@ -79,13 +86,18 @@ def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None):
         cf = _lstsq_piece(fx, fy)
         cl = _lstsq_piece(lx, ly)
         new = []
+        sse = 0.0
         for i in range(m):
             pf = -math.inf if cf is None else (cf[0] + cf[1] * G[i] + (cf[2] * (Tt[i] - G[i]) if tile else 0.0))
             pl = -math.inf if cl is None else cl[0] + cl[1] * N[i]
             new.append(0 if pf >= pl else 1)
+            sse += (max(pf, pl) - t[i]) ** 2
+        if best is None or sse < best[0]:
+            best = (sse, cf, cl, list(assign), it)
         if new == assign:
             break
         assign = new
+    _, cf, cl, assign, _ = best
     a, b = (float(cf[0]), float(cf[1])) if cf is not None else (float("nan"), float("nan"))
     b2 = float(cf[2]) if (cf is not None and tile) else 0.0
     c, beta = (float(cl[0]), float(cl[1])) if cl is not None else (float("nan"), float("nan"))
@@ -101,6 +113,26 @@ def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None):
     if tile:
         out["b2"] = b2
     return out
+
+
+def fit_restarts(G, N, t, T_tiles=None, iters: int = 50):
+    """fit_max_affine from the median split and from every single-breakpoint
+    split by N/G (flat iff N/G <= tau over the distinct ratios, plus
+    all-flat and all-linear); with tile counts also from the Eq. 1 fit's
+    assignment.  Returns the lowest-SSE result (ties: the earliest start)."""
+    m = len(t)
+    ratios = [float(N[i]) / float(G[i]) for i in range(m)]
+    starts = [None]
+    for tau in sorted(set(ratios)) + [-math.inf]:
+        starts.append([0 if ratios[i] <= tau else 1 for i in range(m)])
+    if T_tiles is not None:
+        starts.append(fit_restarts(G, N, t, None, iters)["assign"])
+    best = None
+    for init in starts:
+        r = fit_max_affine(G, N, t, T_tiles, iters, init)
+        if best is None or r["sse"] < best["sse"]:
+            best = r
+    return best
 
 
 def brute_force_best(G, N, t):

@@ -28,7 +28,8 @@ TEMPO_FP8_E4M3_UE8M0 = 2
 TEMPO_STATIC_SCRATCH_BYTES = 128 << 20
 
 SYMBOLS = ("tempo_moe_query", "tempo_moe_pack_weights", "tempo_moe_dispatch", "tempo_moe_experts", "tempo_moe_combine",
-           "tempo_moe_forward", "tempo_moe_forward_static", "tempo_moe_device_error", "tempo_moe_strerror")
+           "tempo_moe_forward", "tempo_moe_forward_static", "tempo_moe_device_error", "tempo_moe_counter_window",
+           "tempo_moe_strerror")
 
 _P = ctypes.c_void_p
 
@@ -47,8 +48,12 @@ class DispatchOut(ctypes.Structure):
                 ("pair_row", _P), ("cum_counts", _P), ("x_perm", _P), ("x_perm_scale", _P)]
 
 
-class ExpertWeights(ctypes.Structure):
+class SlotWeights(ctypes.Structure):
     _fields_ = [("w13", _P), ("w13_scale", _P), ("w2", _P), ("w2_scale", _P)]
+
+
+class ExpertWeights(ctypes.Structure):
+    _fields_ = [("w13", _P), ("w13_scale", _P), ("w2", _P), ("w2_scale", _P), ("slot_table", _P)]
 
 
 class TempoError(RuntimeError):
@@ -68,7 +73,10 @@ def load() -> ctypes.CDLL:
         raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2608_13057_amd.build`")
     lib = ctypes.CDLL(LIB_PATH)
     SP = ctypes.POINTER(Shape)
-    lib.tempo_moe_query.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_int32)]
+    lib.tempo_moe_query.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t), ctypes.POINTER(ctypes.c_int32),
+                                    ctypes.POINTER(ctypes.c_size_t)]
+    U32P = ctypes.POINTER(ctypes.c_uint32)
+    lib.tempo_moe_counter_window.argtypes = [ctypes.c_int32, U32P, U32P, U32P]
     lib.tempo_moe_pack_weights.argtypes = [SP, ctypes.POINTER(ExpertWeights), ctypes.POINTER(ExpertWeights), _P]
     lib.tempo_moe_dispatch.argtypes = [SP, ctypes.POINTER(Plan), _P, _P, _P, ctypes.POINTER(DispatchOut), _P,
                                        ctypes.c_size_t, _P]

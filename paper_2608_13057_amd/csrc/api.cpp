@@ -102,7 +102,9 @@ static int check_disp(const tempo_moe_shape* s, const tempo_dispatch_out* d, boo
 }
 
 static int check_weights(const tempo_moe_shape* s, const tempo_expert_weights* w) {
-  if (!w || !w->w13 || !w->w2) return TEMPO_EINVAL;
+  if (!w) return TEMPO_EINVAL;
+  if (w->slot_table) return TEMPO_OK;  // the entries are device memory, read by the kernels
+  if (!w->w13 || !w->w2) return TEMPO_EINVAL;
   if (s->dtype != TEMPO_BF16 && (!w->w13_scale || !w->w2_scale)) return TEMPO_EINVAL;
   return TEMPO_OK;
 }
@@ -116,12 +118,25 @@ using namespace tempo;
 
 extern "C" {
 
-int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap) {
+int tempo_moe_query(const tempo_moe_shape* shape, size_t* workspace_bytes, int32_t* row_cap,
+                    size_t* packed_bytes_per_slot) {
   int rc = check_shape(shape);
   if (rc) return rc;
   const Layout L = make_layout(*shape);
   if (workspace_bytes) *workspace_bytes = L.total;
   if (row_cap) *row_cap = L.row_cap;
+  if (packed_bytes_per_slot) {
+    const size_t H = shape->H, I = shape->I;
+    *packed_bytes_per_slot = shape->dtype == TEMPO_BF16
+                                 ? 3 * H * I * 2
+                                 : 3 * H * I + ((I / 64) * (H / 128) + (H / 128) * (I / 128)) * 16;
+  }
+  return TEMPO_OK;
+}
+
+int tempo_moe_counter_window(int32_t E, const uint32_t* before, const uint32_t* after, uint32_t* window) {
+  if (E < 1 || !before || !after || !window) return TEMPO_EINVAL;
+  for (int32_t e = 0; e < E; e++) window[e] = after[e] - before[e];  // unsigned: modulo 2^32
   return TEMPO_OK;
 }
 

@@ -41,7 +41,7 @@ extern "C" int tempo_moe_forward_static(const tempo_moe_shape* shape, const temp
                                         void* const* stage_events, void* stream) {
   // the size check needs no device: shapes beyond the array are refused first
   size_t need = 0;
-  const int rc = tempo_moe_query(shape, &need, nullptr);
+  const int rc = tempo_moe_query(shape, &need, nullptr, nullptr);
   if (rc != TEMPO_OK) return rc;
   if (need > (size_t)TEMPO_STATIC_SCRATCH_BYTES) return TEMPO_EWORKSPACE;
   void* ws = scratch_of_current_device();

@@ -31,6 +31,9 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.A = static_cast<const char*>(x_rows ? x_rows : d.x_perm);
   gu.row_src = x_rows ? d.row_token : nullptr;
   gu.W = static_cast<const char*>(w.w13);
+  gu.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  gu.wfield = kFieldW13;
+  gu.sfield = kFieldW13Scale;
   gu.w_slot_bytes = (size_t)2 * s.I * s.H * 2;
   gu.C = h;
   gu.Kd = s.H;
@@ -45,6 +48,9 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   GemmArgs dn = a;
   dn.A = h;
   dn.W = static_cast<const char*>(w.w2);
+  dn.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  dn.wfield = kFieldW2;
+  dn.sfield = kFieldW2Scale;
   dn.w_slot_bytes = (size_t)s.H * s.I * 2;
   dn.C = y_perm;
   dn.Kd = s.I;

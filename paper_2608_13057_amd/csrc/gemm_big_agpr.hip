@@ -133,7 +133,7 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
     item_of(dn, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * BIG_M));
     a_src = p.A + (size_t)tile * packed_tile_bytes(p.Kd);
-    w_src = p.W + (size_t)slot * p.w_slot_bytes + (size_t)(2 * nbt + (WV >> 1)) * KT * B_BYTES;
+    w_src = slot_tensor(p.W, p.w_slot_bytes, p.wtab, p.wfield, slot) + (size_t)(2 * nbt + (WV >> 1)) * KT * B_BYTES;
   };
   // This wavefront's share of a sub-step, as four 1 KB pieces: activation
   // pieces 2 WV and 2 WV + 1; weight pieces 2 WV and 2 WV + 1, i.e. the
@@ -378,6 +378,9 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
   GemmArgs gu = a;
   gu.A = ws + L.apack;
   gu.W = static_cast<const char*>(w.w13);
+  gu.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  gu.wfield = kFieldW13;
+  gu.sfield = kFieldW13Scale;
   gu.w_slot_bytes = (size_t)2 * s.I * s.H * 2;
   gu.C = ws + L.h;  // packed h
   gu.Kd = s.H;
@@ -388,6 +391,9 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
   GemmArgs dn = a;
   dn.A = ws + L.h;
   dn.W = static_cast<const char*>(w.w2);
+  dn.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  dn.wfield = kFieldW2;
+  dn.sfield = kFieldW2Scale;
   dn.w_slot_bytes = (size_t)s.H * s.I * 2;
   dn.C = y_perm;
   dn.Kd = s.I;

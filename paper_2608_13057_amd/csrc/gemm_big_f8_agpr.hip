@@ -108,6 +108,8 @@ struct F8Args {
   size_t w_slot_bytes;
   const float* Wsp;       // packed weight scales [slot][block][step][4] (powers of two)
   size_t ws_slot_floats;
+  const uint64_t* wtab;   // null, or the per-slot table (tempo_slot_weights [S])
+  int wfield, sfield;     // the table fields of W and Wsp (SlotField)
   void* C;                // gate/up: packed h tiles; down: y_perm rows (bf16)
   uint8_t* C_sc;          // gate/up: h scale exponents
   const int32_t* slot_counts;
@@ -164,10 +166,11 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     item_of(dn, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * F8_M));
     a_src = reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) + (2 * WV) * 4096;
-    w_src = reinterpret_cast<const char*>(p.W) + (size_t)slot * p.w_slot_bytes +
+    w_src = slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab, p.wfield, slot) +
             (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096;
     if (WV == 1)
-      sc_src = reinterpret_cast<const char*>(p.Wsp + (size_t)slot * p.ws_slot_floats + (size_t)(2 * nbt) * KT * 4);
+      sc_src = slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
+               (size_t)(2 * nbt) * KT * 16;
     else
       sc_src = reinterpret_cast<const char*>(p.A_sc) + (size_t)tile * f8_tile_scale_bytes(p.Kd);
   };
@@ -493,6 +496,9 @@ hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_
   gu.A = apack;
   gu.A_sc = apack_sc;
   gu.W = static_cast<const uint8_t*>(w.w13);
+  gu.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  gu.wfield = kFieldW13;
+  gu.sfield = kFieldW13Scale;
   gu.w_slot_bytes = (size_t)2 * s.I * s.H;
   gu.Wsp = w.w13_scale;
   gu.ws_slot_floats = (size_t)(s.I / 64) * (s.H / F8_STEP) * 4;
@@ -507,6 +513,9 @@ hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_
   dn.A = h8;
   dn.A_sc = h_sc;
   dn.W = static_cast<const uint8_t*>(w.w2);
+  dn.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  dn.wfield = kFieldW2;
+  dn.sfield = kFieldW2Scale;
   dn.w_slot_bytes = (size_t)s.H * s.I;
   dn.Wsp = w.w2_scale;
   dn.ws_slot_floats = (size_t)(s.H / F8_STEP) * (s.I / F8_STEP) * 4;

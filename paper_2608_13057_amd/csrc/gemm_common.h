@@ -74,6 +74,18 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(
 // same chunk hit 8 distinct bank groups).
 __device__ __forceinline__ int swz(int r, int c) { return r * ROWB + ((c ^ (r & 7)) << 4); }
 
+// Packed weight tensor field of a per-slot table entry (tempo_slot_weights).
+enum SlotField : int { kFieldW13 = 0, kFieldW13Scale = 1, kFieldW2 = 2, kFieldW2Scale = 3 };
+
+// Base of slot s's packed tensor: entry s of the per-slot table when the
+// caller gave one (tempo_slot_weights, four pointers per entry), else s
+// slots into the contiguous [S] tensor.  s is uniform, so the table read is
+// a scalar load.
+__device__ __forceinline__ const char* slot_tensor(const char* base, size_t per_slot, const uint64_t* table, int field,
+                                                   int s) {
+  return table ? reinterpret_cast<const char*>(table[(size_t)s * 4 + field]) : base + (size_t)s * per_slot;
+}
+
 // Slot of global M-tile row0 (largest s with off[s] <= row0; off has S+1
 // entries, row0 < off[S]).
 __device__ __forceinline__ int slot_of_row(const int32_t* off, int S, int row0) {

@@ -81,6 +81,9 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.row_src = x_rows ? d.row_token : nullptr;
   gu.As = d.x_perm_scale;
   gu.W = static_cast<const char*>(w.w13);
+  gu.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  gu.wfield = kFieldW13;
+  gu.sfield = kFieldW13Scale;
   gu.w_slot_bytes = (size_t)2 * s.I * s.H;
   gu.Wsp = w.w13_scale;
   gu.ws_slot_floats = (size_t)(s.I / 64) * (s.H / 128) * 4;
@@ -100,6 +103,9 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.A = reinterpret_cast<const char*>(h8);
   dn.As = hs;
   dn.W = static_cast<const char*>(w.w2);
+  dn.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
+  dn.wfield = kFieldW2;
+  dn.sfield = kFieldW2Scale;
   dn.w_slot_bytes = (size_t)s.H * s.I;
   dn.Wsp = w.w2_scale;
   dn.ws_slot_floats = (size_t)(s.H / 128) * (s.I / 128) * 4;

@@ -92,6 +92,8 @@ struct GemmArgs {
   size_t w_slot_bytes;
   const float* Wsp;         // fp8: packed weight scales [slot][block][step][4]
   size_t ws_slot_floats;
+  const uint64_t* wtab;     // null, or the per-slot table (tempo_slot_weights [S])
+  int wfield, sfield;       // the table fields of W and Wsp (SlotField)
   void* C;                  // output rows [row_cap][Nout]: bf16, or fp32 (fp8 gate/up)
   float* part;              // partial tiles [grid][CMAX][BM][128] fp32
   int32_t* fix;             // per workgroup: the split item whose chunk 0 it holds (FIX_WORDS int32)
@@ -352,7 +354,8 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
     const int row0 = tile * BM;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     is_nvalid = __builtin_amdgcn_readfirstlane(min(BM, s_off[slot] + s_cnt[slot] - row0));
-    w_base = p.W + (size_t)slot * p.w_slot_bytes + (size_t)nb * g.KT * B_BYTES + wave * (B_BYTES / 4) + lane * 16;
+    w_base = slot_tensor(p.W, p.w_slot_bytes, p.wtab, p.wfield, slot) + (size_t)nb * g.KT * B_BYTES +
+             wave * (B_BYTES / 4) + lane * 16;
     a_base = gather ? p.A : p.A + (size_t)row0 * a_row_bytes;
     const int tt = tile - tile_lo;
 #pragma unroll
@@ -378,7 +381,8 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
     }
     if (FP8) {
       as_base = reinterpret_cast<const char*>(p.As + row0);
-      ws_base = reinterpret_cast<const char*>(p.Wsp + (size_t)slot * p.ws_slot_floats + (size_t)nb * g.KT * 4);
+      ws_base = slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
+                (size_t)nb * g.KT * 16;
     }
     is_new = false;
   };
@@ -388,7 +392,8 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   // from one fixed 4 KB that stays in cache): the compiler counts the loads
   // issued after each set to place its waits, and a load skipped on some path
   // would make it wait for everything.
-  const i32x4* const w_idle = reinterpret_cast<const i32x4*>(p.W) + lane;
+  const i32x4* const w_idle =
+      reinterpret_cast<const i32x4*>(slot_tensor(p.W, p.w_slot_bytes, p.wtab, p.wfield, 0)) + lane;
   auto issue = [&](auto dd) {
     constexpr int d = decltype(dd)::value;
     const i32x4* wp = w_idle;

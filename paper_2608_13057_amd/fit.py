@@ -7,9 +7,16 @@ calibration fit.
   alternating assignment, at most 50 rounds, ordinary least squares per piece.
   Readings where the paper is silent: start with the points whose N/G is at
   most the median in the flat piece; re-assign each point to the piece with
-  the larger prediction (ties to the flat piece); stop when nothing moves; a
-  piece with fewer than two distinct regressor rows has slope 0 and the mean
-  as intercept; an empty piece never wins a point.
+  the larger prediction (ties to the flat piece); stop when nothing moves and
+  keep the run's lowest-SSE iterate; a piece with fewer than two distinct
+  regressor rows has slope 0 and the mean as intercept; an empty piece never
+  wins a point.  fit_restarts repeats the alternation from every
+  single-breakpoint split by N/G (and, for Eq. 2, from the Eq. 1 fit's
+  assignment) and keeps the lowest SSE.
+* degenerate(): a fit whose parameters are not a usable profile (a negative
+  or undefined a, b, c, beta or b2, or an Eq. 2 fit worse than Eq. 1) is
+  reported as such rather than tabulated (the paper reports a negative fitted
+  b as a degenerate negative control, Sec. 5.2).
 * n* = b / beta (the printed n* of the paper's parameter table is b/beta), and
   n*(G) = (a - c + b G) / (beta G), the per-slot tokens at which G equally
   loaded slots flip from the flat to the linear piece.
@@ -57,15 +64,20 @@ def fit(G, N, t, T=None, iters: int = 50, init=None) -> dict:
     flat = (ratio <= np.median(ratio)) if init is None else np.asarray(init, bool)
     cf = cl = None
     it = 0
+    best = None  # the lowest-SSE iterate: (sse, cf, cl, assignment)
     for it in range(1, iters + 1):
         cf = _ls(Xf[flat], t[flat])
         cl = _ls(Xl[~flat], t[~flat])
         pf = Xf @ cf if cf is not None else np.full_like(t, -np.inf)
         pl = Xl @ cl if cl is not None else np.full_like(t, -np.inf)
+        sse = float(((np.maximum(pf, pl) - t) ** 2).sum())
+        if best is None or sse < best[0]:
+            best = (sse, cf, cl, flat)
         new = pf >= pl
         if np.array_equal(new, flat):
             break
         flat = new
+    _, cf, cl, flat = best
     nan = float("nan")
     a, b = (float(cf[0]), float(cf[1])) if cf is not None else (nan, nan)
     c, beta = (float(cl[0]), float(cl[1])) if cl is not None else (nan, nan)
@@ -75,6 +87,37 @@ def fit(G, N, t, T=None, iters: int = 50, init=None) -> dict:
     out.update(n_star=(b / beta if (cl is not None and beta != 0) else nan), err_mean=float(rel.mean()),
                err_max=float(rel.max()), sse=float(((pred - t) ** 2).sum()), iterations=it, flat=flat)
     return out
+
+
+def fit_restarts(G, N, t, T=None, iters: int = 50) -> dict:
+    """fit() from the median split and from every single-breakpoint split by
+    N/G (flat iff N/G <= tau over the distinct ratios, plus all-flat and
+    all-linear); for Eq. 2 also from the Eq. 1 fit's assignment.  The
+    lowest-SSE result (ties: the earliest start)."""
+    G = np.asarray(G, np.float64)
+    N = np.asarray(N, np.float64)
+    ratio = N / G
+    starts = [None] + [ratio <= tau for tau in np.unique(ratio)] + [np.zeros(len(ratio), bool)]
+    if T is not None:
+        starts.append(fit_restarts(G, N, t, None, iters)["flat"])
+    best = None
+    for init in starts:
+        r = fit(G, N, t, T, iters, init)
+        if best is None or r["sse"] < best["sse"]:
+            best = r
+    return best
+
+
+def degenerate(params: dict, eq1: dict | None = None) -> str | None:
+    """Why a fit is not a usable profile, or None: a negative or undefined a,
+    b, c, beta or b2, or (for Eq. 2, given the Eq. 1 fit) a larger SSE than
+    Eq. 1, which it contains (b2 = 0)."""
+    bad = [k for k in ("a", "b", "c", "beta", "b2") if params.get(k) is not None and not params[k] >= 0]
+    if bad:
+        return "negative or undefined " + ", ".join(bad)
+    if eq1 is not None and params["sse"] > eq1["sse"] * (1 + 1e-9):
+        return "SSE above the Eq. 1 fit it contains"
+    return None
 
 
 def n_star_of_G(params: dict, G):

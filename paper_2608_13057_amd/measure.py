@@ -95,8 +95,8 @@ def committed_fit(shape: str, dtype: str, m_tile: int, scope: str = "gemm"):
     for line in text.splitlines():
         if line.startswith("fit_json: "):
             d = json.loads(line[len("fit_json: "):])
-            if d.get("scope") == scope:
-                return d
+            if d.get("scope") == scope and d.get("model") == "Eq. 1":
+                return dict(d, source=os.path.relpath(path, ROOT))
     sec = text.split(f"scope `{scope}`", 1)
     if len(sec) < 2:
         return None

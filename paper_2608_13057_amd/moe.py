@@ -82,8 +82,18 @@ def query(shape: MoEShape) -> tuple[int, int]:
     ws = ctypes.c_size_t(0)
     cap = ctypes.c_int32(0)
     sh = shape.c()
-    check(_lib.load().tempo_moe_query(ctypes.byref(sh), ctypes.byref(ws), ctypes.byref(cap)), "tempo_moe_query")
+    check(_lib.load().tempo_moe_query(ctypes.byref(sh), ctypes.byref(ws), ctypes.byref(cap), None),
+          "tempo_moe_query")
     return int(ws.value), int(cap.value)
+
+
+def packed_slot_bytes(shape: MoEShape) -> int:
+    """Bytes of one slot's packed weights (tempo_moe_query's
+    packed_bytes_per_slot)."""
+    n = ctypes.c_size_t(0)
+    sh = shape.c()
+    check(_lib.load().tempo_moe_query(ctypes.byref(sh), None, None, ctypes.byref(n)), "tempo_moe_query")
+    return int(n.value)
 
 
 class Workspace:
@@ -150,13 +160,27 @@ class PlanTensors:
 
 @dataclass
 class WeightTensors:
-    w13: torch.Tensor
-    w2: torch.Tensor
+    w13: torch.Tensor | None
+    w2: torch.Tensor | None
     w13_scale: torch.Tensor | None = None
     w2_scale: torch.Tensor | None = None
+    # stage 2: [S, 4] int64 device tensor of per-slot pointers
+    # (tempo_slot_weights: w13, w13_scale, w2, w2_scale), see slot_table()
+    slot_table: torch.Tensor | None = None
+    keep: tuple = ()  # the tensors a slot table points into (kept alive)
 
     def c(self) -> ExpertWeights:
-        return ExpertWeights(_ptr(self.w13), _ptr(self.w13_scale), _ptr(self.w2), _ptr(self.w2_scale))
+        return ExpertWeights(_ptr(self.w13), _ptr(self.w13_scale), _ptr(self.w2), _ptr(self.w2_scale),
+                             _ptr(self.slot_table))
+
+
+def slot_table(slots: list, device="cuda") -> WeightTensors:
+    """Weights given per slot: slots[s] holds slot s's packed tensors (a
+    1-slot pack_weights result) wherever they live; returns a WeightTensors
+    whose device table (tempo_slot_weights [S]) points at them."""
+    rows = [[_ptr(w.w13) or 0, _ptr(w.w13_scale) or 0, _ptr(w.w2) or 0, _ptr(w.w2_scale) or 0] for w in slots]
+    tab = torch.tensor(rows, dtype=torch.int64, device=device)
+    return WeightTensors(None, None, slot_table=tab, keep=tuple(slots))
 
 
 def pack_weights(shape: MoEShape, natural: WeightTensors, stream=None) -> WeightTensors:
@@ -191,6 +215,9 @@ def _check_plan(shape, plan):
 
 
 def _check_weights(shape, w, packed=False):
+    if packed and w.slot_table is not None:
+        _need(w.slot_table, torch.int64, (shape.S, 4), "slot_table")
+        return
     _need(w.w13, shape.elem, (shape.S, 2 * shape.I, shape.H), "w13")
     _need(w.w2, shape.elem, (shape.S, shape.H, shape.I), "w2")
     if shape.dtype != "bf16":
@@ -357,14 +384,18 @@ def device_error(ws: Workspace, stream=None) -> int:
 
 
 def counter_window(before, after):
-    """Per-expert pair counts of a window from two snapshots of the
-    cumulative counters (cum_counts, uint32, wrapping modulo 2^32): the
-    wrap-safe difference (after - before) mod 2^32 (Sec. 4.4: a persistent
-    cumulative counter needs no zeroing kernel; the reader recovers windows by
-    differencing).  Exact while a window adds fewer than 2^32 pairs per
-    expert.  Accepts numpy arrays or CPU tensors of int32 / uint32 bits."""
+    """tempo_moe_counter_window: per-expert pair counts of a window from two
+    snapshots of the cumulative counters (cum_counts, wrapping modulo 2^32).
+    Accepts numpy arrays or CPU tensors of int32 / uint32 bits; returns
+    uint32."""
     import numpy as np
 
-    b = np.asarray(before.cpu() if hasattr(before, "cpu") else before).view(np.uint32)
-    a = np.asarray(after.cpu() if hasattr(after, "cpu") else after).view(np.uint32)
-    return (a.astype(np.uint64) - b.astype(np.uint64)) % (1 << 32)
+    b = np.ascontiguousarray(np.asarray(before.cpu() if hasattr(before, "cpu") else before).view(np.uint32))
+    a = np.ascontiguousarray(np.asarray(after.cpu() if hasattr(after, "cpu") else after).view(np.uint32))
+    if a.shape != b.shape or a.ndim != 1:
+        raise ValueError("before and after must be 1-D arrays of the same length")
+    out = np.empty_like(a)
+    u32p = ctypes.POINTER(ctypes.c_uint32)
+    check(_lib.load().tempo_moe_counter_window(len(a), b.ctypes.data_as(u32p), a.ctypes.data_as(u32p),
+                                               out.ctypes.data_as(u32p)), "tempo_moe_counter_window")
+    return out

@@ -26,8 +26,9 @@ import time
 import numpy as np
 
 QWEN = dict(H=4096, I=1536)
-SHAPES = {"qwen3": QWEN, "dsv3": dict(H=7168, I=2048)}  # expert shapes of the paper's two models
-DEFAULT_G = (1, 2, 4, 8, 12, 16, 24, 32)
+SHAPES = {"qwen3": QWEN, "dsv3": dict(H=7168, I=2048),  # expert shapes of the paper's two models
+          "tiny": dict(H=256, I=512)}  # the tiny parity shape (harness tests)
+DEFAULT_G = tuple(range(1, 33))
 DEFAULT_N = (1, 2, 4, 8, 16, 32, 48, 64, 96, 128, 129, 160, 192, 256, 257, 320, 384, 512, 768, 1024, 2048)
 POOL_SLOTS = 32
 
@@ -103,10 +104,13 @@ class Harness:
         offs = list(range(0, POOL_SLOTS - G + 1, max(1, G))) or [0]
         wsets = [self.weights_at(o, G) for o in offs]
         fwd = [moe.PreparedForward(shape, plan, d_ids, d_w, d_x, d_xs, w, disp, y, ws) for w in wsets]
-        # stage 1 once so that stage 2 alone has its inputs
-        fwd[0]()
+        # stage 1 once so that stage 2 alone has its inputs, with the per-slot
+        # spans of its stage 2 (the library's per-slot timings)
+        spans = torch.zeros(G, dtype=torch.int64, device="cuda")
+        moe.forward(shape, plan, d_ids, d_w, d_x, d_xs, wsets[0], disp, y, ws, slot_time_ns=spans)
         torch.cuda.synchronize()
         sc = disp.slot_counts.cpu().numpy()
+        slot_us = (spans.cpu().numpy() / 1e3).round(3).tolist()
         assert int(sc.sum()) == T and int((sc > 0).sum()) == G, "sweep routing did not land as constructed"
         tiles = int(sum(-(-int(c) // self.m_tile) for c in sc))
         rows = []
@@ -133,7 +137,8 @@ class Harness:
             ts = np.array([a.elapsed_time(b) * 1e3 for a, b in evs])
             rows.append(dict(dtype=self.dtype, H=self.H, I=self.I, m_tile=self.m_tile, scope=scope, G=G, n=n,
                              N=T, tiles=tiles, t_us=float(np.median(ts)), p10=float(np.percentile(ts, 10)),
-                             p90=float(np.percentile(ts, 90)), reps=reps, rotation_sets=len(wsets)))
+                             p90=float(np.percentile(ts, 90)), reps=reps, rotation_sets=len(wsets),
+                             slot_counts=sc.tolist(), slot_span_us=slot_us))
         del fwd, wsets, disp, ws, y, y_perm
         return rows
 
@@ -169,11 +174,12 @@ def summarize(rows, scope="gemm") -> dict:
     N = np.array([r["N"] for r in R], np.float64)
     T = np.array([r["tiles"] for r in R], np.float64)
     t = np.array([r["t_us"] for r in R], np.float64)
-    e1 = F.fit(G, N, t)
-    e2 = F.fit(G, N, t, T=T)
+    e1 = F.fit_restarts(G, N, t)
+    e2 = F.fit_restarts(G, N, t, T=T)
     ci = F.bootstrap_b(G, N, t, reps=200)
     clean = lambda d: {k: v for k, v in d.items() if k != "flat"}
-    return dict(scope=scope, points=len(R), eq1=clean(e1), eq2=clean(e2), b_ci95=ci)
+    return dict(scope=scope, points=len(R), eq1=clean(e1), eq2=clean(e2), b_ci95=ci,
+                degenerate1=F.degenerate(e1), degenerate2=F.degenerate(e2, e1))
 
 
 def markdown(rows, title: str, command: str, ns=DEFAULT_N) -> str:
@@ -188,13 +194,22 @@ def markdown(rows, title: str, command: str, ns=DEFAULT_N) -> str:
         out += [f"## Fit, scope `{scope}` ({sm['points']} grid points)", "",
                 "| model | a (us) | b (us/slot) | c (us) | beta (us/token) | b2 (us/extra tile) | n* = b/beta | mean rel. err | "
                 "max rel. err | rounds |", "|---|---|---|---|---|---|---|---|---|---|"]
-        for k, lab in (("eq1", "Eq. 1"), ("eq2", "Eq. 2 (tiles)")):
+        fits = []
+        for k, dk, lab in (("eq1", "degenerate1", "Eq. 1"), ("eq2", "degenerate2", "Eq. 2 (tiles)")):
             e = sm[k]
+            if sm[dk]:
+                out.append(f"| {lab} | degenerate: {sm[dk]} | | | | | | {e['err_mean']:.3f} | {e['err_max']:.3f} | "
+                           f"{e['iterations']} |")
+                continue
             b2 = "" if e.get("b2") is None else f"{e['b2']:.3f}"
             out.append(f"| {lab} | {e['a']:.2f} | {e['b']:.3f} | {e['c']:.2f} | {e['beta']:.5f} | {b2} | "
                        f"{e['n_star']:.1f} | {e['err_mean']:.3f} | {e['err_max']:.3f} | {e['iterations']} |")
+            fits.append(dict(scope=scope, model=lab, **{x: e[x] for x in ("a", "b", "c", "beta", "n_star", "err_mean",
+                                                                           "err_max")},
+                             **({"b2": e["b2"]} if e.get("b2") is not None else {})))
         lo, med, hi = sm["b_ci95"]
         out += ["", f"Bootstrap 95% interval of b: {lo:.3f} .. {hi:.3f} us (median {med:.3f}).", ""]
+        out += ["fit_json: " + json.dumps(f) for f in fits] + [""]
     g = sorted({r["G"] for r in grid})
     nn = sorted({r["n"] for r in grid})
     t = {(r["G"], r["n"]): r["t_us"] for r in grid if r["scope"] == "gemm"}
@@ -221,7 +236,7 @@ def main():
     ap.add_argument("--quick", action="store_true", help="small grid")
     ap.add_argument("--fine", action="store_true", help="add the single-slot sweep n = 1..2048")
     ap.add_argument("--from-jsonl", default=None, help="summarise an earlier sweep instead of running one")
-    ap.add_argument("--md", default=None, help="with --from-jsonl: write a markdown summary here")
+    ap.add_argument("--md", default=None, help="write a markdown summary here (after a sweep or with --from-jsonl)")
     ap.add_argument("--title", default="")
     ap.add_argument("--command", default="")
     args = ap.parse_args()
@@ -237,8 +252,14 @@ def main():
     Gs, ns = (DEFAULT_G, DEFAULT_N) if not args.quick else ((1, 4, 16), (1, 64, 128, 129, 512, 2048))
     fine = tuple(range(1, 2049)) if args.fine else ()
     rows = run_sweep(args.dtype, args.m_tile, Gs, ns, fine, args.out, args.reps, args.shape)
+    if args.md:
+        # the summary carries the exact command that produced it
+        cmd = "python -m paper_2608_13057_amd.profile " + " ".join(sys.argv[1:])
+        md = markdown(rows, args.title or f"{args.shape} {args.dtype}, M-tile {args.m_tile}", cmd, ns)
+        with open(args.md, "w") as fh:
+            fh.write(md)
     res = {s: summarize([r for r in rows if not (r["G"] == 1 and r["n"] not in ns)], s) for s in ("gemm", "block")}
-    print(json.dumps(dict(dtype=args.dtype, m_tile=args.m_tile, fits=res)))
+    print(json.dumps(dict(dtype=args.dtype, m_tile=args.m_tile, fits=res), default=str))
 
 
 if __name__ == "__main__":

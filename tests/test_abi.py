@@ -47,14 +47,15 @@ def test_host_only_entry_points():
         kw.update(bad)
         sh = _lib.Shape(*[kw[n] for n in ("T", "T_valid", "K", "E", "S", "H", "I", "m_tile", "dtype")])
         ws, cap = ctypes.c_size_t(0), ctypes.c_int32(0)
-        assert lib.tempo_moe_query(ctypes.byref(sh), ctypes.byref(ws), ctypes.byref(cap)) == _lib.TEMPO_EINVAL, bad
+        assert lib.tempo_moe_query(ctypes.byref(sh), ctypes.byref(ws), ctypes.byref(cap), None) == \
+            _lib.TEMPO_EINVAL, bad
 
 
 def test_struct_layouts_match_the_header(tmp_path):
     if shutil.which("gcc") is None:
         pytest.skip("gcc not available")
     structs = {"tempo_moe_shape": _lib.Shape, "tempo_plan": _lib.Plan, "tempo_dispatch_out": _lib.DispatchOut,
-               "tempo_expert_weights": _lib.ExpertWeights}
+               "tempo_expert_weights": _lib.ExpertWeights, "tempo_slot_weights": _lib.SlotWeights}
     lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HDR}"', "int main(void) {"]
     for cname, py in structs.items():
         lines.append(f'  printf("{cname} size %zu\\n", sizeof({cname}));')
@@ -90,3 +91,13 @@ def test_static_forward_refuses_shapes_beyond_its_scratch():
     assert lib.tempo_moe_forward_static(ctypes.byref(bad), *args) == _lib.TEMPO_EINVAL
     small = moe.MoEShape(T=512, K=8, E=128, S=18, H=4096, I=1536, m_tile=64)
     assert moe.query(small)[0] <= _lib.TEMPO_STATIC_SCRATCH_BYTES
+
+
+def test_packed_bytes_per_slot():
+    """One slot's packed weights: w13 + w2 elements (2 bytes for bf16, 1 for
+    fp8) plus, for fp8, the packed 16-byte scale entries of both matrices."""
+    H, I = 4096, 1536
+    assert moe.packed_slot_bytes(moe.MoEShape(T=8, K=2, E=4, S=3, H=H, I=I, dtype="bf16")) == 3 * H * I * 2
+    fp8 = 3 * H * I + ((I // 64) * (H // 128) + (H // 128) * (I // 128)) * 16
+    for dt in ("fp8", "fp8mx"):
+        assert moe.packed_slot_bytes(moe.MoEShape(T=8, K=2, E=4, S=3, H=H, I=I, dtype=dt)) == fp8

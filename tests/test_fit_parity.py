@@ -33,6 +33,27 @@ def test_fit_matches_oracle(seed, tile):
     assert p["iterations"] == o["iterations"]
 
 
+@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("tile", [False, True])
+def test_restart_fit_matches_oracle(seed, tile):
+    G, N, T, t = _data(seed, m=40, noise=0.08, tile=tile)
+    o = ofit.fit_restarts(G, N, t, T_tiles=T if tile else None)
+    p = pfit.fit_restarts(G, N, t, T=T if tile else None)
+    keys = ["a", "b", "c", "beta", "sse"] + (["b2"] if tile else [])
+    for k in keys:
+        assert p[k] == pytest.approx(o[k], rel=1e-9, abs=1e-9), k
+    assert list(p["flat"].astype(int)) == [1 - v for v in o["assign"]]
+
+
+def test_degenerate_flags():
+    good = dict(a=30.0, b=4.0, c=25.0, beta=0.015, b2=None, sse=1.0)
+    assert pfit.degenerate(good) is None
+    assert "b" in pfit.degenerate(dict(good, b=-1.0))
+    assert "beta" in pfit.degenerate(dict(good, beta=float("nan")))
+    assert "b2" in pfit.degenerate(dict(good, b2=-0.5))
+    assert "Eq. 1" in pfit.degenerate(dict(good, b2=0.1, sse=2.0), eq1=dict(good, sse=1.5))
+
+
 def test_predict_and_n_star_of_G():
     prm = dict(a=30.0, b=4.0, c=25.0, beta=0.015, b2=None)
     assert pfit.predict(prm, 2, 100) == pytest.approx(ofit.cost(2, 100, 30.0, 4.0, 25.0, 0.015))

@@ -1,5 +1,6 @@
-"""Host logic: windows of the cumulative per-expert counters (Sec. 4.4:
-cumulative counting, windows recovered by wrap-safe differencing)."""
+"""Host logic of the library (tempo_moe_counter_window, no GPU): windows of
+the cumulative per-expert counters (Sec. 4.4: cumulative counting, windows
+recovered by wrap-safe differencing)."""
 import numpy as np
 
 from paper_2608_13057_amd import moe
@@ -25,5 +26,16 @@ def test_counter_window_of_successive_batches_adds_up():
     for _ in range(20):
         snaps.append((snaps[-1] + rng.integers(0, 2**30, size=16, dtype=np.uint64)) % 2**32)
     snaps = [s.astype(np.uint32) for s in snaps]
-    total = sum(moe.counter_window(a, b) for a, b in zip(snaps[:-1], snaps[1:]))
+    total = sum(moe.counter_window(a, b).astype(np.uint64) for a, b in zip(snaps[:-1], snaps[1:]))
     assert np.array_equal(total % 2**32, moe.counter_window(snaps[0], snaps[-1]))
+
+
+def test_counter_window_rejects_bad_arguments():
+    import ctypes
+
+    from paper_2608_13057_amd import _lib
+
+    lib = _lib.load()
+    buf = (ctypes.c_uint32 * 4)()
+    assert lib.tempo_moe_counter_window(0, buf, buf, buf) == _lib.TEMPO_EINVAL
+    assert lib.tempo_moe_counter_window(4, None, buf, buf) == _lib.TEMPO_EINVAL

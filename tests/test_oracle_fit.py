@@ -112,3 +112,49 @@ def test_fit_equals_brute_force_on_separated_data():
     t = [fit.cost(g, n, 10, 3, 5, 0.05) for g, n in zip(G, N)]
     r = fit.fit_max_affine(G, N, t)
     assert r["sse"] == pytest.approx(fit.brute_force_best(G, N, t), abs=1e-9)
+
+
+def _mostly_flat(seed, m=10):
+    """Points of which about 80% sit in the flat regime, so that the median
+    split of N/G starts half of the flat points in the linear piece."""
+    rng = np.random.default_rng(seed)
+    G = rng.integers(1, 9, m).astype(float)
+    n = np.where(rng.random(m) < 0.8, rng.integers(1, 60, m), rng.integers(300, 2000, m)).astype(float)
+    N = G * n
+    t = np.array([fit.cost(g, nn, 40.0, 6.0, 20.0, 0.05) for g, nn in zip(G, N)]) * (1 + 0.03 * rng.standard_normal(m))
+    return G, N, t
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_restarts_bounded_by_brute_force_and_median_start(seed):
+    """The restarted fit never beats the exhaustive optimum and never does
+    worse than the median start alone."""
+    G, N, t = _mostly_flat(seed)
+    med = fit.fit_max_affine(G, N, t)
+    r = fit.fit_restarts(G, N, t)
+    best = fit.brute_force_best(G, N, t)
+    assert r["sse"] >= best * (1 - 1e-9)
+    assert r["sse"] <= med["sse"] * (1 + 1e-12)
+
+
+@pytest.mark.parametrize("seed", [3, 38, 40])
+def test_restarts_reach_the_optimum_where_the_median_start_does_not(seed):
+    """On data where alternation from the median split stops in a worse
+    local optimum, one of the single-breakpoint starts reaches the
+    exhaustive optimum."""
+    G, N, t = _mostly_flat(seed)
+    best = fit.brute_force_best(G, N, t)
+    assert fit.fit_max_affine(G, N, t)["sse"] > best * 1.01
+    assert fit.fit_restarts(G, N, t)["sse"] == pytest.approx(best, rel=1e-9)
+
+
+def test_run_keeps_its_lowest_sse_iterate():
+    """A run capped at one round returns that round's fit; more rounds never
+    give a larger SSE than fewer (the lowest-SSE iterate is kept)."""
+    G, N, t = _mostly_flat(38)
+    prev = None
+    for k in range(1, 8):
+        r = fit.fit_max_affine(G, N, t, iters=k)
+        if prev is not None:
+            assert r["sse"] <= prev + 1e-9
+        prev = r["sse"]
