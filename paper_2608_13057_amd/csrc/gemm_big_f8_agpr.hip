@@ -207,11 +207,11 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   };
 
   f32x16 acc[4][4];
-  // Operand registers: the weight fragments of a sub-step are read during
-  // the previous one (fb[buf ^ 1]); the activation fragment of row block
-  // i + 1 during the MFMAs of row block i (fa[(i + 1) & 1]; for i = 3 that is
-  // row block 0 of the next sub-step), so 80 registers hold the operands.
-  i32x8 fa[2], fb[2][4];
+  // Operand registers, double-buffered: every fragment of sub-step g + 1
+  // (activation row blocks, weight pieces, scale exponents) is read during
+  // sub-step g, so a ring slot is free once the barrier that ends the
+  // sub-step before its own has passed.
+  i32x8 fa[2][4], fb[2][4];
   int ea[2][4], eb[2];
   auto rd8 = [&](const char* s) {
     const i32x4 lo = *reinterpret_cast<const i32x4*>(s);
@@ -219,7 +219,9 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     return (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
   // activation row block i of ring slot `slot` (piece 4 wm + i)
-  auto frag_a = [&](int slot, int i) { return rd8(ring + slot * F8_SLOT + (4 * wm + i) * 2048 + lane * 16); };
+  auto frag_a = [&](int slot, int buf, int i) {
+    fa[buf][i] = rd8(ring + slot * F8_SLOT + (4 * wm + i) * 2048 + lane * 16);
+  };
   // weight piece j of block wn
   auto frag_b = [&](int slot, int buf, int j) {
     fb[buf][j] = rd8(ring + slot * F8_SLOT + F8_SUB + (4 * wn + j) * 2048 + lane * 16);
@@ -236,37 +238,31 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     eb[buf] = (int)ue8m0_of(GATEUP ? ws[((lane >> 4) & 1)] : ws[0]);
   };
 
-  // Sub-step g in slot sc: four groups i of four MFMAs (row block i against
-  // weight pieces j).  During group i: the activation fragment of row block
-  // i + 1 (of sub-step g + 1, slot sn, for i = 3) and weight piece i of
-  // sub-step g + 1; this wavefront's DMA of sub-step g + NSS - 1 into slot
-  // (g - 1) % NSS (address sl) during groups 0 and 1.
-  // Then, once sub-step g + 2 has landed (F8_DMA loads per later sub-step:
-  // NSS - 3 of them) and every wavefront holds sub-step g + 1's fragments,
-  // the barrier.
-  int sc = 0, sn = 1;
-  uint32_t sl = ring_lds + (F8_NSS - 1) * F8_SLOT;
+  // Sub-step g, operands in registers (buffer buf), its slot sc already
+  // read: four groups i of four MFMAs (row block i against weight pieces j).
+  // During group i: activation row block i and weight piece i of sub-step
+  // g + 1 (slot sn); the scale exponents in group 3.  This wavefront's DMA
+  // of sub-step g + NSS goes into slot sc during groups 0 and 1 (as early as
+  // possible: the ring holds only a few 32 KB sub-steps).  Then, once
+  // sub-step g + 2 has landed (F8_DMA loads per later sub-step: NSS - 2 of
+  // them) and every wavefront holds sub-step g + 1, the barrier.
   // last: the item's last sub-step, which reads nothing of the next one
   // (its first fragments are read after the epilogue, so that no operand
   // registers are held across it)
+  int sc = 0, sn = 1;
   auto substep = [&](int buf, bool first, bool last) {
     const f32x16 zero = {};
+    const uint32_t sl = ring_lds + sc * F8_SLOT;
 #pragma unroll
     for (int i = 0; i < 4; i++) {
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[buf][j], fa[i & 1], first ? zero : acc[i][j],
+        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[buf][j], fa[buf][i], first ? zero : acc[i][j],
                                                                      0, 0, 0, eb[buf], 0, ea[buf][i]);
-        if (j == 0 && i < 3) fa[(i + 1) & 1] = frag_a(sc, i + 1);
-        if (j == 0 && i == 3 && !last) fa[0] = frag_a(sn, 0);
+        if (j == 0 && !last) frag_a(sn, buf ^ 1, i);
         if (j == 1 && !last) frag_b(sn, buf ^ 1, i);
         if (j == 2 && i == 3 && !last) frag_sc(sn, buf ^ 1);
         __builtin_amdgcn_sched_barrier(0);
-        // DMA: one load after each MFMA of the first two groups, the scale
-        // load after the last of them (issued early: with 32 KB slots the
-        // ring holds only about two sub-steps ahead, so every cycle of
-        // lookahead counts; measured 4% faster than spreading the loads over
-        // the whole sub-step)
         if (i < 2) {
           dma_piece(sl, 4 * i + j);
           if (i == 1 && j == 3) dma_scales(sl);
@@ -275,33 +271,37 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
       }
     }
     dma_advance();
-    sl = ring_lds + sc * F8_SLOT;
     sc = sn;
     sn = sn + 1 == F8_NSS ? 0 : sn + 1;
     wait_lgkm0();
-    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 3)));
+    __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 2)));
     barrier_nofence();
     __builtin_amdgcn_sched_barrier(0);
   };
 
-  // prologue: sub-steps 0 .. NSS - 2 into slots 0 .. NSS - 2; sub-steps 0
+  // prologue: sub-steps 0 .. NSS - 1 into slots 0 .. NSS - 1; sub-steps 0
   // and 1 landed before the first reads
   dma_item();
 #pragma unroll 1
-  for (int g = 0; g < F8_NSS - 1; g++) {
+  for (int g = 0; g < F8_NSS; g++) {
 #pragma unroll
     for (int q = 0; q < 8; q++) dma_piece(ring_lds + g * F8_SLOT, q);
     dma_scales(ring_lds + g * F8_SLOT);
     dma_advance();
   }
-  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 3)));
+  __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 2)));
   barrier_nofence();
-  // the first fragments of the next sub-step (in slot sc), into buffer 0
+  // the fragments of the sub-step in slot sc, into buffer 0; then a barrier,
+  // since that sub-step's DMA refills the slot
   auto first_frags = [&]() {
-    fa[0] = frag_a(sc, 0);
 #pragma unroll
-    for (int j = 0; j < 4; j++) frag_b(sc, 0, j);
+    for (int i = 0; i < 4; i++) {
+      frag_a(sc, 0, i);
+      frag_b(sc, 0, i);
+    }
     frag_sc(sc, 0);
+    wait_lgkm0();
+    barrier_nofence();
     __builtin_amdgcn_sched_barrier(0);
   };
   first_frags();
