@@ -79,11 +79,18 @@ enum SlotField : int { kFieldW13 = 0, kFieldW13Scale = 1, kFieldW2 = 2, kFieldW2
 
 // Base of slot s's packed tensor: entry s of the per-slot table when the
 // caller gave one (tempo_slot_weights, four pointers per entry), else s
-// slots into the contiguous [S] tensor.  s is uniform, so the table read is
-// a scalar load.
+// slots into the contiguous [S] tensor.  s is uniform.  The entry is read
+// with a scalar load in inline assembly: the compiler would otherwise use a
+// vector load (it cannot tell the table from the memory the kernel writes)
+// and wait for every vector load in flight before using it, the operand
+// DMA ring included.
 __device__ __forceinline__ const char* slot_tensor(const char* base, size_t per_slot, const uint64_t* table, int field,
                                                    int s) {
-  return table ? reinterpret_cast<const char*>(table[(size_t)s * 4 + field]) : base + (size_t)s * per_slot;
+  if (!table) return base + (size_t)s * per_slot;
+  const uint64_t* e = table + (size_t)s * 4 + field;
+  uint64_t v;
+  asm volatile("s_load_dwordx2 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(e) : "memory");
+  return reinterpret_cast<const char*>(v);
 }
 
 // Slot of global M-tile row0 (largest s with off[s] <= row0; off has S+1
