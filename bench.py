@@ -285,6 +285,9 @@ def roofline(m):
     traffic, traffic_current = measure.committed_traffic(m.name, m.m_tile)
     common = {"traffic": traffic if traffic_current else None, "kernel": kernel + " (gate/up)",
               "launch_us": m.kernel_us["gate_up_gemm"], "G": m.G, "N": m.N}
+    mf = measure.committed_mfma(m.name, m.m_tile)
+    if mf is not None:  # counter evidence (rocprofv3 --pmc) for the same kernel sources
+        common["mfma_counters"] = {k: mf[k] for k in ("mfma_busy", "clock_ghz", "executed_tflops", "launch_us")}
     # pairs per activated slot against the ideal balance point e P / (2 BW) ~ 312
     linear = measure.uses_big_kernel(wl.dtype, m.m_tile, wl.H, wl.I) or m.N / max(1, m.G) > 312
     if linear:

@@ -12,6 +12,9 @@ under profiles/).
         HBM bytes per launch of the gate/up GEMM from two `rocprofv3 --pmc`
         passes (FETCH_SIZE, WRITE_SIZE), each scaled by the reading of the
         same counter for that elementwise kernel
+    python -m paper_2608_13057_amd.measure mfma PMC_DIR TRACE_DIR --out MD ...
+        MFMA busy fraction, shader clock and executed flops of the gate/up
+        GEMM from one `rocprofv3 --pmc` pass and a kernel trace
     python -m paper_2608_13057_amd.measure snap --out MD
         the tile-aware split (TEMPO_PLAN_SNAP_TILES) against the plain one:
         M-tiles, activated slots and block time per workload and batch size
@@ -236,6 +239,109 @@ def _traffic(args):
     return 0
 
 
+def mfma_path(workload: str, m_tile: int) -> str:
+    return os.path.join(ROOT, "profiles", f"k_gemm_gateup_{workload}_m{m_tile}_mfma.md")
+
+
+def committed_mfma(workload: str, m_tile: int):
+    """The committed MFMA-counter summary of the gate/up kernel (dict), or
+    None when there is none or the stage-2 sources changed since."""
+    path = mfma_path(workload, m_tile)
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        for line in fh:
+            if line.startswith("mfma_json: "):
+                d = json.loads(line[len("mfma_json: "):])
+                return d if d.get("source_hash") == gemm_source_hash() else None
+    return None
+
+
+def _agent(d: str) -> dict:
+    for f in sorted(glob.glob(os.path.join(d, "**", "*agent_info.csv"), recursive=True)):
+        with open(f) as fh:
+            for r in csv.DictReader(fh):
+                if r.get("Name", "").startswith("gfx"):
+                    return r
+    raise SystemExit(f"no GPU agent in {d}")
+
+
+def _kernel_avg_ns(d: str, match):
+    f = glob.glob(os.path.join(d, "**", "*kernel_stats.csv"), recursive=True)
+    if not f:
+        raise SystemExit(f"no kernel_stats.csv under {d}")
+    with open(f[0]) as fh:
+        for r in csv.DictReader(fh):
+            if match(r["Name"]):
+                return float(r["AverageNs"]), r["Name"]
+    raise SystemExit("kernel not in the trace")
+
+
+def _mfma(args):
+    """MFMA utilisation of the gate/up GEMM from one rocprofv3 --pmc pass
+    (SQ_VALU_MFMA_BUSY_CYCLES per SIMD, GRBM_GUI_ACTIVE summed over the XCDs,
+    the MFMA op counters) and the kernel's mean duration from a kernel trace
+    of the same program."""
+    from . import synth
+
+    rows = _rows(args.pmc_dir)
+    ag = _agent(args.pmc_dir)
+    nxcc, nsimd = int(ag["Num_Xcc"]), int(ag["Simd_Count"])
+    busy, n = _mean_counter(rows, "SQ_VALU_MFMA_BUSY_CYCLES", _is_gateup)
+    gui, _ = _mean_counter(rows, "GRBM_GUI_ACTIVE", _is_gateup)
+    ops = 0.0
+    for c in ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_INSTS_VALU_MFMA_MOPS_F8"):
+        try:
+            ops += _mean_counter(rows, c, _is_gateup)[0]
+        except SystemExit:
+            pass
+    dur_ns, kname = _kernel_avg_ns(args.trace_dir, _is_gateup)
+    cycles = gui / nxcc  # GPU cycles of the dispatch (GRBM_GUI_ACTIVE is per XCD)
+    util = busy / (cycles * nsimd)
+    clock = cycles / dur_ns  # GHz
+    wl = synth.make_workload(args.workload)
+    executed = ops * 512
+    dt = wl.dtype
+    peak = {"bf16": 2500.0, "fp8": 5000.0, "fp8mx": 5000.0}[dt]
+    d = {"kernel": kname, "workload": args.workload, "m_tile": args.m_tile, "mfma_busy": util, "clock_ghz": clock,
+         "launch_us": dur_ns / 1e3, "executed_tflops": executed / dur_ns / 1e3,
+         "executed_frac_of_peak": executed / dur_ns / 1e3 / peak, "dispatches": n, "source_hash": gemm_source_hash()}
+    lines = [
+        f"# MFMA utilisation: gate/up GEMM, {args.workload}, M-tile {args.m_tile}",
+        "",
+        "Commands (repo root, MI355X):",
+        "",
+        "```",
+        args.command1,
+        args.command2,
+        f"python -m paper_2608_13057_amd.measure mfma {args.pmc_dir} {args.trace_dir} --workload {args.workload} "
+        f"--m-tile {args.m_tile} --out <this file>",
+        "```",
+        "",
+        f"Kernel: `{kname}` ({n} dispatches averaged; mean duration {dur_ns / 1e3:.1f} us from the kernel trace).",
+        "",
+        "| quantity | value |",
+        "|---|---|",
+        f"| SQ_VALU_MFMA_BUSY_CYCLES (sum over {nsimd} SIMDs) | {busy:.4g} |",
+        f"| GRBM_GUI_ACTIVE (sum over {nxcc} XCDs) | {gui:.4g} |",
+        f"| dispatch cycles = GRBM_GUI_ACTIVE / {nxcc} | {cycles:.4g} |",
+        f"| MFMA busy = busy / (cycles x {nsimd}) | **{util:.3f}** |",
+        f"| shader clock = cycles / duration | {clock:.2f} GHz (nominal {int(ag['Max_Engine_Clk_Fcompute']) / 1e3:.1f}) |",
+        f"| executed MFMA flops (MOPS x 512) | {executed / 1e9:.1f} GFLOP ({executed / dur_ns / 1e3:.0f} TFLOP/s, "
+        f"{executed / dur_ns / 1e3 / peak:.3f} of {peak:.0f}) |",
+        "",
+        "The busy fraction counts MFMA pipe cycles against the cycles of the dispatch at the clock the GPU ran; "
+        "executed flops include the padding rows of partly filled M-tiles, which the roofline's useful flops do not.",
+        "",
+        "mfma_json: " + json.dumps(d),
+        "",
+    ]
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+    return 0
+
+
 def _stats(args):
     f = glob.glob(os.path.join(args.dir, "**", "*kernel_stats.csv"), recursive=True)
     if not f:
@@ -365,6 +471,14 @@ def main(argv=None):
     s.add_argument("--title", default="")
     s.add_argument("--command", default="")
     s.add_argument("--note", default="")
+    mf = sub.add_parser("mfma", help="MFMA utilisation of the gate/up GEMM from a counter pass and a kernel trace")
+    mf.add_argument("pmc_dir")
+    mf.add_argument("trace_dir")
+    mf.add_argument("--workload", required=True)
+    mf.add_argument("--m-tile", type=int, required=True)
+    mf.add_argument("--out", required=True)
+    mf.add_argument("--command1", default="")
+    mf.add_argument("--command2", default="")
     n = sub.add_parser("snap", help="the tile-aware split or sampled replicas against the plain split")
     n.add_argument("--variant", choices=("snap", "sample"), default="snap")
     n.add_argument("--key", type=int, default=12345, help="generator key of the sampled variant")
@@ -377,7 +491,7 @@ def main(argv=None):
     n.add_argument("--out", required=True)
     n.add_argument("--command", default="")
     a = ap.parse_args(argv)
-    return {"run": _run, "traffic": _traffic, "stats": _stats, "snap": _snap}[a.cmd](a)
+    return {"run": _run, "traffic": _traffic, "stats": _stats, "snap": _snap, "mfma": _mfma}[a.cmd](a)
 
 
 if __name__ == "__main__":
