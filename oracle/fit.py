@@ -21,7 +21,9 @@ an empty piece never wins a point.  n* = b/beta.
 :func:`fit_restarts` -- the same alternation restarted from every
 single-breakpoint split of the points by N/G (flat iff N/G <= tau, for each
 distinct tau, and all-flat / all-linear) besides the median split, keeping the
-lowest SSE; for the tile-aware form also from the assignment of the Eq. 1 fit.
+lowest SSE; for the tile-aware form also from the assignment of the Eq. 1 fit
+and from the Eq. 1 fit itself taken as a tile-aware fit with b2 = 0 (Eq. 2
+contains Eq. 1), so the tile-aware fit never ends with a larger SSE.
 """
 from __future__ import annotations
 
@@ -56,9 +58,12 @@ def _lstsq_piece(X_rows, t_vals):
     return sol
 
 
-def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None):
+def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None, start=None):
     """Alternating-assignment fit.  Returns dict(a, b, c, beta, [b2],
-    n_star, err_mean, err_max, sse, iterations, assign)."""
+    n_star, err_mean, err_max, sse, iterations, assign).  `start`, when
+    given, is a parameter dict (a, b, c, beta, [b2]) taken as round 0: its
+    SSE competes for the lowest-SSE iterate and its larger-prediction
+    assignment is the initial one."""
     G = [float(v) for v in G]
     N = [float(v) for v in N]
     t = [float(v) for v in t]
@@ -74,6 +79,16 @@ def fit_max_affine(G, N, t, T_tiles=None, iters: int = 50, init=None):
     cf = cl = None
     it = 0
     best = None  # (sse, cf, cl, assignment that produced them, round)
+    if start is not None:
+        cf = [start["a"], start["b"]] + ([start.get("b2", 0.0)] if tile else [])
+        cl = [start["c"], start["beta"]]
+        assign, sse = [], 0.0
+        for i in range(m):
+            pf = cf[0] + cf[1] * G[i] + (cf[2] * (Tt[i] - G[i]) if tile else 0.0)
+            pl = cl[0] + cl[1] * N[i]
+            assign.append(0 if pf >= pl else 1)
+            sse += (max(pf, pl) - t[i]) ** 2
+        best = (sse, np.array(cf, np.float64), np.array(cl, np.float64), list(assign), 0)
     for it in range(1, iters + 1):
         fx, fy, lx, ly = [], [], [], []
         for i in range(m):
@@ -119,17 +134,20 @@ def fit_restarts(G, N, t, T_tiles=None, iters: int = 50):
     """fit_max_affine from the median split and from every single-breakpoint
     split by N/G (flat iff N/G <= tau over the distinct ratios, plus
     all-flat and all-linear); with tile counts also from the Eq. 1 fit's
-    assignment.  Returns the lowest-SSE result (ties: the earliest start)."""
+    assignment and from the Eq. 1 fit itself with b2 = 0.  Returns the
+    lowest-SSE result (ties: the earliest start)."""
     m = len(t)
     ratios = [float(N[i]) / float(G[i]) for i in range(m)]
-    starts = [None]
+    starts = [(None, None)]
     for tau in sorted(set(ratios)) + [-math.inf]:
-        starts.append([0 if ratios[i] <= tau else 1 for i in range(m)])
+        starts.append(([0 if ratios[i] <= tau else 1 for i in range(m)], None))
     if T_tiles is not None:
-        starts.append(fit_restarts(G, N, t, None, iters)["assign"])
+        eq1 = fit_restarts(G, N, t, None, iters)
+        starts.append((eq1["assign"], None))
+        starts.append((None, dict(eq1, b2=0.0)))
     best = None
-    for init in starts:
-        r = fit_max_affine(G, N, t, T_tiles, iters, init)
+    for init, start in starts:
+        r = fit_max_affine(G, N, t, T_tiles, iters, init, start)
         if best is None or r["sse"] < best["sse"]:
             best = r
     return best

@@ -334,8 +334,9 @@ uint32_t oracle_dispatch(int T, int T_valid, int K, int E, int S, int M, const i
 
 /* dtype: 0 = bf16 (uint16 storage), 1 = fp8 e4m3 (uint8 storage) with
  * scales, 2 = fp8 e4m3 whose scales are powers of two (UE8M0; the paper's
- * note that newer hardware requires them, Sec. 7): the same values, only the
- * re-quantisation of h picks its scale differently (below); 1 or 2
+ * note that newer hardware requires them, App. "Multi-node bring-up
+ * notes"): the same values, only the re-quantisation of h picks its scale
+ * differently (below); 1 or 2
  * fp32 scales: activations 1 x 128 along the contraction, weights 128 x 128
  * blocks (the gate/up matrix [2I, H] is blocked as one matrix). */
 static double x_at(int dtype, const void* x, const float* xs, int H, int t, int h) {

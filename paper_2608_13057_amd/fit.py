@@ -12,7 +12,8 @@ calibration fit.
   regressor rows has slope 0 and the mean as intercept; an empty piece never
   wins a point.  fit_restarts repeats the alternation from every
   single-breakpoint split by N/G (and, for Eq. 2, from the Eq. 1 fit's
-  assignment) and keeps the lowest SSE.
+  assignment and from the Eq. 1 fit itself with b2 = 0, which Eq. 2
+  contains, so Eq. 2 never ends with a larger SSE) and keeps the lowest SSE.
 * degenerate(): a fit whose parameters are not a usable profile (a negative
   or undefined a, b, c, beta or b2, or an Eq. 2 fit worse than Eq. 1) is
   reported as such rather than tabulated (the paper reports a negative fitted
@@ -50,10 +51,12 @@ def _ls(X: np.ndarray, y: np.ndarray):
     return np.linalg.lstsq(X, y, rcond=None)[0]
 
 
-def fit(G, N, t, T=None, iters: int = 50, init=None) -> dict:
+def fit(G, N, t, T=None, iters: int = 50, init=None, start: dict | None = None) -> dict:
     """Alternating-assignment fit of Eq. 1 (or Eq. 2 when tile counts T are
     given).  Returns a, b, c, beta, (b2), n_star, err_mean, err_max, sse,
-    iterations, flat (boolean assignment)."""
+    iterations, flat (boolean assignment).  `start` (a, b, c, beta, [b2])
+    is a round-0 iterate: it competes for the lowest SSE and its
+    larger-piece assignment starts the alternation."""
     G = np.asarray(G, np.float64)
     N = np.asarray(N, np.float64)
     t = np.asarray(t, np.float64)
@@ -65,6 +68,12 @@ def fit(G, N, t, T=None, iters: int = 50, init=None) -> dict:
     cf = cl = None
     it = 0
     best = None  # the lowest-SSE iterate: (sse, cf, cl, assignment)
+    if start is not None:
+        cf = np.array([start["a"], start["b"]] + ([start.get("b2") or 0.0] if tile else []), np.float64)
+        cl = np.array([start["c"], start["beta"]], np.float64)
+        pf, pl = Xf @ cf, Xl @ cl
+        flat = pf >= pl
+        best = (float(((np.maximum(pf, pl) - t) ** 2).sum()), cf, cl, flat)
     for it in range(1, iters + 1):
         cf = _ls(Xf[flat], t[flat])
         cl = _ls(Xl[~flat], t[~flat])
@@ -92,17 +101,19 @@ def fit(G, N, t, T=None, iters: int = 50, init=None) -> dict:
 def fit_restarts(G, N, t, T=None, iters: int = 50) -> dict:
     """fit() from the median split and from every single-breakpoint split by
     N/G (flat iff N/G <= tau over the distinct ratios, plus all-flat and
-    all-linear); for Eq. 2 also from the Eq. 1 fit's assignment.  The
-    lowest-SSE result (ties: the earliest start)."""
+    all-linear); for Eq. 2 also from the Eq. 1 fit's assignment and from the
+    Eq. 1 fit with b2 = 0.  The lowest-SSE result (ties: the earliest
+    start)."""
     G = np.asarray(G, np.float64)
     N = np.asarray(N, np.float64)
     ratio = N / G
-    starts = [None] + [ratio <= tau for tau in np.unique(ratio)] + [np.zeros(len(ratio), bool)]
+    starts = [(None, None)] + [(ratio <= tau, None) for tau in np.unique(ratio)] + [(np.zeros(len(ratio), bool), None)]
     if T is not None:
-        starts.append(fit_restarts(G, N, t, None, iters)["flat"])
+        e1 = fit_restarts(G, N, t, None, iters)
+        starts += [(e1["flat"], None), (None, dict(e1, b2=0.0))]
     best = None
-    for init in starts:
-        r = fit(G, N, t, T, iters, init)
+    for init, start in starts:
+        r = fit(G, N, t, T, iters, init, start)
         if best is None or r["sse"] < best["sse"]:
             best = r
     return best

@@ -1,4 +1,4 @@
-"""The tempo_fast dispatch solver (Sec. 3.4) for the fixed-charge makespan
+"""The tempo_fast dispatch solver (Sec. 4.2) for the fixed-charge makespan
 problem of Sec. 3.1:
 
     min over integer shares x[e, g] >= 0 with sum_g x[e, g] = n_e, supported

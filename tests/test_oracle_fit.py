@@ -158,3 +158,53 @@ def test_run_keeps_its_lowest_sse_iterate():
         if prev is not None:
             assert r["sse"] <= prev + 1e-9
         prev = r["sse"]
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_tile_aware_fit_never_worse_than_eq1(seed):
+    """Eq. 2 contains Eq. 1 (b2 = 0), so its restarted fit, which also starts
+    from the Eq. 1 fit, never ends with a larger SSE.  Unless that start is
+    the winner (not a least-squares fit of any assignment), it never beats
+    the exhaustive optimum over Eq. 2's assignments either."""
+    G, N, t = _mostly_flat(seed)
+    rng = np.random.default_rng(100 + seed)
+    T = G * np.ceil(N / G / 64.0) + rng.integers(0, 2, len(G))  # tile counts with some noise
+    e1 = fit.fit_restarts(G, N, t)
+    e2 = fit.fit_restarts(G, N, t, T)
+    assert e2["sse"] <= e1["sse"] * (1 + 1e-12)
+    # brute force over the 2^m assignments with the tile regressor in the flat piece
+    m = len(t)
+    best = np.inf
+    for mask in range(1 << m):
+        lin = np.array([(mask >> i) & 1 for i in range(m)], bool)
+        pf = np.full(m, -np.inf)
+        pl = np.full(m, -np.inf)
+        if (~lin).any():
+            X = np.stack([np.ones(m), G, T - G], 1)[~lin]
+            cf = np.linalg.lstsq(X, t[~lin], rcond=None)[0] if len({tuple(r) for r in X.tolist()}) >= 2 else \
+                np.array([t[~lin].mean(), 0.0, 0.0])
+            pf = cf[0] + cf[1] * G + cf[2] * (T - G)
+        if lin.any():
+            X = np.stack([np.ones(m), N], 1)[lin]
+            cl = np.linalg.lstsq(X, t[lin], rcond=None)[0] if len({tuple(r) for r in X.tolist()}) >= 2 else \
+                np.array([t[lin].mean(), 0.0])
+            pl = cl[0] + cl[1] * N
+        best = min(best, float(((np.maximum(pf, pl) - t) ** 2).sum()))
+    if (e2["a"], e2["b"], e2["c"], e2["beta"], e2["b2"]) != (e1["a"], e1["b"], e1["c"], e1["beta"], 0.0):
+        assert e2["sse"] >= best * (1 - 1e-9) - 1e-9
+
+
+def test_start_parameters_are_round_zero():
+    """With no alternation rounds the fit returns the start parameters, and
+    its SSE is that of the max-affine prediction written out by hand."""
+    G = np.array([1.0, 2.0, 4.0, 8.0])
+    N = np.array([4.0, 900.0, 40.0, 4000.0])
+    T = np.array([1.0, 8.0, 4.0, 64.0])
+    t = np.array([50.0, 80.0, 70.0, 260.0])
+    p = dict(a=40.0, b=5.0, c=20.0, beta=0.05, b2=1.0)
+    r = fit.fit_max_affine(G, N, t, T, iters=0, start=p)
+    assert (r["a"], r["b"], r["c"], r["beta"], r["b2"]) == (40.0, 5.0, 20.0, 0.05, 1.0)
+    # flat a + bG + b2 (T - G): 45, 56, 60, 136; linear c + beta N: 20.2, 65, 22, 220
+    pred = np.array([45.0, 65.0, 60.0, 220.0])
+    assert r["sse"] == pytest.approx(float(((pred - t) ** 2).sum()))
+    assert r["assign"] == [0, 1, 0, 1]

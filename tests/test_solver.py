@@ -1,4 +1,4 @@
-"""Pins for the tempo_fast solver (Sec. 3.4) and its candidates, on the CPU:
+"""Pins for the tempo_fast solver (Sec. 4.2) and its candidates, on the CPU:
 feasibility, the ensemble's guarantee against the token LP, Theorem 1's
 additive bound for the round-robin placement, the beta -> 0 limit (Lemma 2)
 against a brute-force semi-matching, near-optimality against a MILP optimum
