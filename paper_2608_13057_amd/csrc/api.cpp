@@ -202,7 +202,7 @@ int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* di
   hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t e = shape->dtype == TEMPO_BF16
                            ? launch_experts_bf16(*shape, *disp, *weights, nullptr, y_perm, ws, L, false, nullptr, st)
-                           : launch_experts_fp8(*shape, *disp, *weights, nullptr, y_perm, ws, L, false, nullptr, st);
+                           : launch_experts_fp8(*shape, *disp, *weights, nullptr, nullptr, y_perm, ws, L, false, nullptr, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   return dev_status(e);
 }
@@ -239,15 +239,17 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   auto mark = [&](int i) { return !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!mark(0)) return TEMPO_EDEVICE;
-  // decode-sized batches: the gate/up GEMM gathers the activation rows itself
-  // and x_perm stays unwritten; otherwise stage 1 permutes them into x_perm
+  // decode-sized batches and the large-tile kernels: stage 2 gathers the
+  // activation rows (and fp8 scales) itself and x_perm (x_perm_scale) stays
+  // unwritten; otherwise stage 1 permutes them into x_perm
   const bool gemm_gathers = experts_gather_rows(*shape, L);
   const void* x_rows = gemm_gathers ? x : nullptr;
   hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, !gemm_gathers, st);
   if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
   e = shape->dtype == TEMPO_BF16
           ? launch_experts_bf16(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev + 2, st)
-          : launch_experts_fp8(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev + 2, st);
+          : launch_experts_fp8(*shape, *disp, *weights, x_rows, gemm_gathers ? x_scale : nullptr, y_perm, ws, L,
+                                       timing, ev + 2, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   if (e != hipSuccess || !mark(5)) return TEMPO_EDEVICE;
   e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,

@@ -20,8 +20,9 @@
 // give the offset of earlier wavefronts and a running count the offset of
 // earlier rounds.  No atomics decide positions.
 //
-// One launch for decode-sized bf16 batches whose rows stage 2 gathers itself
-// (k_dispatch_small: one workgroup does all of it); otherwise two launches
+// One launch for decode-sized batches whose rows (and fp8 scales) stage 2
+// gathers itself (k_dispatch_small: one workgroup does all of it); otherwise
+// two launches
 // (three for large batches, see k_scan); no block ever waits for or signals
 // another (device-scope fences write back L2 on this multi-XCD chip and cost
 // more than the work):
@@ -37,7 +38,8 @@
 //            pairs rank -> slot -> row and writes the index outputs and
 //            copies the rows, one wavefront per row with every load in
 //            flight (the whole forward skips the copy: its gate/up GEMM reads
-//            the activation rows through row_token directly).
+//            the activation rows and their scales through row_token
+//            directly).
 // Global loads are issued before the values are needed: at one wavefront per
 // SIMD every exposed memory latency (~0.3-0.5 us) adds up.
 #include <algorithm>
@@ -1013,19 +1015,19 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
-  // one workgroup for decode-sized bf16 batches whose rows stage 2 gathers;
-  // sampled replicas always take this path (then a row-copy launch when
-  // x_perm or the fp8 scales are needed)
+  // one workgroup for decode-sized batches whose rows (and fp8 scales) stage
+  // 2 gathers itself; sampled replicas always take this path (then a
+  // row-copy launch when x_perm and the fp8 scales are asked for)
   const bool small = P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE;
   if (sample && !dispatch_sample_supported(s)) return hipErrorNotSupported;
-  if (sample || (small && s.dtype == TEMPO_BF16 && !gather_rows)) {
+  if (sample || (small && !gather_rows)) {
     const int KW = sample ? s.S : s.E;
     const size_t lds = (size_t)kSmallWaves * KW * 8 + (size_t)(kSmallWaves * KW + 5 * s.E) * sizeof(int32_t);
     hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
                        s.m_tile, snap, sample, plan.seed, L.row_cap, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, hdr, timing ? 1 : 0, t0, t1);
-    if (gather_rows || s.dtype != TEMPO_BF16) {
+    if (gather_rows) {
       const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
       if (s.dtype == TEMPO_BF16)
         hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
@@ -1053,7 +1055,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   // row and scale copies: inside k_place for small batches; for large ones a
   // row-parallel launch after it (a placing block holds a few dozen rows, too
   // few loads in flight)
-  const int copies = large ? 0 : (gather_rows ? 1 : 0) | (s.dtype != TEMPO_BF16 ? 2 : 0);
+  const int copies = large || !gather_rows ? 0 : 1 | (s.dtype != TEMPO_BF16 ? 2 : 0);
   const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
   auto launch = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, snap, s.H, L.row_cap,
@@ -1069,7 +1071,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
     if (large) launch(k_place<1, kPlaceChunkLarge>);
     else launch(k_place<1, kPlaceChunk>);
   }
-  if (large && (gather_rows || s.dtype != TEMPO_BF16)) {
+  if (large && gather_rows) {
     const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
     if (s.dtype == TEMPO_BF16)
       hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,

@@ -63,9 +63,10 @@ __device__ __forceinline__ uint32_t ue8m0_of(float s) { return (__float_as_uint(
 
 // The activation rows of every live 256-row tile in the packed fp8 layout,
 // with their scale exponents, from token rows (gather: row r is token
-// row_token[r] of A) or from permuted rows (row r of A); the scales of row r
-// are A_scale[kt][row_cap] (block-major, as stage 1 writes them in both
-// cases); padding rows are zero with exponent 127 (scale 1).  One (tile, step) block per workgroup of a fixed
+// row_token[r] of A) or from permuted rows (row r of A); the scales are the
+// token rows' own, A_scale[token][K/128], when gathering, else the
+// block-major A_scale[kt][row_cap] of stage 1; padding rows are zero with
+// exponent 127 (scale 1).  One (tile, step) block per workgroup of a fixed
 // grid at a time: wavefront w writes pieces 2w and 2w + 1 (1 KB per store
 // instruction), thread t the exponent of row t.
 __global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict__ A, const float* __restrict__ A_scale,
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict_
     const int row = tile * F8_M + tid;
     const int tok = row_token[row];
     uint32_t e = 127;
-    if (tok >= 0) e = ue8m0_of(A_scale[(size_t)kt * row_cap + row]);
+    if (tok >= 0) e = ue8m0_of(gather ? A_scale[(size_t)tok * KT + kt] : A_scale[(size_t)kt * row_cap + row]);
     out_sc[(size_t)tile * f8_tile_scale_bytes(K) + (size_t)kt * 256 + (tid & 31) * 8 + (tid >> 5)] = (uint8_t)e;
   }
 }
@@ -465,12 +466,12 @@ size_t experts_big_f8_pack_bytes(const tempo_moe_shape& s, int row_cap) {
 }
 
 // Both GEMMs of stage 2 for UE8M0 fp8 with 256 x 256 items.  The activation
-// rows come from x_rows (token rows, gathered through row_token) or, if that
-// is null, from the permuted rows in x_perm; their scales from the
-// block-major x_perm_scale of stage 1.
+// rows come from x_rows (token rows, gathered through row_token, with their
+// scales x_rows_scale [tokens][H/128]) or, if that is null, from the permuted
+// rows in x_perm with the block-major x_perm_scale of stage 1.
 hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                                 const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
-                                 const hipEvent_t* ev, hipStream_t st) {
+                                 const void* x_rows, const float* x_rows_scale, void* y_perm, char* ws,
+                                 const Layout& L, bool timing, const hipEvent_t* ev, hipStream_t st) {
   const int grid = persistent_grid(1);
   const int max_tiles = L.row_cap / F8_M;
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
@@ -478,7 +479,7 @@ hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_
   uint8_t* apack_sc = apack + (size_t)L.row_cap * s.H;
   const bool gather = x_rows != nullptr;
   hipLaunchKernelGGL(k_pack_rows_f8, dim3(persistent_grid(4)), dim3(256), 0, st,
-                     static_cast<const uint8_t*>(gather ? x_rows : d.x_perm), d.x_perm_scale,
+                     static_cast<const uint8_t*>(gather ? x_rows : d.x_perm), gather ? x_rows_scale : d.x_perm_scale,
                      gather ? 1 : 0, L.row_cap, d.row_token, d.slot_offsets, s.S, max_tiles, s.H, apack, apack_sc);
 
   F8Args a{};

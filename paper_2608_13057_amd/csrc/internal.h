@@ -53,8 +53,8 @@ Layout make_layout(const tempo_moe_shape& s);
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---- launchers (stream-ordered, no synchronisation) ----
-// gather_rows = false leaves x_perm unwritten (stage 2 then gathers through
-// row_token; x_perm_scale is still written for fp8).
+// gather_rows = false leaves x_perm and x_perm_scale unwritten (stage 2 then
+// gathers the rows and their scales through row_token).
 // Whether sampled replicas (TEMPO_PLAN_SAMPLE) are available for this shape.
 bool dispatch_sample_supported(const tempo_moe_shape& s);
 
@@ -64,15 +64,17 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
 
 // ev: null, or 3 events (each nullable) recorded after the gate/up GEMM
 // kernel, after the gate/up step and after the down GEMM kernel.
-// x_rows: null -> the gate/up GEMM reads d.x_perm; otherwise it reads the
-// activation rows x_rows[row_token[row]] (x_rows = the unpermuted x).
+// x_rows: null -> the gate/up GEMM reads d.x_perm (and for fp8
+// d.x_perm_scale); otherwise it reads the activation rows
+// x_rows[row_token[row]] (x_rows = the unpermuted x) and for fp8 their
+// scales x_rows_scale[row_token[row]] ([tokens][H/128] fp32).
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                                const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
                                const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                              const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
-                              const hipEvent_t* ev, hipStream_t st);
+                              const void* x_rows, const float* x_rows_scale, void* y_perm, char* ws, const Layout& L,
+                              bool timing, const hipEvent_t* ev, hipStream_t st);
 
 // bf16 with 256-row M-tiles (and H a multiple of 256): both GEMMs as 256 x 256
 // items on MFMA-blocked wavefronts (the large-tile kernel), with the
@@ -92,8 +94,8 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
 bool experts_big_f8_supported(const tempo_moe_shape& s);
 size_t experts_big_f8_pack_bytes(const tempo_moe_shape& s, int row_cap);
 hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                                 const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
-                                 const hipEvent_t* ev, hipStream_t st);
+                                 const void* x_rows, const float* x_rows_scale, void* y_perm, char* ws,
+                                 const Layout& L, bool timing, const hipEvent_t* ev, hipStream_t st);
 
 hipError_t launch_combine(const tempo_moe_shape& s, const int32_t* pair_row, const float* topk_w, const void* y_perm,
                           void* y, const int32_t* slot_counts, const uint64_t* t0, const uint64_t* t1,
