@@ -290,11 +290,12 @@ int tempo_moe_combine(const tempo_moe_shape* shape, const int32_t* pair_row, con
 
 /*
  * Stages 1-3 on one stream.  disp receives the stage-1 outputs (caller
- * buffers as for tempo_moe_dispatch), except that x_perm and x_perm_scale
- * are left unwritten where stage 2 gathers the token rows and their scales
- * itself (decode-sized batches, and the 256-row large-tile kernels of bf16
- * and UE8M0 fp8, whose GEMMs read the rows packed in MFMA operand order in
- * the workspace); y_perm lives in the workspace.
+ * buffers as for tempo_moe_dispatch), except that x_perm is left unwritten
+ * where stage 2 gathers the token rows itself (decode-sized batches, and
+ * the 256-row large-tile kernels of bf16 and UE8M0 fp8, whose GEMMs read
+ * the rows packed in MFMA operand order in the workspace), and so is
+ * x_perm_scale for the large-tile fp8 kernel, which packs the token rows'
+ * own scales; y_perm lives in the workspace.
  * slot_time_ns [S] uint64 device, nullable: per slot, the span from the
  * first stage-2 tile that started on it to the last that ended, measured
  * with the GPU's 100 MHz real-time counter (0 for slots with c_s = 0).

@@ -185,7 +185,7 @@ int tempo_moe_dispatch(const tempo_moe_shape* shape, const tempo_plan* plan, con
   const Layout L = make_layout(*shape);
   if (workspace_bytes < L.total) return TEMPO_EWORKSPACE;
   return dev_status(launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *out, static_cast<char*>(workspace), L,
-                                    false, true, static_cast<hipStream_t>(stream)));
+                                    false, true, true, static_cast<hipStream_t>(stream)));
 }
 
 int tempo_moe_experts(const tempo_moe_shape* shape, const tempo_dispatch_out* disp,
@@ -240,15 +240,18 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
   if (!experts_supported(*shape)) return TEMPO_EUNSUPPORTED;
   if (!mark(0)) return TEMPO_EDEVICE;
   // decode-sized batches and the large-tile kernels: stage 2 gathers the
-  // activation rows (and fp8 scales) itself and x_perm (x_perm_scale) stays
-  // unwritten; otherwise stage 1 permutes them into x_perm
+  // activation rows itself and x_perm stays unwritten (the large-tile fp8
+  // kernel also reads the token rows' scales); otherwise stage 1 permutes the
+  // rows into x_perm
   const bool gemm_gathers = experts_gather_rows(*shape, L);
+  const bool own_scales = gemm_gathers && shape->dtype != TEMPO_BF16 && experts_reads_token_scales(*shape);
   const void* x_rows = gemm_gathers ? x : nullptr;
-  hipError_t e = launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, !gemm_gathers, st);
+  hipError_t e =
+      launch_dispatch(*shape, *plan, topk_ids, x, x_scale, *disp, ws, L, timing, !gemm_gathers, !own_scales, st);
   if (e != hipSuccess || !mark(1)) return TEMPO_EDEVICE;
   e = shape->dtype == TEMPO_BF16
           ? launch_experts_bf16(*shape, *disp, *weights, x_rows, y_perm, ws, L, timing, ev + 2, st)
-          : launch_experts_fp8(*shape, *disp, *weights, x_rows, gemm_gathers ? x_scale : nullptr, y_perm, ws, L,
+          : launch_experts_fp8(*shape, *disp, *weights, x_rows, own_scales ? x_scale : nullptr, y_perm, ws, L,
                                        timing, ev + 2, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
   if (e != hipSuccess || !mark(5)) return TEMPO_EDEVICE;

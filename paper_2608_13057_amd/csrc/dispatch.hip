@@ -21,8 +21,8 @@
 // earlier rounds.  No atomics decide positions.
 //
 // One launch for decode-sized batches whose rows (and fp8 scales) stage 2
-// gathers itself (k_dispatch_small: one workgroup does all of it); otherwise
-// two launches
+// reads from the token rows (k_dispatch_small: one workgroup does all of it);
+// otherwise two launches
 // (three for large batches, see k_scan); no block ever waits for or signals
 // another (device-scope fences write back L2 on this multi-XCD chip and cost
 // more than the work):
@@ -37,9 +37,9 @@
 //            per-expert / per-slot outputs and the header), then maps its
 //            pairs rank -> slot -> row and writes the index outputs and
 //            copies the rows, one wavefront per row with every load in
-//            flight (the whole forward skips the copy: its gate/up GEMM reads
-//            the activation rows and their scales through row_token
-//            directly).
+//            flight (the whole forward skips what stage 2 reads through
+//            row_token directly: the rows for decode-sized batches, rows and
+//            fp8 scales for the large-tile kernels).
 // Global loads are issued before the values are needed: at one wavefront per
 // SIMD every exposed memory latency (~0.3-0.5 us) adds up.
 #include <algorithm>
@@ -961,8 +961,9 @@ __global__ __launch_bounds__(kSmallWaves * 64) void k_dispatch_small(
 }
 
 // Row copies after k_dispatch_small: the token rows into x_perm (when asked)
-// and, for fp8, their activation scales into x_perm_scale (block-major), for
-// the rows in use (slot_offsets[S]); one wavefront per row.
+// and, for fp8, their activation scales into x_perm_scale (block-major; when
+// it is not null), for the rows in use (slot_offsets[S]); one wavefront per
+// row.
 template <int ESIZE>
 __global__ __launch_bounds__(256) void k_gather_rows(const int32_t* __restrict__ row_token,
                                                      const int32_t* __restrict__ slot_offsets, int S, int H, int row_cap,
@@ -975,7 +976,7 @@ __global__ __launch_bounds__(256) void k_gather_rows(const int32_t* __restrict__
   for (int row = blockIdx.x * 4 + (threadIdx.x >> 6); row < used; row += gridDim.x * 4) {
     const int tok = row_token[row];
     if (tok < 0) continue;
-    if (ESIZE == 1) {
+    if (ESIZE == 1 && x_perm_scale) {
       const int ns = H / 128;
       for (int i = lane; i < ns; i += 64) x_perm_scale[(size_t)i * row_cap + row] = x_scale[(size_t)tok * ns + i];
     }
@@ -1002,7 +1003,7 @@ bool dispatch_sample_supported(const tempo_moe_shape& s) {
 
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids, const void* x,
                            const float* x_scale, const tempo_dispatch_out& out, char* ws, const Layout& L,
-                           bool timing, bool gather_rows, hipStream_t st) {
+                           bool timing, bool copy_rows, bool copy_scales, hipStream_t st) {
   const int P = s.T * s.K, Pv = s.T_valid * s.K;
   const int snap = (plan.flags & TEMPO_PLAN_SNAP_TILES) ? 1 : 0;
   const int sample = (plan.flags & TEMPO_PLAN_SAMPLE) ? 1 : 0;
@@ -1015,28 +1016,30 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   uint64_t* t1 = reinterpret_cast<uint64_t*>(ws + L.slot_t1);
   uint32_t* hdr = reinterpret_cast<uint32_t*>(ws + L.header);
 
+  copy_scales = copy_scales && s.dtype != TEMPO_BF16;
+  float* const xps = copy_scales ? out.x_perm_scale : nullptr;
   // one workgroup for decode-sized batches whose rows (and fp8 scales) stage
-  // 2 gathers itself; sampled replicas always take this path (then a
-  // row-copy launch when x_perm and the fp8 scales are asked for)
+  // 2 reads from the token rows; sampled replicas always take this path
+  // (then a row-copy launch for what is asked for)
   const bool small = P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE;
   if (sample && !dispatch_sample_supported(s)) return hipErrorNotSupported;
-  if (sample || (small && !gather_rows)) {
+  if (sample || (small && !copy_rows && !copy_scales)) {
     const int KW = sample ? s.S : s.E;
     const size_t lds = (size_t)kSmallWaves * KW * 8 + (size_t)(kSmallWaves * KW + 5 * s.E) * sizeof(int32_t);
     hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
                        s.m_tile, snap, sample, plan.seed, L.row_cap, plan.slot_expert,
                        plan.slot_weight, plan.remote_weight, plan.remote_replicas, out.expert_counts, out.cum_counts,
                        out.slot_counts, out.slot_offsets, out.pair_row, out.row_token, hdr, timing ? 1 : 0, t0, t1);
-    if (gather_rows) {
+    if (copy_rows || copy_scales) {
       const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
       if (s.dtype == TEMPO_BF16)
         hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
-                           L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
-                           static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                           L.row_cap, copy_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                           static_cast<uint8_t*>(out.x_perm), xps);
       else
         hipLaunchKernelGGL(k_gather_rows<1>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
-                           L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
-                           static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                           L.row_cap, copy_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                           static_cast<uint8_t*>(out.x_perm), xps);
     }
     return hipGetLastError();
   }
@@ -1055,7 +1058,7 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
   // row and scale copies: inside k_place for small batches; for large ones a
   // row-parallel launch after it (a placing block holds a few dozen rows, too
   // few loads in flight)
-  const int copies = large || !gather_rows ? 0 : 1 | (s.dtype != TEMPO_BF16 ? 2 : 0);
+  const int copies = large ? 0 : (copy_rows ? 1 : 0) | (copy_scales ? 2 : 0);
   const size_t lds = (size_t)3 * s.E * sizeof(int32_t);
   auto launch = [&](auto kern) {
     hipLaunchKernelGGL(kern, dim3(nb), dim3(256), lds, st, topk_ids, P, Pv, s.K, s.E, s.S, s.m_tile, snap, s.H, L.row_cap,
@@ -1071,16 +1074,16 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
     if (large) launch(k_place<1, kPlaceChunkLarge>);
     else launch(k_place<1, kPlaceChunk>);
   }
-  if (large && gather_rows) {
+  if (large && (copy_rows || copy_scales)) {
     const int grid = std::min(ceil_div(L.row_cap, 4), persistent_grid(8));
     if (s.dtype == TEMPO_BF16)
       hipLaunchKernelGGL(k_gather_rows<2>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
-                         L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
-                         static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                         L.row_cap, copy_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                         static_cast<uint8_t*>(out.x_perm), xps);
     else
       hipLaunchKernelGGL(k_gather_rows<1>, dim3(grid), dim3(256), 0, st, out.row_token, out.slot_offsets, s.S, s.H,
-                         L.row_cap, gather_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
-                         static_cast<uint8_t*>(out.x_perm), out.x_perm_scale);
+                         L.row_cap, copy_rows ? 1 : 0, static_cast<const uint8_t*>(x), x_scale,
+                         static_cast<uint8_t*>(out.x_perm), xps);
   }
   return hipGetLastError();
 }

@@ -66,8 +66,6 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
 bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L) {
   // the large-tile kernels pack the token rows themselves
   if (experts_big_supported(s) || experts_big_f8_supported(s)) return true;
-  // the fp8 stream-K GEMM gathers row scales with tiles of up to 192 rows
-  if (s.dtype != TEMPO_BF16 && s.m_tile > 192) return false;
   // upper bound of the M-tiles one workgroup range of the gate/up GEMM spans
   const int grid = persistent_grid(1);
   const int NB = s.I / 64;

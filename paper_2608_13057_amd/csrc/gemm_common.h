@@ -65,21 +65,6 @@ __device__ __forceinline__ void lds_dma16s(const void* sbase, uint32_t voff, uin
       : "memory", "m0");
 }
 
-// One dword per lane (global address = sbase + voff) into 4 consecutive LDS
-// bytes per lane from lds_addr: a gather of 64 scattered words.
-__device__ __forceinline__ void lds_dma4s(const void* sbase, uint32_t voff, uint32_t lds_addr) {
-  const uint64_t b = (uint64_t)(uintptr_t)sbase;
-  const uint64_t bu = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(b >> 32)) << 32) |
-                      (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)b);
-  const uint32_t l = __builtin_amdgcn_readfirstlane(lds_addr);
-  asm volatile(
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dword %0, %1" ::"v"(voff),
-      "s"(bu), "s"(l)
-      : "memory", "m0");
-}
-
 // LDS byte address of a shared-memory pointer (the low 32 bits of its
 // generic address).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
@@ -102,11 +87,7 @@ enum SlotField : int { kFieldW13 = 0, kFieldW13Scale = 1, kFieldW2 = 2, kFieldW2
 __device__ __forceinline__ const char* slot_tensor(const char* base, size_t per_slot, const uint64_t* table, int field,
                                                    int s) {
   if (!table) return base + (size_t)s * per_slot;
-  const uint64_t a = (uint64_t)(uintptr_t)(table + (size_t)s * 4 + field);
-  // (the address is uniform; read through the first lane so that it sits in
-  // scalar registers whatever the compiler proves about it)
-  const uint64_t e = ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(a >> 32)) << 32) |
-                     (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)a);
+  const uint64_t* e = table + (size_t)s * 4 + field;
   uint64_t v;
   asm volatile("s_load_dwordx2 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(v) : "s"(e) : "memory");
   return reinterpret_cast<const char*>(v);

@@ -57,9 +57,8 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
 
 template <int BM, bool MX>
 hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
-                     const void* x_rows, const float* x_rows_scale, void* y_perm, char* ws, const Layout& L,
-                     bool timing, const hipEvent_t* ev, hipStream_t st) {
-  if (BM > 192 && x_rows) return hipErrorNotSupported;  // no scale gathering with 256-row tiles
+                     const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing, const hipEvent_t* ev,
+                     hipStream_t st) {
   const int grid = persistent_grid(1);
   GemmArgs a{};
   a.as_ld = L.row_cap;
@@ -80,7 +79,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   GemmArgs gu = a;
   gu.A = static_cast<const char*>(x_rows ? x_rows : d.x_perm);
   gu.row_src = x_rows ? d.row_token : nullptr;
-  gu.As = x_rows ? x_rows_scale : d.x_perm_scale;
+  gu.As = d.x_perm_scale;
   gu.W = static_cast<const char*>(w.w13);
   gu.wtab = reinterpret_cast<const uint64_t*>(w.slot_table);
   gu.wfield = kFieldW13;
@@ -123,21 +122,24 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
 
 bool experts_supported(const tempo_moe_shape&) { return true; }
 
+bool experts_reads_token_scales(const tempo_moe_shape& s) { return experts_big_f8_supported(s); }
+
 hipError_t launch_experts_fp8(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                               const void* x_rows, const float* x_rows_scale, void* y_perm, char* ws, const Layout& L,
                               bool timing, const hipEvent_t* ev, hipStream_t st) {
   if (s.dtype == TEMPO_FP8_E4M3_UE8M0) {
-    if (experts_big_f8_supported(s)) return launch_experts_big_f8(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-    if (s.m_tile == 128) return launch_bm<128, true>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-    if (s.m_tile == 64) return launch_bm<64, true>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-    if (s.m_tile == 256) return launch_bm<256, true>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-    if (s.m_tile == 192) return launch_bm<192, true>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
+    if (experts_big_f8_supported(s))
+      return launch_experts_big_f8(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 128) return launch_bm<128, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 64) return launch_bm<64, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 256) return launch_bm<256, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+    if (s.m_tile == 192) return launch_bm<192, true>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
     return hipErrorInvalidValue;
   }
-  if (s.m_tile == 128) return launch_bm<128, false>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 64) return launch_bm<64, false>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 256) return launch_bm<256, false>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
-  if (s.m_tile == 192) return launch_bm<192, false>(s, d, w, x_rows, x_rows_scale, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 128) return launch_bm<128, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 64) return launch_bm<64, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 256) return launch_bm<256, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
+  if (s.m_tile == 192) return launch_bm<192, false>(s, d, w, x_rows, y_perm, ws, L, timing, ev, st);
   return hipErrorInvalidValue;
 }
 

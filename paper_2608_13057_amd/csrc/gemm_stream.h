@@ -86,8 +86,7 @@ typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
 struct GemmArgs {
   const char* A;            // activation rows (row_src == null: permuted rows; else token rows)
   const int32_t* row_src;   // null, or [row_cap] token of each permuted row (-1 = padding)
-  const float* As;          // fp8: activation scales, block-major [Kd/128][as_ld]; with
-                            // row_src, the token rows' own scales [tokens][Kd/128]
+  const float* As;          // fp8: activation scales, block-major [Kd/128][as_ld]
   int as_ld;
   const char* W;            // packed weights (tempo_moe_pack_weights)
   size_t w_slot_bytes;
@@ -277,9 +276,6 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   constexpr int STG_ROWS = BM % 128 == 0 ? 128 : 64;
   constexpr int STG_BYTES = STG_ROWS * ROW_OUT;
   constexpr int NROWT = nrowt_of(BM);
-  // fp8 scales gathered through row_token (up to 192-row tiles; with 256 the
-  // host has stage 1 permute rows and scales, the registers being spent)
-  constexpr bool SCALE_GATHER = FP8 && BM <= 192;
 
   __shared__ __attribute__((aligned(1024))) char ring[NSL * SLOT_MAX];
   __shared__ __attribute__((aligned(16))) char stg[STG_BYTES];
@@ -349,7 +345,6 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   const char* as_base = nullptr;
   const char* ws_base = nullptr;
   uint32_t a_voff[AG];
-  int is_tt = 0, is_row0 = 0;  // fp8 with gathering: the item's row table and first row
   int iss = 0, is_slot = 0;
   i32x4 wr[DR][4];   // weight operands of the steps in flight
 
@@ -385,11 +380,9 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
       a_voff[j] = row * a_row_bytes + gchunk * 16;
     }
     if (FP8) {
+      as_base = reinterpret_cast<const char*>(p.As + row0);
       ws_base = slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
                 (size_t)nb * g.KT * 16;
-      as_base = reinterpret_cast<const char*>(gather ? p.As : p.As + row0);
-      is_tt = tt;
-      is_row0 = row0;
     }
     is_new = false;
   };
@@ -416,25 +409,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
         }
         if (FP8) {
           if (wave == 3) {
-            if (SCALE_GATHER && gather) {  // each lane the scale of its row: BM / 64 dword gathers
-#pragma unroll
-              for (int j = 0; j < BM / 64; j++) {
-                const int r = min(j * 64 + lane, is_nvalid - 1);
-                int v;
-                if (is_tt < NROWT) {
-                  v = s_rows[is_tt][r];
-                } else {  // not reached when the host chose gathering (as above)
-                  asm volatile("global_load_dword %0, %1, off\n\ts_waitcnt vmcnt(0)"
-                               : "=v"(v)
-                               : "v"(p.row_src + is_row0 + r)
-                               : "memory");
-                }
-                lds_dma4s(as_base + is_kt * 4, (uint32_t)max(v, 0) * (uint32_t)(p.Kd / 128) * 4u,
-                          sl + A_BYTES + j * 256);
-              }
-            } else if (lane < BM / 4) {
-              lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES);
-            }
+            if (lane < BM / 4) lds_dma16s(as_base + (size_t)is_kt * p.as_ld * 4, lane * 16, sl + A_BYTES);
           } else if (wave == 2) {
             if (lane == 0) lds_dma16s(ws_base + is_kt * 16, 0, sl + A_BYTES + BM * 4);
           }

@@ -53,21 +53,24 @@ Layout make_layout(const tempo_moe_shape& s);
 inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
 
 // ---- launchers (stream-ordered, no synchronisation) ----
-// gather_rows = false leaves x_perm and x_perm_scale unwritten (stage 2 then
-// gathers the rows and their scales through row_token).
+// copy_rows = false leaves x_perm unwritten, copy_scales = false (or bf16)
+// x_perm_scale (stage 2 then reads them through row_token).
 // Whether sampled replicas (TEMPO_PLAN_SAMPLE) are available for this shape.
 bool dispatch_sample_supported(const tempo_moe_shape& s);
 
 hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, const int32_t* topk_ids,
                            const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
-                           const Layout& L, bool timing, bool gather_rows, hipStream_t st);
+                           const Layout& L, bool timing, bool copy_rows, bool copy_scales, hipStream_t st);
 
 // ev: null, or 3 events (each nullable) recorded after the gate/up GEMM
 // kernel, after the gate/up step and after the down GEMM kernel.
-// x_rows: null -> the gate/up GEMM reads d.x_perm (and for fp8
-// d.x_perm_scale); otherwise it reads the activation rows
-// x_rows[row_token[row]] (x_rows = the unpermuted x) and for fp8 their
-// scales x_rows_scale[row_token[row]] ([tokens][H/128] fp32).
+// x_rows: null -> the gate/up GEMM reads d.x_perm; otherwise it reads the
+// activation rows x_rows[row_token[row]] (x_rows = the unpermuted x).  fp8:
+// the stream-K GEMM reads the scales from d.x_perm_scale; the large-tile
+// kernel from x_rows_scale[row_token[row]] ([tokens][H/128] fp32) when
+// x_rows is given, else from d.x_perm_scale.  Whether stage 2 reads the
+// token rows, and their fp8 scales, itself: experts_gather_rows /
+// experts_reads_token_scales.
 hipError_t launch_experts_bf16(const tempo_moe_shape& s, const tempo_dispatch_out& d, const tempo_expert_weights& w,
                                const void* x_rows, void* y_perm, char* ws, const Layout& L, bool timing,
                                const hipEvent_t* ev, hipStream_t st);
@@ -110,6 +113,7 @@ hipError_t launch_pack(const tempo_moe_shape& s, const tempo_expert_weights& nat
 // GEMM when every workgroup's range spans few enough M-tiles (the row tables
 // of its M-tiles sit in LDS).
 bool experts_gather_rows(const tempo_moe_shape& s, const Layout& L);
+bool experts_reads_token_scales(const tempo_moe_shape& s);
 
 // Whether stage-2 kernels exist for this shape's element type and M-tile.
 bool experts_supported(const tempo_moe_shape& s);
