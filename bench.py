@@ -6,18 +6,20 @@ M-tile padded permute), stage 2 grouped expert FFN (gate/up + SwiGLU, down)
 and stage 3 combine -- over one synthetic batch already resident in HBM.
 Default workload: the Qwen3-235B-shaped prefill share (18 local slots = 16
 home experts of 128 + 2 replicas of the hottest experts homed elsewhere,
-H 4096, I 1536, bf16, 8192 tokens, top-8, Zipf(1.0) popularity, uniform
-plan), the largest configuration; almost every slot is in the linear
-(compute-bound) regime of the cost model.
+H 4096, I 1536, 8192 tokens, top-8, Zipf(1.0) popularity, uniform plan) in
+fp8 e4m3 with power-of-two (UE8M0) block scales, the largest configuration;
+almost every slot is in the linear (compute-bound) regime of the cost model.
+The same share in bf16 is measured beside it (`roofline_bf16`).
 
 Prints ONE JSON line: the block time (us/batch, lower is better), the
 roofline of the dominant kernel (the gate/up GEMM: MFMA-bound at prefill,
-HBM-bound at decode), the same for the flat-regime decode share
-(`roofline_flat`: 512 tokens, the weight-streaming regime), the fitted
-max-affine profile (a, b, c, beta, n*) of the headline's dtype and M-tile,
-per-stage times, and the CPU oracle timed on the host cores as a baseline.
+HBM-bound at decode), the same for the bf16 prefill share and for the
+flat-regime decode share (`roofline_flat`: 512 tokens, the weight-streaming
+regime), the fitted max-affine profile (a, b, c, beta, n*) of each one's
+dtype and M-tile, per-stage times, and the CPU oracle timed on the host
+cores as a baseline.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME] [--no-flat]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME] [--no-flat] [--no-bf16]
 """
 from __future__ import annotations
 
@@ -46,7 +48,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="qwen3_prefill_bf16")
+    ap.add_argument("--workload", default="qwen3_prefill_fp8mx")
+    ap.add_argument("--bf16-workload", default="qwen3_prefill_bf16",
+                    help="the same share in bf16, measured beside the headline for roofline_bf16")
+    ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--flat-workload", default="qwen3_decode_bf16",
                     help="the weight-streaming (decode) share measured beside the headline for roofline_flat")
     ap.add_argument("--no-flat", action="store_true")
@@ -132,19 +137,24 @@ def cpu_baseline(wl, plan, x, xs, w13, s13, w2, s2, m_tile, budget_s):
     loc = np.nonzero(npairs.any(axis=1))[0]
     total_pairs = int(npairs.sum())
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    # calibrate on a few tokens, then size the sample to the budget
+    # calibrate on two small token sets (a call has a fixed cost besides its
+    # per-pair work), then size the sample to the budget
     rng = np.random.default_rng(0)
     order = rng.permutation(loc)
-    probe = order[: min(len(order), max(1, threads))]
-    sel = np.zeros(wl.T, np.uint8)
-    sel[probe] = 1
-    t0 = time.perf_counter()
-    oracle.moe(x, wl.topk_w, ps, w13, w2, wl.dtype, "exact", xs, s13, s2, token_sel=sel)
-    t_probe = time.perf_counter() - t0
-    probe_pairs = int(npairs[probe].sum())
-    per_pair = t_probe / max(1, probe_pairs)
-    n_more = int(max(0, budget_s - t_probe) / max(per_pair, 1e-9))
-    sample = order[: min(len(order), len(probe) + max(0, n_more // max(1, wl.K)))]
+    pts = []
+    for n in (max(1, threads), 4 * max(1, threads)):
+        probe = order[: min(len(order), n)]
+        sel = np.zeros(wl.T, np.uint8)
+        sel[probe] = 1
+        t0 = time.perf_counter()
+        oracle.moe(x, wl.topk_w, ps, w13, w2, wl.dtype, "exact", xs, s13, s2, token_sel=sel)
+        pts.append((int(npairs[probe].sum()), time.perf_counter() - t0))
+    (p1, t1), (p2, t2) = pts
+    per_pair = max((t2 - t1) / max(1, p2 - p1), t2 / max(1, p2) * 0.05, 1e-9)
+    fixed = max(0.0, t2 - per_pair * p2)
+    want_pairs = max(p2, int((budget_s - fixed) / per_pair))
+    pairs_per_token = max(1e-9, total_pairs / max(1, len(loc)))
+    sample = order[: min(len(order), int(want_pairs / pairs_per_token) + 1)]
     sel = np.zeros(wl.T, np.uint8)
     sel[sample] = 1
     t0 = time.perf_counter()
@@ -257,12 +267,15 @@ def measure_workload(torch, name, m_tile, plan_name, steps, warmup, seed, copies
     m.eager_ms = evs[0][0].elapsed_time(evs[K - 1][NE - 1]) / K
     m.stage_us = {
         "dispatch": float(np.mean(at[:, 1])),
-        "gate_up": float(np.mean(at[:, 3] - at[:, 1])),
-        "down": float(np.mean(at[:, 5] - at[:, 3])),
-        "combine": float(np.mean(at[:, 6] - at[:, 5])),
+        "gate_up": float(np.mean(at[:, 4] - at[:, 1])),
+        "down": float(np.mean(at[:, 6] - at[:, 4])),
+        "combine": float(np.mean(at[:, 7] - at[:, 6])),
     }
-    m.kernel_us = {"gate_up_gemm": float(np.mean(at[:, 2] - at[:, 1])),
-                   "down_gemm": float(np.mean(at[:, 4] - at[:, 3]))}
+    # the gate/up GEMM kernel alone (events right before and after it; the
+    # large-tile path packs the activation rows first), and the down GEMM
+    m.kernel_us = {"gate_up_gemm": float(np.mean(at[:, 3] - at[:, 2])),
+                   "down_gemm": float(np.mean(at[:, 5] - at[:, 4])),
+                   "before_gate_up_gemm": float(np.mean(at[:, 2] - at[:, 1]))}
     log(f"{name}: graph ms/step {m.ms_per_step:.4f} eager(events) ms/step {m.eager_ms:.4f} "
         f"stages_us {m.stage_us} kernels_us {m.kernel_us}")
     del graphs, fwd, wsets, weights0, ws, disp, y
@@ -359,6 +372,12 @@ def main():
         "mfma": mfma,
         "fit": measure.committed_fit(shape_name, wl.dtype, m.m_tile),
     }
+    if not args.no_bf16 and args.bf16_workload != args.workload:
+        o = measure_workload(torch, args.bf16_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
+        out["roofline_bf16"] = {**roofline(o), "workload": args.bf16_workload, "m_tile": o.m_tile,
+                                "block_us": o.ms_per_step * 1e3, "stages_us": o.stage_us,
+                                "fit": measure.committed_fit(shape_name, o.wl.dtype, o.m_tile)}
+        del o
     if not args.no_flat and args.flat_workload != args.workload:
         f = measure_workload(torch, args.flat_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
         out["roofline_flat"] = {**roofline(f), "workload": args.flat_workload, "m_tile": f.m_tile,

@@ -300,14 +300,15 @@ int tempo_moe_combine(const tempo_moe_shape* shape, const int32_t* pair_row, con
  * first stage-2 tile that started on it to the last that ended, measured
  * with the GPU's 100 MHz real-time counter (0 for slots with c_s = 0).
  * Spans of concurrently running slots overlap; it is exact for one slot.
- * stage_events: nullable host array of TEMPO_STAGE_EVENTS (7) hipEvent_t
- * (created by the caller) recorded on `stream` before stage 1, after stage 1,
- * after the gate/up GEMM kernel, after the whole gate/up step (split-item
- * fixup and, for fp8, the re-quantisation of h), after the down GEMM kernel,
- * after the whole down step and after stage 3, for per-stage and per-kernel
- * timing.
+ * stage_events: nullable host array of TEMPO_STAGE_EVENTS (8) hipEvent_t
+ * (created by the caller; each entry nullable) recorded on `stream` before
+ * stage 1, after stage 1, right before the gate/up GEMM kernel (after the
+ * activation pack of the 256-row large-tile kernels), after it, after the
+ * whole gate/up step (split-item fixup and, for fp8, the re-quantisation of
+ * h), after the down GEMM kernel, after the whole down step and after
+ * stage 3, for per-stage and per-kernel timing.
  */
-#define TEMPO_STAGE_EVENTS 7
+#define TEMPO_STAGE_EVENTS 8
 int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, const int32_t* topk_ids,
                       const float* topk_w, const void* x, const float* x_scale, const tempo_expert_weights* weights,
                       const tempo_dispatch_out* disp, void* y, uint64_t* slot_time_ns, void* const* stage_events,

@@ -254,11 +254,11 @@ int tempo_moe_forward(const tempo_moe_shape* shape, const tempo_plan* plan, cons
           : launch_experts_fp8(*shape, *disp, *weights, x_rows, own_scales ? x_scale : nullptr, y_perm, ws, L,
                                        timing, ev + 2, st);
   if (e == hipErrorNotSupported) return TEMPO_EUNSUPPORTED;
-  if (e != hipSuccess || !mark(5)) return TEMPO_EDEVICE;
+  if (e != hipSuccess || !mark(6)) return TEMPO_EDEVICE;
   e = launch_combine(*shape, disp->pair_row, topk_w, y_perm, y, disp->slot_counts,
                      reinterpret_cast<const uint64_t*>(ws + L.slot_t0),
                      reinterpret_cast<const uint64_t*>(ws + L.slot_t1), slot_time_ns, st);
-  if (e != hipSuccess || !mark(6)) return TEMPO_EDEVICE;
+  if (e != hipSuccess || !mark(7)) return TEMPO_EDEVICE;
   return TEMPO_OK;
 }
 

@@ -385,8 +385,9 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
   gu.C = ws + L.h;  // packed h
   gu.Kd = s.H;
   gu.Nout = s.I;
+  if (!mark(0)) return hipErrorLaunchFailure;  // after the pack: the GEMM kernel alone is timed
   hipLaunchKernelGGL(k_gemm_big<true>, dim3(grid), dim3(256), 0, st, gu);
-  if (!mark(0) || !mark(1)) return hipErrorLaunchFailure;
+  if (!mark(1) || !mark(2)) return hipErrorLaunchFailure;
 
   GemmArgs dn = a;
   dn.A = ws + L.h;
@@ -399,7 +400,7 @@ hipError_t launch_experts_big(const tempo_moe_shape& s, const tempo_dispatch_out
   dn.Kd = s.I;
   dn.Nout = s.H;
   hipLaunchKernelGGL(k_gemm_big<false>, dim3(grid), dim3(256), 0, st, dn);
-  if (!mark(2)) return hipErrorLaunchFailure;
+  if (!mark(3)) return hipErrorLaunchFailure;
   return hipGetLastError();
 }
 

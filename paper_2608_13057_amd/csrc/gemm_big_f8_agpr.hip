@@ -507,8 +507,9 @@ hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_
   gu.C_sc = h_sc;
   gu.Kd = s.H;
   gu.Nout = s.I;
+  if (!mark(0)) return hipErrorLaunchFailure;  // after the pack: the GEMM kernel alone is timed
   hipLaunchKernelGGL(k_gemm_big_f8<true>, dim3(grid), dim3(256), 0, st, gu);
-  if (!mark(0) || !mark(1)) return hipErrorLaunchFailure;
+  if (!mark(1) || !mark(2)) return hipErrorLaunchFailure;
 
   F8Args dn = a;
   dn.A = h8;
@@ -524,7 +525,7 @@ hipError_t launch_experts_big_f8(const tempo_moe_shape& s, const tempo_dispatch_
   dn.Kd = s.I;
   dn.Nout = s.H;
   hipLaunchKernelGGL(k_gemm_big_f8<false>, dim3(grid), dim3(256), 0, st, dn);
-  if (!mark(2)) return hipErrorLaunchFailure;
+  if (!mark(3)) return hipErrorLaunchFailure;
   return hipGetLastError();
 }
 

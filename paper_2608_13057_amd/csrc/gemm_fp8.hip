@@ -91,12 +91,13 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.Kd = s.H;
   gu.Nout = s.I;
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
-  hipLaunchKernelGGL((k_gemm<true, BM, true, MX>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
   if (!mark(0)) return hipErrorLaunchFailure;
+  hipLaunchKernelGGL((k_gemm<true, BM, true, MX>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
+  if (!mark(1)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, true>), dim3(grid * (BM / 8)), dim3(256), 0, st, gu, grid);
   hipLaunchKernelGGL(k_quant_h<MX>, dim3(std::min(ceil_div(L.row_cap, 4), persistent_grid(8))), dim3(256), 0, st, h32, s.I, L.row_cap, d.row_token,
                      d.slot_offsets, s.S, h8, hs);
-  if (!mark(1)) return hipErrorLaunchFailure;
+  if (!mark(2)) return hipErrorLaunchFailure;
 
   // down -> y_perm [row_cap, H] bf16
   GemmArgs dn = a;
@@ -113,7 +114,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.Kd = s.I;
   dn.Nout = s.H;
   hipLaunchKernelGGL((k_gemm<true, BM, false, MX>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
-  if (!mark(2)) return hipErrorLaunchFailure;
+  if (!mark(3)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_fixup<true, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }

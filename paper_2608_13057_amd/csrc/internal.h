@@ -62,8 +62,9 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
                            const void* x, const float* x_scale, const tempo_dispatch_out& out, char* ws,
                            const Layout& L, bool timing, bool copy_rows, bool copy_scales, hipStream_t st);
 
-// ev: null, or 3 events (each nullable) recorded after the gate/up GEMM
-// kernel, after the gate/up step and after the down GEMM kernel.
+// ev: null, or 4 events (each nullable) recorded right before the gate/up
+// GEMM kernel (after the activation pack of the large-tile kernels), after
+// it, after the gate/up step and after the down GEMM kernel.
 // x_rows: null -> the gate/up GEMM reads d.x_perm; otherwise it reads the
 // activation rows x_rows[row_token[row]] (x_rows = the unpermuted x).  fp8:
 // the stream-K GEMM reads the scales from d.x_perm_scale; the large-tile

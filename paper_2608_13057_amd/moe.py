@@ -282,17 +282,18 @@ def combine(shape: MoEShape, pair_row, topk_w, y_perm, y, stream=None):
 
 
 # events of tempo_moe_forward's stage_events (TEMPO_STAGE_EVENTS)
-STAGE_EVENTS = 7
+STAGE_EVENTS = 8
 
 
 def forward(shape: MoEShape, plan: PlanTensors, topk_ids, topk_w, x, x_scale, weights: WeightTensors,
             disp: DispatchBuffers, y, ws: Workspace, slot_time_ns=None, stage_events=None, stream=None):
     """Stages 1-3 (tempo_moe_forward): writes y [T, H] bf16 (int16 bits);
     weights must be packed (pack_weights).
-    stage_events: optional list of STAGE_EVENTS (7) torch.cuda.Event (created
-    with enable_timing=True) recorded before stage 1, after stage 1, after the
-    gate/up GEMM kernel, after the gate/up step, after the down GEMM kernel,
-    after the down step and after stage 3."""
+    stage_events: optional list of STAGE_EVENTS (8) torch.cuda.Event (created
+    with enable_timing=True) recorded before stage 1, after stage 1, right
+    before the gate/up GEMM kernel (after the activation pack of the
+    large-tile kernels), after it, after the gate/up step, after the down GEMM
+    kernel, after the down step and after stage 3."""
     _check_inputs(shape, topk_ids, x, x_scale)
     _need(topk_w, torch.float32, (shape.T, shape.K), "topk_w")
     _check_plan(shape, plan)
@@ -369,8 +370,11 @@ class PreparedForward:
         check(self._fn(*self._args, evs, *self._tail, _stream(stream)), "tempo_moe_forward")
 
 
-def _event_handle(ev) -> int:
-    """The hipEvent_t behind a torch.cuda.Event (created on first record)."""
+def _event_handle(ev):
+    """The hipEvent_t behind a torch.cuda.Event (created on first record);
+    None for a null entry (the library skips it)."""
+    if ev is None:
+        return None
     if ev.cuda_event == 0:
         ev.record()  # materialise the event on the current stream
     return ev.cuda_event

@@ -127,6 +127,33 @@ def test_forward_tiny(m_tile, name):
     assert np.all((st > 0) == (sc > 0))
 
 
+@pytest.mark.parametrize("name,m_tile", [("tiny", 64), ("tiny", 256), ("tiny_fp8", 128), ("tiny_fp8mx", 256)])
+def test_stage_events_in_order(name, m_tile):
+    """The eight stage events of the forward are recorded in stream order
+    (stage 1, the gate/up GEMM kernel alone, the gate/up step, the down GEMM,
+    the down step, stage 3), on the stream-K and the large-tile paths, with a
+    null entry skipped; the outputs are those of a forward without events."""
+    import torch
+    from paper_2608_13057_amd import moe, synth
+
+    wl = synth.make_workload(name)
+    c = Case(wl, "uniform", m_tile)
+    y0, _ = _run_forward(c)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(moe.STAGE_EVENTS)]
+    y = torch.empty(c.wl.T, c.wl.H, dtype=torch.int16, device="cuda")
+    moe.forward(c.shape, c.d_plan, c.d_ids, c.d_w, c.d_x, c.d_xs, c.d_weights, c.disp, y, c.ws, stage_events=ev)
+    torch.cuda.synchronize()
+    t = [ev[0].elapsed_time(e) for e in ev]
+    assert all(b >= a for a, b in zip(t, t[1:])), t
+    assert t[3] - t[2] > 0  # the gate/up GEMM kernel takes time
+    assert np.array_equal(to_host(y), y0)
+    ev2 = list(ev)
+    ev2[2] = None  # a null entry is skipped
+    moe.forward(c.shape, c.d_plan, c.d_ids, c.d_w, c.d_x, c.d_xs, c.d_weights, c.disp, y, c.ws, stage_events=ev2)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(y), y0)
+
+
 @pytest.mark.parametrize("name", ["tiny", "tiny_fp8", "tiny_fp8mx"])
 def test_forward_split_invariance_bit_exact(name):
     """The same batch under different splits of the replicated experts over
