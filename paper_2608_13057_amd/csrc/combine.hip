@@ -10,16 +10,20 @@
 namespace tempo {
 namespace {
 
-__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+// Two fp32 values as bf16 (round to nearest even) in one word, lo in the
+// low half: gfx950's packed conversion.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t bf16x2_rne(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2_t));
 }
 
-// One wavefront per (token, 512-column segment): each lane owns 8 columns,
-// reads the token's K rows and weights (one load each, issued together) and
-// then the K 16-byte pieces of y_perm at once, so the kernel waits on two
-// memory latencies whatever K is.
+// One wavefront per (token, 512-column segment): each lane owns 8 columns.
+// The token is uniform over the wavefront, so its K row indices and weights
+// are scalar loads and the skip of a pair without a local row is a uniform
+// branch; the K 16-byte pieces of y_perm are then loaded together, so the
+// kernel waits on two memory latencies whatever K is.  Lanes past the end of
+// a short row load a valid piece and store nothing.
 constexpr int kCombKU = 8;  // pairs whose loads are in flight together
 
 __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int H, const int32_t* __restrict__ pair_row,
@@ -30,7 +34,7 @@ __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int 
                                                  uint64_t* __restrict__ slot_time_ns) {
   const int lane = threadIdx.x & 63;
   const int nseg = (H + 511) / 512;
-  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   if (slot_time_ns && blockIdx.x == 0)
     for (int s = threadIdx.x; s < S; s += 256)
       slot_time_ns[s] = slot_counts[s] > 0 ? (t1[s] - t0[s]) * 10ull : 0ull;  // 100 MHz counter
@@ -38,25 +42,36 @@ __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int 
   if (t >= T) return;
   const int c = seg * 64 + lane;  // this lane's 16-byte chunk (8 columns)
   const bool own = c < H / 8;
+  const int cl = own ? c : 0;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   if (t < T_valid) {
     for (int k0 = 0; k0 < K; k0 += kCombKU) {
       int r[kCombKU];
       float wk[kCombKU];
+      const int32_t* pr = pair_row + (size_t)t * K + k0;
+      const float* pw = topk_w + (size_t)t * K + k0;
+      if (k0 + kCombKU <= K) {  // (a whole group: one scalar load of each array)
 #pragma unroll
-      for (int u = 0; u < kCombKU; u++) {
-        const bool ok = k0 + u < K;
-        r[u] = ok ? pair_row[(size_t)t * K + k0 + u] : -1;
-        wk[u] = ok ? topk_w[(size_t)t * K + k0 + u] : 0.f;
+        for (int u = 0; u < kCombKU; u++) {
+          r[u] = __builtin_amdgcn_readfirstlane(pr[u]);
+          wk[u] = pw[u];
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < kCombKU; u++) {
+          const bool ok = k0 + u < K;
+          r[u] = ok ? __builtin_amdgcn_readfirstlane(pr[u]) : -1;
+          wk[u] = ok ? pw[u] : 0.f;
+        }
       }
       uint4 v[kCombKU];
 #pragma unroll
       for (int u = 0; u < kCombKU; u++)
-        if (r[u] >= 0 && own) v[u] = *reinterpret_cast<const uint4*>(y_perm + (size_t)r[u] * H + c * 8);
+        v[u] = r[u] >= 0 ? *reinterpret_cast<const uint4*>(y_perm + (size_t)r[u] * H + cl * 8) : make_uint4(0, 0, 0, 0);
       // ascending k: the fp32 sum is formed in the order of the definition
 #pragma unroll
       for (int u = 0; u < kCombKU; u++) {
-        if (r[u] < 0 || !own) continue;
+        if (r[u] < 0) continue;
         const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
 #pragma unroll
         for (int q = 0; q < 4; q++) {
@@ -68,10 +83,10 @@ __global__ __launch_bounds__(256) void k_combine(int T, int T_valid, int K, int 
   }
   if (!own) return;
   uint4 o;
-  o.x = (uint32_t)f32_to_bf16_rne(acc[0]) | ((uint32_t)f32_to_bf16_rne(acc[1]) << 16);
-  o.y = (uint32_t)f32_to_bf16_rne(acc[2]) | ((uint32_t)f32_to_bf16_rne(acc[3]) << 16);
-  o.z = (uint32_t)f32_to_bf16_rne(acc[4]) | ((uint32_t)f32_to_bf16_rne(acc[5]) << 16);
-  o.w = (uint32_t)f32_to_bf16_rne(acc[6]) | ((uint32_t)f32_to_bf16_rne(acc[7]) << 16);
+  o.x = bf16x2_rne(acc[0], acc[1]);
+  o.y = bf16x2_rne(acc[2], acc[3]);
+  o.z = bf16x2_rne(acc[4], acc[5]);
+  o.w = bf16x2_rne(acc[6], acc[7]);
   *reinterpret_cast<uint4*>(y + (size_t)t * H + c * 8) = o;
 }
 

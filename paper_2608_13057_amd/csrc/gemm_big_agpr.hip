@@ -75,13 +75,22 @@ __global__ __launch_bounds__(256) void k_pack_rows(const char* __restrict__ A, i
     const int tile = blk / KT, k = blk - tile * KT;
     char* dst = out + (size_t)tile * packed_tile_bytes(K) + (size_t)(4 * k + w) * SUB_BYTES;
     const int col = k * 128 + (2 * w + (lane >> 5)) * 16;
+    // the block's row indices, then all of its row loads, then the stores:
+    // two memory latencies per block (padding rows load row 0 and store 0)
+    int tok[8];
+#pragma unroll
+    for (int b = 0; b < 8; b++) tok[b] = row_token[tile * BIG_M + 32 * b + (lane & 31)];
+    i32x4 v[8];
 #pragma unroll
     for (int b = 0; b < 8; b++) {
       const int row = tile * BIG_M + 32 * b + (lane & 31);
-      const int tok = row_token[row];
-      i32x4 v = {0, 0, 0, 0};
-      if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + (size_t)(gather ? tok : row) * row_bytes + col);
-      *reinterpret_cast<i32x4*>(dst + b * 1024 + lane * 16) = v;
+      const int src = tok[b] < 0 ? 0 : gather ? tok[b] : row;
+      v[b] = *reinterpret_cast<const i32x4*>(A + (size_t)src * row_bytes + col);
+    }
+#pragma unroll
+    for (int b = 0; b < 8; b++) {
+      const i32x4 z = {0, 0, 0, 0};
+      *reinterpret_cast<i32x4*>(dst + b * 1024 + lane * 16) = tok[b] < 0 ? z : v[b];
     }
   }
 }
@@ -258,8 +267,8 @@ __device__ __forceinline__ void big_body(const GemmArgs& p, char* ring, const in
     const int l31 = lid & 31, h = lid >> 5;
     auto pack4 = [](float v0, float v1, float v2, float v3) {
       uint2 w;
-      w.x = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
-      w.y = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+      w.x = bf16x2_rne(v0, v1);
+      w.y = bf16x2_rne(v2, v3);
       return w;
     };
     // Lanes l and l + 32 hold the two 8-byte halves (columns 8 q .. 8 q + 3

@@ -80,25 +80,38 @@ __global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict_
   for (int blk = blockIdx.x; blk < blocks; blk += gridDim.x) {
     const int tile = blk / KT, kt = blk - tile * KT;
     uint8_t* dst = out + (size_t)tile * f8_tile_bytes(K) + (size_t)kt * (F8_M * F8_STEP);
+    // the block's row indices, then all of its row and scale loads, then
+    // the stores: two memory latencies per block (padding rows load row 0
+    // and store zeros with exponent 127)
+    int tok[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; pb++) tok[pb] = row_token[tile * F8_M + 32 * (2 * w + pb) + (lane & 31)];
+    const int row_e = tile * F8_M + tid;
+    const int tok_e = row_token[row_e];
+    i32x4 v[2][4];
 #pragma unroll
     for (int pb = 0; pb < 2; pb++) {
-      const int b = 2 * w + pb;
-      const int row = tile * F8_M + 32 * b + (lane & 31);
-      const int tok = row_token[row];
-      const size_t src_row = (size_t)(gather ? tok : row) * K + kt * F8_STEP;
+      const int row = tile * F8_M + 32 * (2 * w + pb) + (lane & 31);
+      const size_t src_row = (size_t)(tok[pb] < 0 ? 0 : gather ? tok[pb] : row) * K + kt * F8_STEP;
 #pragma unroll
       for (int j = 0; j < 4; j++) {
         const int c = 4 * (j >> 1) + 2 * (lane >> 5) + (j & 1);
-        i32x4 v = {0, 0, 0, 0};
-        if (tok >= 0) v = *reinterpret_cast<const i32x4*>(A + src_row + c * 16);
-        *reinterpret_cast<i32x4*>(dst + b * 4096 + j * 1024 + lane * 16) = v;
+        v[pb][j] = *reinterpret_cast<const i32x4*>(A + src_row + c * 16);
       }
     }
-    const int row = tile * F8_M + tid;
-    const int tok = row_token[row];
-    uint32_t e = 127;
-    if (tok >= 0) e = ue8m0_of(gather ? A_scale[(size_t)tok * KT + kt] : A_scale[(size_t)kt * row_cap + row]);
-    out_sc[(size_t)tile * f8_tile_scale_bytes(K) + (size_t)kt * 256 + (tid & 31) * 8 + (tid >> 5)] = (uint8_t)e;
+    const float sc = tok_e < 0 ? 1.0f
+                               : (gather ? A_scale[(size_t)tok_e * KT + kt] : A_scale[(size_t)kt * row_cap + row_e]);
+#pragma unroll
+    for (int pb = 0; pb < 2; pb++) {
+      const int b = 2 * w + pb;
+#pragma unroll
+      for (int j = 0; j < 4; j++) {
+        const i32x4 z = {0, 0, 0, 0};
+        *reinterpret_cast<i32x4*>(dst + b * 4096 + j * 1024 + lane * 16) = tok[pb] < 0 ? z : v[pb][j];
+      }
+    }
+    out_sc[(size_t)tile * f8_tile_scale_bytes(K) + (size_t)kt * 256 + (tid & 31) * 8 + (tid >> 5)] =
+        (uint8_t)(tok_e < 0 ? 127u : ue8m0_of(sc));
   }
 }
 
@@ -336,8 +349,8 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     const int l31 = lid & 31, hl = lid >> 5;
     auto pack4 = [](float v0, float v1, float v2, float v3) {
       uint2 w;
-      w.x = (uint32_t)f32_to_bf16_rne(v0) | ((uint32_t)f32_to_bf16_rne(v1) << 16);
-      w.y = (uint32_t)f32_to_bf16_rne(v2) | ((uint32_t)f32_to_bf16_rne(v3) << 16);
+      w.x = bf16x2_rne(v0, v1);
+      w.y = bf16x2_rne(v2, v3);
       return w;
     };
     if (GATEUP) {

@@ -290,6 +290,16 @@ def test_forward_slot_table_bit_exact(name, m_tile):
     moe.forward(c.shape, c.d_plan, c.d_ids, c.d_w, c.d_x, c.d_xs, tab, c.disp, y, c.ws)
     torch.cuda.synchronize()
     assert np.array_equal(to_host(y), y_ref)
+    # replicas of one expert sharing a single packed copy (the use the table
+    # is for): every slot points at the copy of the first slot of its expert
+    se = wl.placement.slot_expert.tolist()
+    first = {e: se.index(e) for e in se}
+    assert len(first) < wl.S  # the workload has replicated experts
+    shared = moe.slot_table([slots[first[e]] for e in se])
+    y.fill_(0)
+    moe.forward(c.shape, c.d_plan, c.d_ids, c.d_w, c.d_x, c.d_xs, shared, c.disp, y, c.ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(to_host(y), y_ref)
 
 
 def _expect_packed(w, rows_of_block, nblk, fp8):
