@@ -36,7 +36,8 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 COPY_BYTES = 256 << 20
-GEMM_SOURCES = ("gemm_stream.h", "gemm_common.h", "gemm_bf16.hip", "gemm_fp8.hip", "gemm_big_agpr.hip", "pack.hip")
+GEMM_SOURCES = ("gemm_stream.h", "gemm_common.h", "gemm_bf16.hip", "gemm_fp8.hip", "gemm_big_agpr.hip", "gemm_big_f8_agpr.hip",
+                "pack.hip")
 
 
 def gemm_source_hash() -> str:
