@@ -180,19 +180,26 @@ def test_forward_split_invariance_bit_exact(name):
         assert np.array_equal(outs[m_tile][0], outs[same[0]][0]), f"M={m_tile} differs from M={same[0]}"
 
 
-def test_forward_padding_rows_and_empty_batch():
+@pytest.mark.parametrize("name,m_tile", [("tiny", 64), ("tiny", 256), ("tiny_fp8", 128), ("tiny_fp8mx", 64),
+                                         ("tiny_fp8mx", 256)])
+def test_forward_padding_rows_and_empty_batch(name, m_tile):
+    """Graph-padding rows (t >= T_valid) and the empty batch, on the stream-K
+    kernel and both large-tile kernels: padding rows and tokens without a
+    local pair are exactly zero, the rest within tolerance; T_valid = 0
+    leaves no tile and y all zero."""
     from paper_2608_13057_amd import synth
 
-    wl = synth.make_workload("tiny")
+    wl = synth.make_workload(name)
     wl.topk_ids[60:] = 0  # degenerate routing on graph-padding rows
-    c = Case(wl, "uniform", 64, T_valid=60)
+    print(f"[padding {name} M={m_tile}]", flush=True)
+    c = Case(wl, "uniform", m_tile, T_valid=60)
     y, _ = _run_forward(c)
     d = c.oracle_dispatch()
     loc, none = _local_rows(d, 60)
     assert np.all(y[60:] == 0) and np.all(y[none] == 0)
     ref = _oracle_y(c, d)
-    assert rel_err_rows(bf16_to_f64(y), ref, loc) <= TOL_EXACT["bf16"]
-    c0 = Case(wl, "uniform", 64, T_valid=0)
+    assert rel_err_rows(bf16_to_f64(y), ref, loc) <= TOL_EXACT[wl.dtype]
+    c0 = Case(wl, "uniform", m_tile, T_valid=0)
     y0, _ = _run_forward(c0)
     assert np.all(y0 == 0)
 
