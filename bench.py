@@ -250,6 +250,19 @@ def measure_workload(torch, name, m_tile, plan_name, steps, warmup, seed, copies
     ev_b.record()
     torch.cuda.synchronize()
     m.ms_per_step = ev_a.elapsed_time(ev_b) / K
+    # the spread of single replays: the same replays with an event between
+    # each (reported beside the headline mean, not instead of it)
+    evr = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    torch.cuda.synchronize()
+    torch.cuda._sleep(spin)
+    evr[0].record()
+    for i in range(K):
+        graphs[i % copies].replay()
+        evr[i + 1].record()
+    torch.cuda.synchronize()
+    per = np.array([evr[i].elapsed_time(evr[i + 1]) for i in range(K)]) * 1e3
+    m.replay_us = {"p10": float(np.percentile(per, 10)), "median": float(np.median(per)),
+                   "p90": float(np.percentile(per, 90))}
 
     # (2) per-kernel times: K eager steps with HIP events between the stages
     # and around the two GEMM kernels, all on the stream the kernels run on
@@ -284,7 +297,7 @@ def measure_workload(torch, name, m_tile, plan_name, steps, warmup, seed, copies
     return m
 
 
-def roofline(m):
+def roofline(m, copy_gbs=None):
     """Roofline of the dominant kernel, the gate/up GEMM launch: MFMA-bound
     (useful flops 2 N H 2I per launch against the dense peak of the dtype)
     when the path runs the large-tile kernel or most pairs sit in slots past
@@ -307,12 +320,18 @@ def roofline(m):
         fl = gemm_flops(wl, m.N, "gateup")
         peak = MFMA_PEAK_TFLOPS[wl.dtype]
         ach = fl / gu_s / 1e12
-        return {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
-                **common, "flops_per_launch": fl}
+        out = {"bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s", "frac": ach / peak,
+               **common, "flops_per_launch": fl}
+        if mf is not None:  # against the peak at the shader clock the counters saw under this load
+            out["frac_at_counter_clock"] = ach / (peak * mf["clock_ghz"] / 2.4)
+        return out
     b = gemm_bytes(wl, wl.dtype, m.G, m.N, "gateup")
     ach = b / gu_s / 1e9
-    return {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
-            **common, "bytes_per_launch": b}
+    out = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+           **common, "bytes_per_launch": b}
+    if copy_gbs:  # against what a plain copy attains on this GPU
+        out["frac_of_attainable"] = ach / copy_gbs
+    return out
 
 
 def main():
@@ -363,25 +382,28 @@ def main():
             "G": m.G, "N": m.N, "tiles": m.tiles,
             "weight_copies_rotated": m.copies,
         },
-        "roofline": roofline(m),
+        "roofline": roofline(m, copy_gbs),
+        "replay_us": m.replay_us,
         "stages_us": m.stage_us,
         "kernels_us": m.kernel_us,
         "eager_ms_per_step": m.eager_ms,
         "attainable_copy_gbs": copy_gbs,
         "stage2_hbm_gbs": (gu_bytes + dn_bytes) / (gu_s + dn_s) / 1e9,
         "mfma": mfma,
+        "env": {"device": torch.cuda.get_device_name(0), "hip": torch.version.hip, "torch": torch.__version__,
+                "compute_units": torch.cuda.get_device_properties(0).multi_processor_count},
         "fit": measure.committed_fit(shape_name, wl.dtype, m.m_tile),
     }
     if not args.no_bf16 and args.bf16_workload != args.workload:
         o = measure_workload(torch, args.bf16_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
-        out["roofline_bf16"] = {**roofline(o), "workload": args.bf16_workload, "m_tile": o.m_tile,
-                                "block_us": o.ms_per_step * 1e3, "stages_us": o.stage_us,
+        out["roofline_bf16"] = {**roofline(o, copy_gbs), "workload": args.bf16_workload, "m_tile": o.m_tile,
+                                "block_us": o.ms_per_step * 1e3, "replay_us": o.replay_us, "stages_us": o.stage_us,
                                 "fit": measure.committed_fit(shape_name, o.wl.dtype, o.m_tile)}
         del o
     if not args.no_flat and args.flat_workload != args.workload:
         f = measure_workload(torch, args.flat_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
-        out["roofline_flat"] = {**roofline(f), "workload": args.flat_workload, "m_tile": f.m_tile,
-                                "block_us": f.ms_per_step * 1e3, "stages_us": f.stage_us,
+        out["roofline_flat"] = {**roofline(f, copy_gbs), "workload": args.flat_workload, "m_tile": f.m_tile,
+                                "block_us": f.ms_per_step * 1e3, "replay_us": f.replay_us, "stages_us": f.stage_us,
                                 "fit": measure.committed_fit(shape_name, f.wl.dtype, f.m_tile)}
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
