@@ -172,16 +172,24 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   // 16-byte dummy so that every wavefront issues F8_DMA loads per sub-step).
   // Past the last item the cursor re-loads the last item's sub-steps.
   int dn = 0, du = 0;
-  const char* a_src = nullptr;
-  const char* w_src = nullptr;
+  // (the cursor is uniform; kept as values read through the first lane so
+  // that it stays in scalar registers and a DMA needs no per-lane address
+  // arithmetic: the per-lane part is a constant offset)
+  uint64_t a_src = 0, w_src = 0;
   const char* sc_src = nullptr;
+  auto uni = [](uint64_t v) {
+    return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
+  };
   auto dma_item = [&]() {
     int tile, nbt;
     item_of(dn, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * F8_M));
-    a_src = reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) + (2 * WV) * 4096;
-    w_src = slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab, p.wfield, slot) +
-            (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096;
+    a_src = uni((uint64_t)(uintptr_t)(reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) +
+                                      (2 * WV) * 4096));
+    w_src = uni((uint64_t)(uintptr_t)(slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab,
+                                                  p.wfield, slot) +
+                                      (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096));
     if (WV == 1)
       sc_src = slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
                (size_t)(2 * nbt) * KT * 16;
@@ -190,12 +198,16 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   };
   const uint32_t ring_lds = lds_addr(ring);
   const uint32_t lane16 = lane * 16;
+  // per-lane offsets of this wavefront's four 1 KB loads of a stream
+  uint32_t voff[4];
+#pragma unroll
+  for (int b = 0; b < 4; b++) voff[b] = lane16 + (b >> 1) * 4096 + (b & 1) * 1024;
   // sub-step du of the cursor: step du >> 1, half du & 1
   auto dma_piece = [&](uint32_t sl, int q) {
     // q = 0..3 activation loads, 4..7 weight loads; each 1 KB
     const int b = q & 3;  // load within this wavefront's share: piece (b >> 1), part (b & 1)
-    const char* src = (q < 4 ? a_src : w_src) + (b >> 1) * 4096 + (b & 1) * 1024;
-    lds_dma16s(src, lane16, sl + (q < 4 ? 0 : F8_SUB) + (4 * WV + b) * 1024);
+    lds_dma16s(reinterpret_cast<const void*>(q < 4 ? a_src : w_src), voff[b],
+               sl + (q < 4 ? 0 : F8_SUB) + (4 * WV + b) * 1024);
   };
   auto dma_scales = [&](uint32_t sl) {
     const int kt = du >> 1;
@@ -211,8 +223,8 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     // half 0 -> 1 within a step: +2 KB; half 1 -> the next step's half 0
     const int st = (du & 1) ? F8_M * F8_STEP - 2048 : 2048;
     const int sw = (du & 1) ? 128 * F8_STEP - 2048 : 2048;
-    a_src += st;
-    w_src += sw;
+    a_src = uni(a_src + st);
+    w_src = uni(w_src + sw);
     if (++du == NU) {
       du = 0;
       if (dn + 1 < my_items) ++dn;
