@@ -178,7 +178,16 @@ def summarize(rows, scope="gemm") -> dict:
     e2 = F.fit_restarts(G, N, t, T=T)
     ci = F.bootstrap_b(G, N, t, reps=200)
     clean = lambda d: {k: v for k, v in d.items() if k != "flat"}
-    return dict(scope=scope, points=len(R), eq1=clean(e1), eq2=clean(e2), b_ci95=ci,
+    # where Eq. 1's error sits: its mean relative error on the points of each
+    # piece, beside the spread of the repetitions themselves
+    rel = np.abs(F.predict(e1, G, N) - t) / t
+    flat = np.asarray(e1["flat"], bool)
+    spread = np.array([(r["p90"] - r["p10"]) / r["t_us"] for r in R])
+    pieces = dict(flat_points=int(flat.sum()), flat_err=float(rel[flat].mean()) if flat.any() else float("nan"),
+                  linear_points=int((~flat).sum()),
+                  linear_err=float(rel[~flat].mean()) if (~flat).any() else float("nan"),
+                  rep_spread=float(spread.mean()))
+    return dict(scope=scope, points=len(R), eq1=clean(e1), eq2=clean(e2), b_ci95=ci, eq1_pieces=pieces,
                 degenerate1=F.degenerate(e1), degenerate2=F.degenerate(e2, e1))
 
 
@@ -208,7 +217,11 @@ def markdown(rows, title: str, command: str, ns=DEFAULT_N) -> str:
                                                                            "err_max")},
                              **({"b2": e["b2"]} if e.get("b2") is not None else {})))
         lo, med, hi = sm["b_ci95"]
-        out += ["", f"Bootstrap 95% interval of b: {lo:.3f} .. {hi:.3f} us (median {med:.3f}).", ""]
+        pc = sm["eq1_pieces"]
+        out += ["", f"Bootstrap 95% interval of b: {lo:.3f} .. {hi:.3f} us (median {med:.3f}).", "",
+                f"Eq. 1 mean relative error on the {pc['flat_points']} points of its flat piece "
+                f"{pc['flat_err']:.3f}, on the {pc['linear_points']} of its linear piece {pc['linear_err']:.3f}; "
+                f"mean spread of the repetitions (p90 - p10) / median {pc['rep_spread']:.3f}.", ""]
         out += ["fit_json: " + json.dumps(f) for f in fits] + [""]
     g = sorted({r["G"] for r in grid})
     nn = sorted({r["n"] for r in grid})
