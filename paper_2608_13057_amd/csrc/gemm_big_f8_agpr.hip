@@ -368,8 +368,8 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     if (GATEUP) {
       // h of element e (0..7) of tile (i, j): silu(v[e]) * v[e + 8], h column
       // 64 wn + 16 j + 8 (e / 4) + 4 hl + e % 4 of the item's 128
-      // one row block i at a time: its 32 h values of this lane, their amax
-      // over the lane, the row's other lane (l ^ 32) and the other
+      // two row blocks i at a time: the 32 h values of this lane in each,
+      // their amax over the lane, the row's other lane (l ^ 32) and the other
       // wavefront (wn, through LDS), the smallest power-of-two scale
       // >= amax / 448 (1 for an all-zero row), then e4m3 codes of h / 2^k
       // (exact scaling), saturated at 448, round to nearest even.  Lane l
@@ -379,45 +379,53 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
       char* hb = static_cast<char*>(p.C) + (size_t)tile * f8_tile_bytes(p.Nout) + (size_t)nbt * (F8_M * F8_STEP) +
                  (4 * wm) * 4096 + (2 * wn) * 1024 + l31 * 16 + 4 * hl;
       uint32_t ew = 0;
+      // two row blocks per exchange (one barrier for both)
 #pragma unroll
-      for (int i = 0; i < 4; i++) {
-        float h[4][8];
-        float m = 0.f;
+      for (int ip = 0; ip < 2; ip++) {
+        float h[2][4][8];
+        float m[2] = {0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-          f32x16 v = acc[i][j];  // (one tile at a time, as below)
-          asm volatile("" : "+v"(v));
+        for (int ii = 0; ii < 2; ii++) {
 #pragma unroll
-          for (int e = 0; e < 8; e++) {
-            h[j][e] = silu_mul(v[e], v[e + 8]);
-            m = fmaxf(m, fabsf(h[j][e]));
+          for (int j = 0; j < 4; j++) {
+            f32x16 v = acc[2 * ip + ii][j];  // (one tile at a time, as below)
+            asm volatile("" : "+v"(v));
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+              h[ii][j][e] = silu_mul(v[e], v[e + 8]);
+              m[ii] = fmaxf(m[ii], fabsf(h[ii][j][e]));
+            }
           }
+          m[ii] = fmaxf(m[ii], __shfl_xor(m[ii], 32));
+          if (hl == 0) xamax[wn * F8_M + 128 * wm + 32 * (2 * ip + ii) + l31] = m[ii];
         }
-        m = fmaxf(m, __shfl_xor(m, 32));
-        if (hl == 0) xamax[wn * F8_M + 128 * wm + 32 * i + l31] = m;
         wait_lgkm0();
         barrier_nofence();
-        m = fmaxf(m, xamax[(1 - wn) * F8_M + 128 * wm + 32 * i + l31]);
-        float sc = m > 0.f ? m / 448.0f : 1.0f;
-        uint32_t bits = __float_as_uint(sc);
-        if (m > 0.f && (bits & 0x7FFFFFu)) bits = (bits & 0xFF800000u) + 0x800000u;
-        const uint32_t e8 = (bits >> 23) & 0xFFu;
-        const int k = (int)e8 - 127;
-        ew |= e8 << (8 * i);
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
-          float q[8];
+        for (int ii = 0; ii < 2; ii++) {
+          const int i = 2 * ip + ii;
+          const float mm = fmaxf(m[ii], xamax[(1 - wn) * F8_M + 128 * wm + 32 * i + l31]);
+          float sc = mm > 0.f ? mm / 448.0f : 1.0f;
+          uint32_t bits = __float_as_uint(sc);
+          if (mm > 0.f && (bits & 0x7FFFFFu)) bits = (bits & 0xFF800000u) + 0x800000u;
+          const uint32_t e8 = (bits >> 23) & 0xFFu;
+          const int k = (int)e8 - 127;
+          ew |= e8 << (8 * i);
 #pragma unroll
-          for (int e = 0; e < 8; e++) q[e] = fminf(fmaxf(ldexpf(h[j][e], -k), -448.f), 448.f);
-          uint32_t w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
-          w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], w0, true);
-          uint32_t w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
-          w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], w1, true);
-          char* d = hb + i * 4096 + (j & 1) * 1024 + (j >> 1) * 512;
-          *reinterpret_cast<uint32_t*>(d) = w0;
-          *reinterpret_cast<uint32_t*>(d + 8) = w1;
+          for (int j = 0; j < 4; j++) {
+            float q[8];
+#pragma unroll
+            for (int e = 0; e < 8; e++) q[e] = fminf(fmaxf(ldexpf(h[ii][j][e], -k), -448.f), 448.f);
+            uint32_t w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[0], q[1], 0, false);
+            w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], w0, true);
+            uint32_t w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
+            w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], w1, true);
+            char* d = hb + i * 4096 + (j & 1) * 1024 + (j >> 1) * 512;
+            *reinterpret_cast<uint32_t*>(d) = w0;
+            *reinterpret_cast<uint32_t*>(d + 8) = w1;
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
-        __builtin_amdgcn_sched_barrier(0);
       }
       if (wn == 0 && hl == 0)
         *reinterpret_cast<uint32_t*>(p.C_sc + (size_t)tile * f8_tile_scale_bytes(p.Nout) + (size_t)nbt * 256 +
