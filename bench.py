@@ -13,9 +13,10 @@ The same share in bf16 is measured beside it (`roofline_bf16`).
 
 Prints ONE JSON line: the block time (us/batch, lower is better), the
 roofline of the dominant kernel (the gate/up GEMM: MFMA-bound at prefill,
-HBM-bound at decode), the same for the bf16 prefill share and for the
-flat-regime decode share (`roofline_flat`: 512 tokens, the weight-streaming
-regime), the fitted max-affine profile (a, b, c, beta, n*) of each one's
+HBM-bound at decode), the same for the bf16 prefill share and for two
+flat-regime decode shares (`roofline_flat`: the Qwen3 share, 512 tokens,
+mixed regime; `roofline_flat_dsv3`: the DeepSeek-V3 share, 256 tokens, most
+slots weight-streaming), the fitted max-affine profile (a, b, c, beta, n*) of each one's
 dtype and M-tile, per-stage times, and the CPU oracle timed on the host
 cores as a baseline.
 
@@ -54,6 +55,8 @@ def parse():
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--flat-workload", default="qwen3_decode_bf16",
                     help="the weight-streaming (decode) share measured beside the headline for roofline_flat")
+    ap.add_argument("--flat2-workload", default="dsv3_decode_fp8",
+                    help="a second weight-streaming share (most slots far below n*) for roofline_flat_dsv3")
     ap.add_argument("--no-flat", action="store_true")
     ap.add_argument("--plan", default=None)
     ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, 128 above, 256 for bf16 beyond 128 rows per expert")
@@ -405,6 +408,15 @@ def main():
         out["roofline_flat"] = {**roofline(f, copy_gbs), "workload": args.flat_workload, "m_tile": f.m_tile,
                                 "block_us": f.ms_per_step * 1e3, "replay_us": f.replay_us, "stages_us": f.stage_us,
                                 "fit": measure.committed_fit(shape_name, f.wl.dtype, f.m_tile)}
+        del f
+    if not args.no_flat and args.flat2_workload not in (args.workload, args.flat_workload):
+        f2 = measure_workload(torch, args.flat2_workload, 0, None, args.steps, args.warmup, args.seed, 0, spin)
+        sh2 = "dsv3" if f2.wl.H == 7168 else "qwen3"
+        out["roofline_flat_dsv3"] = {**roofline(f2, copy_gbs), "workload": args.flat2_workload, "m_tile": f2.m_tile,
+                                     "block_us": f2.ms_per_step * 1e3, "replay_us": f2.replay_us,
+                                     "stages_us": f2.stage_us,
+                                     "fit": measure.committed_fit(sh2, f2.wl.dtype, f2.m_tile)}
+        del f2
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(wl, m.plan, m.x, m.xs, m.w13, m.s13, m.w2, m.s2, m.m_tile,
