@@ -166,42 +166,52 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   // DMA cursor: item ordinal dn, sub-step du; a_src / w_src point at this
   // wavefront's first 1 KB load of the sub-step (activation loads 4 WV ..
   // 4 WV + 3: pieces 2 WV and 2 WV + 1; weight loads 4 WV .. 4 WV + 3: pieces
-  // 2 (WV & 1), 2 (WV & 1) + 1 of weight block 2 nbt + (WV >> 1)); sc_src:
-  // this wavefront's scale load (WV 0: the tile's 256 exponents of the step;
-  // WV 1: the two weight blocks' packed scales, lanes 0 and 1; WV 2, 3: a
-  // 16-byte dummy so that every wavefront issues F8_DMA loads per sub-step).
-  // Past the last item the cursor re-loads the last item's sub-steps.
+  // 2 (WV & 1), 2 (WV & 1) + 1 of weight block 2 nbt + (WV >> 1)); s_src:
+  // this wavefront's scale load of the step (WV 0: the tile's 256 exponents,
+  // lanes 0..15; WV 1: the two weight blocks' packed scales, lanes 0 and 1;
+  // WV 2, 3: a 16-byte dummy, lane 0, so that every wavefront issues F8_DMA
+  // loads per sub-step).  Past the last item the cursor re-loads the last
+  // item's sub-steps.  The cursor is uniform (values read through the first
+  // lane, so it stays in scalar registers and a DMA needs no per-lane address
+  // arithmetic: the per-lane part is a constant offset), and it moves with
+  // selects only: the bases of the item after the cursor's (a_nxt, w_nxt,
+  // s_nxt) are looked up once per item, outside the sub-steps, so a sub-step
+  // has no branch and its MFMAs stay where the schedule puts them.
   int dn = 0, du = 0;
-  // (the cursor is uniform; kept as values read through the first lane so
-  // that it stays in scalar registers and a DMA needs no per-lane address
-  // arithmetic: the per-lane part is a constant offset)
-  uint64_t a_src = 0, w_src = 0;
-  const char* sc_src = nullptr;
+  uint64_t a_src = 0, w_src = 0, s_src = 0;
+  uint64_t a_nxt = 0, w_nxt = 0, s_nxt = 0;
   auto uni = [](uint64_t v) {
     return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
            (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
   };
-  auto dma_item = [&]() {
+  auto bases = [&](int n, uint64_t& a, uint64_t& w, uint64_t& sc) {
     int tile, nbt;
-    item_of(dn, tile, nbt);
+    item_of(n, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * F8_M));
-    a_src = uni((uint64_t)(uintptr_t)(reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) +
-                                      (2 * WV) * 4096));
-    w_src = uni((uint64_t)(uintptr_t)(slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab,
-                                                  p.wfield, slot) +
-                                      (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096));
-    if (WV == 1)
-      sc_src = slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
-               (size_t)(2 * nbt) * KT * 16;
-    else
-      sc_src = reinterpret_cast<const char*>(p.A_sc) + (size_t)tile * f8_tile_scale_bytes(p.Kd);
+    a = uni((uint64_t)(uintptr_t)(reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) +
+                                  (2 * WV) * 4096));
+    w = uni((uint64_t)(uintptr_t)(slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab, p.wfield,
+                                              slot) +
+                                  (size_t)(2 * nbt + (WV >> 1)) * KT * (F8_STEP * 128) + (2 * (WV & 1)) * 4096));
+    const char* scb =
+        WV == 1 ? slot_tensor(reinterpret_cast<const char*>(p.Wsp), p.ws_slot_floats * 4, p.wtab, p.sfield, slot) +
+                      (size_t)(2 * nbt) * KT * 16
+                : reinterpret_cast<const char*>(p.A_sc) + (size_t)tile * f8_tile_scale_bytes(p.Kd);
+    sc = uni((uint64_t)(uintptr_t)scb);
   };
+  auto load_next = [&]() { bases(min(dn + 1, my_items - 1), a_nxt, w_nxt, s_nxt); };
   const uint32_t ring_lds = lds_addr(ring);
   const uint32_t lane16 = lane * 16;
   // per-lane offsets of this wavefront's four 1 KB loads of a stream
   uint32_t voff[4];
 #pragma unroll
   for (int b = 0; b < 4; b++) voff[b] = lane16 + (b >> 1) * 4096 + (b & 1) * 1024;
+  // the scale load of this wavefront: its lanes, per-lane offset, place in a
+  // ring slot and advance per step
+  const uint64_t sc_mask = WV == 0 ? 0xFFFFull : WV == 1 ? 0x3ull : 0x1ull;
+  const uint32_t sc_voff = WV == 0 ? lane16 : WV == 1 ? lane * (uint32_t)(KT * 16) : 0u;
+  const uint32_t sc_lds = WV == 0 ? F8_SC : WV == 1 ? F8_SC + 256 : F8_SC + 256 + 32 + 16 * (WV - 2);
+  const int sc_step = WV == 0 ? 256 : WV == 1 ? 16 : 0;
   // sub-step du of the cursor: step du >> 1, half du & 1
   auto dma_piece = [&](uint32_t sl, int q) {
     // q = 0..3 activation loads, 4..7 weight loads; each 1 KB
@@ -209,26 +219,19 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     lds_dma16s(reinterpret_cast<const void*>(q < 4 ? a_src : w_src), voff[b],
                sl + (q < 4 ? 0 : F8_SUB) + (4 * WV + b) * 1024);
   };
-  auto dma_scales = [&](uint32_t sl) {
-    const int kt = du >> 1;
-    if (WV == 0) {
-      if (lane < 16) lds_dma16s(sc_src + kt * 256, lane16, sl + F8_SC);
-    } else if (WV == 1) {
-      if (lane < 2) lds_dma16s(sc_src + kt * 16, lane * (uint32_t)(KT * 16), sl + F8_SC + 256);
-    } else {
-      if (lane == 0) lds_dma16s(sc_src, 0, sl + F8_SC + 256 + 32 + 16 * (WV - 2));
-    }
-  };
-  auto dma_advance = [&]() {
-    // half 0 -> 1 within a step: +2 KB; half 1 -> the next step's half 0
-    const int st = (du & 1) ? F8_M * F8_STEP - 2048 : 2048;
-    const int sw = (du & 1) ? 128 * F8_STEP - 2048 : 2048;
-    a_src = uni(a_src + st);
-    w_src = uni(w_src + sw);
-    if (++du == NU) {
-      du = 0;
-      if (dn + 1 < my_items) ++dn;
-      dma_item();
+  auto dma_scales = [&](uint32_t sl) { lds_dma16s_lanes(s_src, sc_voff, sl + sc_lds, sc_mask); };
+  // the cursor's move to the next sub-step, in three parts that the
+  // schedule places after different MFMAs (part 2 last: it moves du)
+  auto dma_advance = [&](int part) {
+    // half 0 -> 1 within a step: +2 KB; half 1 -> the next step's half 0;
+    // after the item's last sub-step: the next item's bases
+    const bool odd = du & 1, wrap = du == NU - 1;
+    if (part == 0) a_src = wrap ? a_nxt : a_src + (odd ? F8_M * F8_STEP - 2048 : 2048);
+    if (part == 1) w_src = wrap ? w_nxt : w_src + (odd ? 128 * F8_STEP - 2048 : 2048);
+    if (part == 2) {
+      s_src = wrap ? s_nxt : s_src + (odd ? sc_step : 0);
+      dn = wrap ? min(dn + 1, my_items - 1) : dn;
+      du = wrap ? 0 : du + 1;
     }
   };
 
@@ -291,12 +294,18 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
         __builtin_amdgcn_sched_barrier(0);
         if (i < 2) {
           dma_piece(sl, 4 * i + j);
-          if (i == 1 && j == 3) dma_scales(sl);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if (i == 2 && j == 0) {
+          dma_scales(sl);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        if ((i == 2 && j >= 2) || (i == 3 && j == 0)) {
+          dma_advance(i == 3 ? 2 : j - 2);
           __builtin_amdgcn_sched_barrier(0);
         }
       }
     }
-    dma_advance();
     sc = sn;
     sn = sn + 1 == F8_NSS ? 0 : sn + 1;
     wait_lgkm0();
@@ -307,13 +316,16 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
 
   // prologue: sub-steps 0 .. NSS - 1 into slots 0 .. NSS - 1; sub-steps 0
   // and 1 landed before the first reads
-  dma_item();
+  bases(0, a_src, w_src, s_src);
+  load_next();
 #pragma unroll 1
   for (int g = 0; g < F8_NSS; g++) {
 #pragma unroll
     for (int q = 0; q < 8; q++) dma_piece(ring_lds + g * F8_SLOT, q);
     dma_scales(ring_lds + g * F8_SLOT);
-    dma_advance();
+    dma_advance(0);
+    dma_advance(1);
+    dma_advance(2);
   }
   __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(F8_DMA * (F8_NSS - 2)));
   barrier_nofence();
@@ -340,6 +352,10 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     const int nvalid = __builtin_amdgcn_readfirstlane(min(F8_M, s_off[slot] + s_cnt[slot] - row0));
     const uint64_t tstart = p.timing ? __builtin_amdgcn_s_memrealtime() : 0;
+    // the bases the DMA cursor moves to when it passes its item's last
+    // sub-step (during this item, since the cursor runs F8_NSS <= NU
+    // sub-steps ahead)
+    load_next();
 
     // NU = 2 KT >= 4 sub-steps, an even number
     substep(0, true, false);

@@ -74,6 +74,24 @@ __device__ __forceinline__ void lds_dma16s(const void* sbase, uint32_t voff, uin
       : "memory", "m0");
 }
 
+// The same DMA for the lanes set in `lanes` only.  EXEC is switched inside
+// the asm statement and restored there, so the load needs no branch around
+// it (a branch would split the caller's basic block, and the scheduling
+// fences that order its MFMAs hold only within one block).
+__device__ __forceinline__ void lds_dma16s_lanes(uint64_t sbase, uint32_t voff, uint32_t lds_addr, uint64_t lanes) {
+  uint64_t saved;
+  asm volatile(
+      "s_mov_b64 %0, exec\n\t"
+      "s_mov_b64 exec, %4\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %3\n\t"
+      "s_mov_b64 exec, %0"
+      : "=&s"(saved)
+      : "v"(voff), "s"(lds_addr), "s"(sbase), "s"(lanes)
+      : "memory", "m0");
+}
+
 // LDS byte address of a shared-memory pointer (the low 32 bits of its
 // generic address).
 __device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
