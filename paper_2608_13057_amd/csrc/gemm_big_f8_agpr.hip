@@ -53,6 +53,7 @@ constexpr int F8_SLOT = F8_SC + 512;            // activations, weights, then sc
 constexpr int F8_NSS = 4;                       // ring slots
 constexpr int F8_DMA = 9;                       // DMA instructions per wavefront and sub-step
 constexpr int F8_GM = 4;                        // M-tiles per group of the item order
+constexpr int F8_MAX_SORT = 4096;               // M-tiles the cost-ordered item list covers (beyond: tile order)
 
 // bytes of a packed 256-row tile of K-byte rows, and of its scale exponents
 __host__ __device__ constexpr size_t f8_tile_bytes(int K) { return (size_t)F8_M * K; }
@@ -86,11 +87,17 @@ __global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict_
     int tok[2];
 #pragma unroll
     for (int pb = 0; pb < 2; pb++) tok[pb] = row_token[tile * F8_M + 32 * (2 * w + pb) + (lane & 31)];
+    // a piece whose first row is padding holds padding only (a tile's valid
+    // rows come first) and the GEMMs skip it: neither loaded nor stored
+    bool live[2];
+#pragma unroll
+    for (int pb = 0; pb < 2; pb++) live[pb] = __builtin_amdgcn_readfirstlane(tok[pb]) >= 0;
     const int row_e = tile * F8_M + tid;
     const int tok_e = row_token[row_e];
     i32x4 v[2][4];
 #pragma unroll
     for (int pb = 0; pb < 2; pb++) {
+      if (!live[pb]) continue;
       const int row = tile * F8_M + 32 * (2 * w + pb) + (lane & 31);
       const size_t src_row = (size_t)(tok[pb] < 0 ? 0 : gather ? tok[pb] : row) * K + kt * F8_STEP;
 #pragma unroll
@@ -103,6 +110,7 @@ __global__ __launch_bounds__(256) void k_pack_rows_f8(const uint8_t* __restrict_
                                : (gather ? A_scale[(size_t)tok_e * KT + kt] : A_scale[(size_t)kt * row_cap + row_e]);
 #pragma unroll
     for (int pb = 0; pb < 2; pb++) {
+      if (!live[pb]) continue;
       const int b = 2 * w + pb;
 #pragma unroll
       for (int j = 0; j < 4; j++) {
@@ -136,11 +144,12 @@ struct F8Args {
 
 // The GEMM of wavefront WV (0..3, uniform) of a workgroup.  (All four
 // issue their loads at the same points, so one code instance serves them.)
+// tord: the M-tiles in cost order (sorted != 0), else tile order.
 template <bool GATEUP>
 __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xamax, const int32_t* s_off,
-                                        const int32_t* s_cnt, const int WV) {
+                                        const int32_t* s_cnt, const uint16_t* tord, const int sorted, const int WV) {
   constexpr int NCOLS = GATEUP ? F8_N / 2 : F8_N;  // output columns per item
-  const int wm = WV & 1, wn = WV >> 1;             // this wavefront's 128-row and 128-weight-row halves
+  const int wm = WV & 1, wn = WV >> 1;             // this wavefront's row blocks 2 i + wm and 128-weight-row half
   const int lane = threadIdx.x & 63;
 
   const int NT = __builtin_amdgcn_readfirstlane(max(0, min(s_off[p.S] / F8_M, p.max_tiles)));
@@ -149,18 +158,25 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   const int NBT = p.Nout / NCOLS;  // items per M-tile
   const int items = NT * NBT;
 
-  // item order: as in the bf16 large-tile kernel (XCD-aware groups of F8_GM
-  // M-tiles, tile index fastest)
+  // Item order.  The item list goes over groups of F8_GM M-tiles (taken in
+  // cost order: most live row blocks first) with the tile index fastest, so
+  // the 32 items an XCD runs at once share weight blocks and activation
+  // tiles in its L2 (workgroup b runs on XCD b % 8; each XCD takes a
+  // contiguous run of the list per round).  Rounds are dealt alternately
+  // forwards and backwards over the workgroups, so the workgroups that take
+  // the costliest items of one round take the cheapest of the next.
   const int G = gridDim.x;
   const int lin0 = (G % 8 == 0) ? (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8 : blockIdx.x;
-  const int my_items = lin0 < items ? (items - 1 - lin0) / G + 1 : 0;
+  const int full = items / G;
+  const int my_items = full + (((full & 1) ? G - 1 - lin0 : lin0) < items - full * G ? 1 : 0);
   if (my_items == 0) return;
   auto item_of = [&](int n, int& tile, int& nbt) {
-    const int it = lin0 + n * G;
+    const int it = n * G + ((n & 1) ? G - 1 - lin0 : lin0);
     const int grp = it / (F8_GM * NBT), w_in = it - grp * (F8_GM * NBT);
     const int gm = min(F8_GM, NT - grp * F8_GM);
     nbt = w_in / gm;
-    tile = grp * F8_GM + (w_in - nbt * gm);
+    const int ti = grp * F8_GM + (w_in - nbt * gm);
+    tile = sorted ? (int)tord[ti] : ti;
   };
 
   // DMA cursor: item ordinal dn, sub-step du; a_src / w_src point at this
@@ -170,8 +186,11 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   // this wavefront's scale load of the step (WV 0: the tile's 256 exponents,
   // lanes 0..15; WV 1: the two weight blocks' packed scales, lanes 0 and 1;
   // WV 2, 3: a 16-byte dummy, lane 0, so that every wavefront issues F8_DMA
-  // loads per sub-step).  Past the last item the cursor re-loads the last
-  // item's sub-steps.  The cursor is uniform (values read through the first
+  // loads per sub-step); d_src: per activation piece of this wavefront, 0,
+  // or, for a piece of padding rows only (nobody reads it), the distance
+  // back to the tile's piece 0, which the load then fetches again (a cache
+  // hit instead of a stream of padding).  Past the last item the cursor
+  // re-loads the last item's sub-steps.  The cursor is uniform (values read through the first
   // lane, so it stays in scalar registers and a DMA needs no per-lane address
   // arithmetic: the per-lane part is a constant offset), and it moves with
   // selects only: the bases of the item after the cursor's (a_nxt, w_nxt,
@@ -180,14 +199,18 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   int dn = 0, du = 0;
   uint64_t a_src = 0, w_src = 0, s_src = 0;
   uint64_t a_nxt = 0, w_nxt = 0, s_nxt = 0;
+  uint32_t d_src[2] = {0, 0}, d_nxt[2] = {0, 0};
   auto uni = [](uint64_t v) {
     return ((uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(v >> 32)) << 32) |
            (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)v);
   };
-  auto bases = [&](int n, uint64_t& a, uint64_t& w, uint64_t& sc) {
+  auto bases = [&](int n, uint64_t& a, uint64_t& w, uint64_t& sc, uint32_t* d) {
     int tile, nbt;
     item_of(n, tile, nbt);
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, tile * F8_M));
+    const int live = __builtin_amdgcn_readfirstlane((min(F8_M, s_off[slot] + s_cnt[slot] - tile * F8_M) + 31) >> 5);
+#pragma unroll
+    for (int k = 0; k < 2; k++) d[k] = 2 * WV + k < live ? 0u : (uint32_t)(2 * WV + k) * 4096u;
     a = uni((uint64_t)(uintptr_t)(reinterpret_cast<const char*>(p.A) + (size_t)tile * f8_tile_bytes(p.Kd) +
                                   (2 * WV) * 4096));
     w = uni((uint64_t)(uintptr_t)(slot_tensor(reinterpret_cast<const char*>(p.W), p.w_slot_bytes, p.wtab, p.wfield,
@@ -199,7 +222,7 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
                 : reinterpret_cast<const char*>(p.A_sc) + (size_t)tile * f8_tile_scale_bytes(p.Kd);
     sc = uni((uint64_t)(uintptr_t)scb);
   };
-  auto load_next = [&]() { bases(min(dn + 1, my_items - 1), a_nxt, w_nxt, s_nxt); };
+  auto load_next = [&]() { bases(min(dn + 1, my_items - 1), a_nxt, w_nxt, s_nxt, d_nxt); };
   const uint32_t ring_lds = lds_addr(ring);
   const uint32_t lane16 = lane * 16;
   // per-lane offsets of this wavefront's four 1 KB loads of a stream
@@ -216,22 +239,33 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   auto dma_piece = [&](uint32_t sl, int q) {
     // q = 0..3 activation loads, 4..7 weight loads; each 1 KB
     const int b = q & 3;  // load within this wavefront's share: piece (b >> 1), part (b & 1)
-    lds_dma16s(reinterpret_cast<const void*>(q < 4 ? a_src : w_src), voff[b],
+    lds_dma16s(reinterpret_cast<const void*>(q < 4 ? a_src - d_src[b >> 1] : w_src), voff[b],
                sl + (q < 4 ? 0 : F8_SUB) + (4 * WV + b) * 1024);
   };
   auto dma_scales = [&](uint32_t sl) { lds_dma16s_lanes(s_src, sc_voff, sl + sc_lds, sc_mask); };
   // the cursor's move to the next sub-step, in three parts that the
-  // schedule places after different MFMAs (part 2 last: it moves du)
+  // schedule places after different MFMAs (part 2 last: it moves du); the
+  // empty asm statements hold each part there (scalar arithmetic would
+  // otherwise be sunk to the end of the sub-step)
   auto dma_advance = [&](int part) {
     // half 0 -> 1 within a step: +2 KB; half 1 -> the next step's half 0;
     // after the item's last sub-step: the next item's bases
     const bool odd = du & 1, wrap = du == NU - 1;
-    if (part == 0) a_src = wrap ? a_nxt : a_src + (odd ? F8_M * F8_STEP - 2048 : 2048);
-    if (part == 1) w_src = wrap ? w_nxt : w_src + (odd ? 128 * F8_STEP - 2048 : 2048);
+    if (part == 0) {
+      a_src = wrap ? a_nxt : a_src + (odd ? F8_M * F8_STEP - 2048 : 2048);
+      d_src[0] = wrap ? d_nxt[0] : d_src[0];
+      d_src[1] = wrap ? d_nxt[1] : d_src[1];
+      asm volatile("" : "+s"(a_src), "+s"(d_src[0]), "+s"(d_src[1]));
+    }
+    if (part == 1) {
+      w_src = wrap ? w_nxt : w_src + (odd ? 128 * F8_STEP - 2048 : 2048);
+      asm volatile("" : "+s"(w_src));
+    }
     if (part == 2) {
       s_src = wrap ? s_nxt : s_src + (odd ? sc_step : 0);
       dn = wrap ? min(dn + 1, my_items - 1) : dn;
       du = wrap ? 0 : du + 1;
+      asm volatile("" : "+s"(s_src), "+s"(dn), "+s"(du));
     }
   };
 
@@ -247,48 +281,58 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     const i32x4 hi = *reinterpret_cast<const i32x4*>(s + 1024);
     return (i32x8){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
   };
-  // activation row block i of ring slot `slot` (piece 4 wm + i)
+  // this wavefront's activation row block i of ring slot `slot` (piece 2 i + wm)
   auto frag_a = [&](int slot, int buf, int i) {
-    fa[buf][i] = rd8(ring + slot * F8_SLOT + (4 * wm + i) * 2048 + lane * 16);
+    fa[buf][i] = rd8(ring + slot * F8_SLOT + (2 * i + wm) * 2048 + lane * 16);
   };
   // weight piece j of block wn
   auto frag_b = [&](int slot, int buf, int j) {
     fb[buf][j] = rd8(ring + slot * F8_SLOT + F8_SUB + (4 * wn + j) * 2048 + lane * 16);
   };
-  // scale exponents of this lane's token rows (one word, byte i for row
-  // block i) and of its weight row (gate or up scale of block wn for
-  // gate/up)
+  // scale exponents of this lane's token rows (8 bytes, byte b for row
+  // block b; this wavefront's are bytes 2 i + wm) and of its weight row
+  // (gate or up scale of block wn for gate/up)
   auto frag_sc = [&](int slot, int buf) {
     const char* s = ring + slot * F8_SLOT + F8_SC;
-    const uint32_t w = *reinterpret_cast<const uint32_t*>(s + (lane & 31) * 8 + 4 * wm);
+    const uint64_t w = *reinterpret_cast<const uint64_t*>(s + (lane & 31) * 8);
 #pragma unroll
-    for (int i = 0; i < 4; i++) ea[buf][i] = (int)((w >> (8 * i)) & 0xFFu);
+    for (int i = 0; i < 4; i++) ea[buf][i] = (int)((w >> (16 * i + 8 * wm)) & 0xFFu);
     const float* ws = reinterpret_cast<const float*>(s + 256 + 16 * wn);
     eb[buf] = (int)ue8m0_of(GATEUP ? ws[((lane >> 4) & 1)] : ws[0]);
   };
 
   // Sub-step g, operands in registers (buffer buf), its slot sc already
-  // read: four groups i of four MFMAs (row block i against weight pieces j).
-  // During group i: activation row block i and weight piece i of sub-step
-  // g + 1 (slot sn); the scale exponents in group 3.  This wavefront's DMA
-  // of sub-step g + NSS goes into slot sc during groups 0 and 1 (as early as
-  // possible: the ring holds only a few 32 KB sub-steps).  Then, once
-  // sub-step g + 2 has landed (F8_DMA loads per later sub-step: NSS - 2 of
-  // them) and every wavefront holds sub-step g + 1, the barrier.
-  // last: the item's last sub-step, which reads nothing of the next one
-  // (its first fragments are read after the epilogue, so that no operand
-  // registers are held across it)
+  // read: four groups i of four MFMAs (row block 2 i + wm against weight
+  // pieces j), of which only the first nb (this wavefront's live row blocks)
+  // run: the others are skipped on a uniform branch each, while the loads
+  // keep their places.  During group i: activation row block i (if live)
+  // and weight piece i of sub-step g + 1 (slot sn); the scale exponents in
+  // group 3.  This wavefront's DMA of sub-step g + NSS goes into slot sc
+  // during groups 0 and 1 (as early as possible: the ring holds only a few
+  // 32 KB sub-steps), its scale load and the cursor's move in groups 2 and
+  // 3.  Then, once sub-step g + 2 has landed (F8_DMA loads per later
+  // sub-step: NSS - 2 of them) and every wavefront holds sub-step g + 1,
+  // the barrier.  last: the item's last sub-step, which reads nothing of
+  // the next one (its first fragments are read after the epilogue, so that
+  // no operand registers are held across it)
   int sc = 0, sn = 1;
-  auto substep = [&](int buf, bool first, bool last) {
+  // 1, from a move the compiler cannot see through: row block 0's MFMAs
+  // run under it, so that like the others each sits in a block of its own
+  // (unconditional ones would be sunk past the branches, to the barrier)
+  int on;
+  asm volatile("s_mov_b32 %0, 1" : "=s"(on));
+  auto substep = [&](int buf, bool first, bool last, int nb) {
     const f32x16 zero = {};
     const uint32_t sl = ring_lds + sc * F8_SLOT;
 #pragma unroll
     for (int i = 0; i < 4; i++) {
 #pragma unroll
       for (int j = 0; j < 4; j++) {
-        acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[buf][j], fa[buf][i], first ? zero : acc[i][j],
-                                                                     0, 0, 0, eb[buf], 0, ea[buf][i]);
-        if (j == 0 && !last) frag_a(sn, buf ^ 1, i);
+        if (i == 0 ? on != 0 : i < nb) {
+          acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fb[buf][j], fa[buf][i], first ? zero : acc[i][j],
+                                                                       0, 0, 0, eb[buf], 0, ea[buf][i]);
+          if (j == 0 && !last) frag_a(sn, buf ^ 1, i);
+        }
         if (j == 1 && !last) frag_b(sn, buf ^ 1, i);
         if (j == 2 && i == 3 && !last) frag_sc(sn, buf ^ 1);
         __builtin_amdgcn_sched_barrier(0);
@@ -316,7 +360,7 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
 
   // prologue: sub-steps 0 .. NSS - 1 into slots 0 .. NSS - 1; sub-steps 0
   // and 1 landed before the first reads
-  bases(0, a_src, w_src, s_src);
+  bases(0, a_src, w_src, s_src, d_src);
   load_next();
 #pragma unroll 1
   for (int g = 0; g < F8_NSS; g++) {
@@ -351,25 +395,29 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
     const int row0 = tile * F8_M;
     const int slot = __builtin_amdgcn_readfirstlane(slot_of_row(s_off, p.S, row0));
     const int nvalid = __builtin_amdgcn_readfirstlane(min(F8_M, s_off[slot] + s_cnt[slot] - row0));
+    // this wavefront's live row blocks 2 i + wm, i < nb (a tile's valid rows
+    // come first; row blocks of padding only are skipped)
+    const int nb = __builtin_amdgcn_readfirstlane((((nvalid + 31) >> 5) + 1 - wm) >> 1);
     const uint64_t tstart = p.timing ? __builtin_amdgcn_s_memrealtime() : 0;
     // the bases the DMA cursor moves to when it passes its item's last
     // sub-step (during this item, since the cursor runs F8_NSS <= NU
     // sub-steps ahead)
     load_next();
 
-    // NU = 2 KT >= 4 sub-steps, an even number
-    substep(0, true, false);
-    substep(1, false, false);
+    // NU = 2 KT >= 4 sub-steps, an even number (row block 0 is always live:
+    // a wavefront without live rows, nb = 0, computes it and drops it)
+    substep(0, true, false, nb);
+    substep(1, false, false, nb);
 #pragma unroll 1
     for (int u = 2; u < NU - 2; u += 2) {
-      substep(0, false, false);
-      substep(1, false, false);
+      substep(0, false, false, nb);
+      substep(1, false, false, nb);
     }
-    substep(0, false, false);
-    substep(1, false, true);
+    substep(0, false, false, nb);
+    substep(1, false, true, nb);
 
-    // Epilogue.  Lane l of tile (i, j) holds token row 128 wm + 32 i + (l & 31)
-    // and, in element e, packed weight row 8 (e / 4) + 4 (l / 32) + e % 4 of
+    // Epilogue (live row blocks only).  Lane l of tile (i, j) holds token
+    // row 32 (2 i + wm) + (l & 31) and, in element e, packed weight row 8 (e / 4) + 4 (l / 32) + e % 4 of
     // piece j of block wn (gate/up: rows 0..15 gate, 16..31 the matching up
     // columns, so gate and up of a column are elements e and e + 8).
     int lid;
@@ -391,20 +439,25 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
       // (exact scaling), saturated at 448, round to nearest even.  Lane l
       // holds bytes 4 hl .. 4 hl + 3 and 8 + 4 hl .. of the 16-byte chunk
       // 4 wn + j of its row in the down GEMM's step nbt, which sits at load
-      // 2 wn + (j & 1), lane (l & 31) + 32 (j >> 1) of piece 4 wm + i.
+      // 2 wn + (j & 1), lane (l & 31) + 32 (j >> 1) of piece 2 i + wm, with
+      // the scale exponent at byte 8 (l & 31) + 2 i + wm of the step's 256.
       char* hb = static_cast<char*>(p.C) + (size_t)tile * f8_tile_bytes(p.Nout) + (size_t)nbt * (F8_M * F8_STEP) +
-                 (4 * wm) * 4096 + (2 * wn) * 1024 + l31 * 16 + 4 * hl;
-      uint32_t ew = 0;
-      // two row blocks per exchange (one barrier for both)
+                 (2 * wn) * 1024 + l31 * 16 + 4 * hl;
+      uint8_t* hs = p.C_sc + (size_t)tile * f8_tile_scale_bytes(p.Nout) + (size_t)nbt * 256 + l31 * 8 + wm;
+      // two row blocks per exchange (one barrier for both, also where they
+      // are not live: every wavefront passes the same barriers)
 #pragma unroll
       for (int ip = 0; ip < 2; ip++) {
         float h[2][4][8];
         float m[2] = {0.f, 0.f};
 #pragma unroll
         for (int ii = 0; ii < 2; ii++) {
+          // (also for row blocks that are not live, whose values are
+          // dropped: a branch here makes the compiler spill)
+          const int i = 2 * ip + ii;
 #pragma unroll
           for (int j = 0; j < 4; j++) {
-            f32x16 v = acc[2 * ip + ii][j];  // (one tile at a time, as below)
+            f32x16 v = acc[i][j];  // (one tile at a time, as below)
             asm volatile("" : "+v"(v));
 #pragma unroll
             for (int e = 0; e < 8; e++) {
@@ -413,20 +466,21 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
             }
           }
           m[ii] = fmaxf(m[ii], __shfl_xor(m[ii], 32));
-          if (hl == 0) xamax[wn * F8_M + 128 * wm + 32 * (2 * ip + ii) + l31] = m[ii];
+          if (hl == 0) xamax[wn * F8_M + 32 * (2 * i + wm) + l31] = m[ii];
         }
         wait_lgkm0();
         barrier_nofence();
 #pragma unroll
         for (int ii = 0; ii < 2; ii++) {
           const int i = 2 * ip + ii;
-          const float mm = fmaxf(m[ii], xamax[(1 - wn) * F8_M + 128 * wm + 32 * i + l31]);
+          if (i >= nb) continue;
+          const float mm = fmaxf(m[ii], xamax[(1 - wn) * F8_M + 32 * (2 * i + wm) + l31]);
           float sc = mm > 0.f ? mm / 448.0f : 1.0f;
           uint32_t bits = __float_as_uint(sc);
           if (mm > 0.f && (bits & 0x7FFFFFu)) bits = (bits & 0xFF800000u) + 0x800000u;
           const uint32_t e8 = (bits >> 23) & 0xFFu;
           const int k = (int)e8 - 127;
-          ew |= e8 << (8 * i);
+          if (wn == 0 && hl == 0) hs[2 * i] = (uint8_t)e8;
 #pragma unroll
           for (int j = 0; j < 4; j++) {
             float q[8];
@@ -436,16 +490,13 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
             w0 = __builtin_amdgcn_cvt_pk_fp8_f32(q[2], q[3], w0, true);
             uint32_t w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[4], q[5], 0, false);
             w1 = __builtin_amdgcn_cvt_pk_fp8_f32(q[6], q[7], w1, true);
-            char* d = hb + i * 4096 + (j & 1) * 1024 + (j >> 1) * 512;
+            char* d = hb + (2 * i + wm) * 4096 + (j & 1) * 1024 + (j >> 1) * 512;
             *reinterpret_cast<uint32_t*>(d) = w0;
             *reinterpret_cast<uint32_t*>(d + 8) = w1;
           }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
-      if (wn == 0 && hl == 0)
-        *reinterpret_cast<uint32_t*>(p.C_sc + (size_t)tile * f8_tile_scale_bytes(p.Nout) + (size_t)nbt * 256 +
-                                     l31 * 8 + 4 * wm) = ew;
     } else {
       // bf16 rows of y_perm, as in the bf16 large-tile kernel: lanes l and
       // l + 32 hold the two 8-byte halves of a row's 8-column chunk; one
@@ -459,7 +510,8 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
       char* yb = static_cast<char*>(p.C) + (size_t)row0 * ld + (size_t)(nbt * NCOLS + 128 * wn + 8 * hl) * 2;
 #pragma unroll
       for (int i = 0; i < 4; i++) {
-        const int r = 128 * wm + 32 * i + l31;
+        if (i >= nb) continue;
+        const int r = 32 * (2 * i + wm) + l31;
         char* yr = yb + r * ld;
 #pragma unroll
         for (int j = 0; j < 4; j++) {
@@ -489,17 +541,58 @@ __device__ __forceinline__ void f8_body(const F8Args& p, char* ring, float* xama
   __builtin_amdgcn_s_waitcnt(TEMPO_VMCNT_IMM(0));
 }
 
+// The M-tiles in cost order, by one wavefront: the cost of an item is set
+// by the live 32-row blocks of its busier wavefront, ceil(L / 2) for a tile
+// with L live blocks (1..4); tiles go by that class, highest first, and by
+// index within a class (a stable counting sort, the same in every
+// workgroup).
+__device__ void f8_tile_order(const int32_t* s_off, const int32_t* s_cnt, int S, int NT, uint16_t* ord) {
+  const int lane = threadIdx.x & 63;
+  auto cls = [&](int t) {
+    const int row0 = t * F8_M;
+    const int s = slot_of_row(s_off, S, row0);
+    const int live = (min(F8_M, s_off[s] + s_cnt[s] - row0) + 31) >> 5;
+    return min(4, max(1, (live + 1) >> 1));
+  };
+  int base[5] = {0, 0, 0, 0, 0};
+  for (int t0 = 0; t0 < NT; t0 += 64) {
+    const int c = t0 + lane < NT ? cls(t0 + lane) : 0;
+#pragma unroll
+    for (int k = 1; k <= 4; k++) base[k] += __popcll(__ballot(c == k));
+  }
+  // start of each class in the list: class 4 first
+  base[1] = base[4] + base[3] + base[2];
+  base[2] = base[4] + base[3];
+  base[3] = base[4];
+  base[4] = 0;
+  const uint64_t below = (1ull << lane) - 1;
+  for (int t0 = 0; t0 < NT; t0 += 64) {
+    const int c = t0 + lane < NT ? cls(t0 + lane) : 0;
+#pragma unroll
+    for (int k = 1; k <= 4; k++) {
+      const uint64_t m = __ballot(c == k);
+      if (c == k) ord[base[k] + __popcll(m & below)] = (uint16_t)(t0 + lane);
+      base[k] += __popcll(m);
+    }
+  }
+}
+
 template <bool GATEUP>
 __global__ __launch_bounds__(256, 1) void k_gemm_big_f8(const F8Args p) {
   __shared__ __attribute__((aligned(1024))) char ring[F8_NSS * F8_SLOT];
   __shared__ float xamax[2 * F8_M];
   __shared__ int32_t s_off[kMaxS + 1];
   __shared__ int32_t s_cnt[kMaxS];
+  __shared__ uint16_t s_tord[F8_MAX_SORT];
   const int tid = threadIdx.x;
   for (int s = tid; s <= p.S; s += 256) s_off[s] = p.slot_offsets[s];
   for (int s = tid; s < p.S; s += 256) s_cnt[s] = p.slot_counts[s];
   __syncthreads();
-  f8_body<GATEUP>(p, ring, xamax, s_off, s_cnt, __builtin_amdgcn_readfirstlane(tid >> 6));
+  const int NT = max(0, min(s_off[p.S] / F8_M, p.max_tiles));
+  const int sorted = NT <= F8_MAX_SORT ? 1 : 0;
+  if (sorted && tid < 64) f8_tile_order(s_off, s_cnt, p.S, NT, s_tord);
+  __syncthreads();
+  f8_body<GATEUP>(p, ring, xamax, s_off, s_cnt, s_tord, sorted, __builtin_amdgcn_readfirstlane(tid >> 6));
 }
 
 }  // namespace

@@ -45,7 +45,10 @@ def test_large_tile_gemm_has_no_spills_and_fits_lds(tmp_path, which):
     for name, f in big.items():
         assert f["vgpr_spill_count"] == 0, (name, f)
         # scalar spills go to lanes of a VGPR (v_writelane / v_readlane), no
-        # memory access; the bf16 kernel has none, the fp8 one a few dozen
-        assert f["sgpr_spill_count"] <= (0 if which == "bf16" else 64), (name, f)
+        # memory access; the bf16 kernel has none, the fp8 one several dozen
+        # (its DMA cursor keeps the next item's bases and per-piece offsets
+        # in scalar registers; the spilled values are read per item, not
+        # per sub-step)
+        assert f["sgpr_spill_count"] <= (0 if which == "bf16" else 96), (name, f)
         assert f["group_segment_fixed_size"] <= 160 * 1024, (name, f)
         assert f.get("private_segment_fixed_size", 0) == 0, (name, f)
