@@ -18,6 +18,12 @@ under profiles/).
     python -m paper_2608_13057_amd.measure snap --out MD
         the tile-aware split (TEMPO_PLAN_SNAP_TILES) against the plain one:
         M-tiles, activated slots and block time per workload and batch size
+    python -m paper_2608_13057_amd.measure library --out MD
+        reference points, not part of the path: the vendor GEMM (hipBLASLt,
+        through torch) on dense GEMMs of the prefill shapes, fp8 and bf16
+    python -m paper_2608_13057_amd.measure readbw --out MD
+        the attainable HBM rates of plain torch kernels: a row-wise max
+        (reads), a copy (reads and writes) and a fill (writes)
 
 The traffic summary ends with a `traffic_json:` line that bench.py reads; it
 carries a hash of the stage-2 sources, and bench.py reports no traffic once
@@ -449,6 +455,76 @@ def _snap(args):
     return 0
 
 
+def _timed_us(f, n=20):
+    """Mean time of f over n calls after three warm-up calls, from events."""
+    import torch
+
+    for _ in range(3):
+        f()
+    torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(n):
+        f()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / n * 1e3
+
+
+def _library(args):
+    import torch
+
+    torch.cuda.set_device(0)
+    # the padded and unpadded gate/up GEMM of the Qwen3 prefill share at
+    # 256-row tiles, its down GEMM, and a large square one
+    shapes = [(14336, 3072, 4096), (11486, 3072, 4096), (14336, 4096, 1536), (8192, 8192, 8192)]
+    lines = ["# Vendor GEMM on dense GEMMs of the prefill shapes (reference points)", "",
+             "Command (repo root, MI355X):", "", "```", args.command, "```", "",
+             "torch's `_scaled_mm` (fp8 e4m3fn operands, tensor scales, bf16 out; hipBLASLt on ROCm) and bf16 `@`, "
+             "20 timed calls after 3 warm-up calls, random operands; one weight matrix per GEMM (no grouping, no gather).",
+             "", "| M x N x K | fp8 us | fp8 TFLOP/s | bf16 us | bf16 TFLOP/s |", "|---|---|---|---|---|"]
+    for m, n, k in shapes:
+        a = torch.randn(m, k, device="cuda").to(torch.float8_e4m3fn)
+        b = torch.randn(n, k, device="cuda").to(torch.float8_e4m3fn)
+        one = torch.tensor(1.0, device="cuda")
+        t8 = _timed_us(lambda: torch._scaled_mm(a, b.t(), scale_a=one, scale_b=one, out_dtype=torch.bfloat16))
+        ab = torch.randn(m, k, device="cuda", dtype=torch.bfloat16)
+        bb = torch.randn(k, n, device="cuda", dtype=torch.bfloat16)
+        t16 = _timed_us(lambda: ab @ bb)
+        fl = 2.0 * m * n * k
+        lines.append(f"| {m} x {n} x {k} | {t8:.1f} | {fl / t8 / 1e6:.0f} | {t16:.1f} | {fl / t16 / 1e6:.0f} |")
+        print(lines[-1], flush=True)
+        del a, b, ab, bb
+    lines.append("")
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines))
+    return 0
+
+
+def _readbw(args):
+    import torch
+
+    torch.cuda.set_device(0)
+    lines = ["# Attainable HBM rates of plain kernels", "", "Command (repo root, MI355X):", "", "```", args.command, "```",
+             "", "torch kernels over fp32 tensors, 10 timed calls after 3 warm-up calls; bytes counted once each way.",
+             "", "| size | row max (4096 per row) read GB/s | copy read+write GB/s | fill write GB/s |", "|---|---|---|---|"]
+    for gib in (1, 4):
+        n = gib * (1 << 30) // 4
+        x = torch.randn(n, device="cuda")
+        y = torch.empty_like(x)
+        rd = n * 4 / _timed_us(lambda: torch.amax(x.view(-1, 4096), dim=1), 10) / 1e3
+        cp = 2 * n * 4 / _timed_us(lambda: y.copy_(x), 10) / 1e3
+        wr = n * 4 / _timed_us(lambda: y.fill_(1.0), 10) / 1e3
+        lines.append(f"| {gib} GiB | {rd:.0f} | {cp:.0f} | {wr:.0f} |")
+        print(lines[-1], flush=True)
+        del x, y
+    lines.append("")
+    with open(args.out, "w") as fh:
+        fh.write("\n".join(lines))
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -491,8 +567,15 @@ def main(argv=None):
     n.add_argument("--calls", type=int, default=30)
     n.add_argument("--out", required=True)
     n.add_argument("--command", default="")
+    lb = sub.add_parser("library", help="vendor GEMM on dense GEMMs of the prefill shapes (reference points)")
+    lb.add_argument("--out", required=True)
+    lb.add_argument("--command", default="python -m paper_2608_13057_amd.measure library --out <this file>")
+    rb = sub.add_parser("readbw", help="attainable HBM rates of plain kernels")
+    rb.add_argument("--out", required=True)
+    rb.add_argument("--command", default="python -m paper_2608_13057_amd.measure readbw --out <this file>")
     a = ap.parse_args(argv)
-    return {"run": _run, "traffic": _traffic, "stats": _stats, "snap": _snap, "mfma": _mfma}[a.cmd](a)
+    return {"run": _run, "traffic": _traffic, "stats": _stats, "snap": _snap, "mfma": _mfma, "library": _library,
+            "readbw": _readbw}[a.cmd](a)
 
 
 if __name__ == "__main__":
