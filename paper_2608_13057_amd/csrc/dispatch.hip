@@ -61,6 +61,7 @@ constexpr int kScanBlocks = 32;  // above this many count blocks, k_scan compute
 constexpr int kSmallWaves = 16;
 constexpr int kSmallRounds = 8;
 constexpr int kSmallMaxE = 256;
+constexpr int kSmallScalesMaxP = 4096;  // pairs up to which fp8 batches with permuted scales use it
 
 // ---------------------------------------------------------------------------
 // shared pieces
@@ -1018,12 +1019,16 @@ hipError_t launch_dispatch(const tempo_moe_shape& s, const tempo_plan& plan, con
 
   copy_scales = copy_scales && s.dtype != TEMPO_BF16;
   float* const xps = copy_scales ? out.x_perm_scale : nullptr;
-  // one workgroup for decode-sized batches whose rows (and fp8 scales) stage
-  // 2 reads from the token rows; sampled replicas always take this path
-  // (then a row-copy launch for what is asked for)
+  // one workgroup for decode-sized batches whose rows stage 2 reads from the
+  // token rows, and for sampled replicas (then a row-copy launch for what is
+  // asked for).  fp8 batches whose activation scales stage 2 reads permuted
+  // take it up to kSmallScalesMaxP pairs, with a launch that copies the
+  // scales: for more pairs the single workgroup's ranking costs more than
+  // count + place (measured: 2048 pairs 15.6 against 20.3 us; 8192 pairs
+  // 18.6 against 15.7 us)
   const bool small = P <= kSmallRounds * kSmallWaves * 64 && s.E <= kSmallMaxE;
   if (sample && !dispatch_sample_supported(s)) return hipErrorNotSupported;
-  if (sample || (small && !copy_rows && !copy_scales)) {
+  if (sample || (small && !copy_rows && (!copy_scales || P <= kSmallScalesMaxP))) {
     const int KW = sample ? s.S : s.E;
     const size_t lds = (size_t)kSmallWaves * KW * 8 + (size_t)(kSmallWaves * KW + 5 * s.E) * sizeof(int32_t);
     hipLaunchKernelGGL(k_dispatch_small, dim3(1), dim3(kSmallWaves * 64), lds, st, topk_ids, P, Pv, s.K, s.E, s.S,
