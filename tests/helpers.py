@@ -85,6 +85,23 @@ def rel_err_rows(y: np.ndarray, ref: np.ndarray, rows: np.ndarray) -> float:
     return float(np.max(d / np.maximum(n, 1e-30)))
 
 
+def mirror_err_rows(y: np.ndarray, ref: np.ndarray, rows: np.ndarray) -> float:
+    """Like rel_err_rows against the oracle's mirror mode, counting per
+    element only what exceeds one bf16 ulp of the larger of the two values.
+    The mirror mode rounds y to bf16 where the GPU does, so an fp32 sum that
+    lands on the other side of a rounding boundary moves y by one ulp (up to
+    2^-7 of the row's largest value when it is that value) without any error
+    upstream; such flips are bounded by the share of identical elements, and
+    what remains beyond them is the effect of h flips and accumulation
+    order."""
+    if len(rows) == 0:
+        return 0.0
+    a, b = y[rows], ref[rows]
+    d = np.maximum(np.abs(a - b) - bf16_ulp(np.maximum(np.abs(a), np.abs(b))), 0.0).max(axis=1)
+    n = np.abs(b).max(axis=1)
+    return float(np.max(d / np.maximum(n, 1e-30)))
+
+
 def tile_sample(d: dict, m_tile: int, rng) -> np.ndarray:
     """Tokens of a stage-1 result stratified by M-tile: for every activated
     slot, one random real row of each of its M-tiles and its last real row;
