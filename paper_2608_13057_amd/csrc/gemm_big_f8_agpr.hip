@@ -20,13 +20,20 @@
 //   64 contraction elements 64h .. 64h + 63 of the step: a sub-step.
 // * Per tile and step, the 256 activation-row scale exponents (UE8M0 bytes)
 //   sit at byte 8 (r & 31) + (r >> 5) of a 256-byte block, so a lane reads the
-//   exponents of its four row blocks as one word.
+//   exponents of its token row in all eight row blocks as one 8-byte word.
 // * A work item is (256-row M-tile, 256 packed weight rows); four wavefronts
-//   in a 2 x 2 arrangement each own 128 x 128 of it as 4 x 4 MFMA tiles of
+//   in a 2 x 2 arrangement, wavefront (wm, wn) owning the row blocks 2i + wm
+//   (i = 0..3) against the 128 weight rows of half wn, as 4 x 4 MFMA tiles of
 //   32 x 32 with the accumulators in AGPRs; the MFMAs take the weights as
 //   their first operand (a lane owns one token row and runs of four output
 //   columns).  Items are never split and accumulate their sub-steps in
 //   order, so a row's result depends only on its own inputs.
+// * A tile's valid rows come first, so its row blocks of padding only are
+//   its last ones: their MFMAs and fragment reads are skipped, their DMA
+//   pieces re-load a live piece, and neither the pack nor the gate/up
+//   epilogue writes them.  Items are dealt in an order sorted by their
+//   live row blocks, in rounds alternately forwards and backwards over the
+//   workgroups.
 // * The operands of a sub-step (16 KB of activations, 16 KB of weights, and
 //   the step's scale exponents) stream through an LDS ring of NSS slots by
 //   DMA; one barrier per sub-step, the fragment reads of sub-step u + 1 and
