@@ -16,7 +16,8 @@ roofline of the dominant kernel (the gate/up GEMM: MFMA-bound at prefill,
 HBM-bound at decode), the same for the bf16 prefill share and for two
 flat-regime decode shares (`roofline_flat`: the Qwen3 share, 512 tokens,
 mixed regime; `roofline_flat_dsv3`: the DeepSeek-V3 share, 256 tokens, most
-slots weight-streaming), the fitted max-affine profile (a, b, c, beta, n*) of each one's
+slots weight-streaming), stage 2 at a grid point where every slot is in the
+linear regime (`roofline_linear`: 32 slots of 1024 rows, UE8M0 fp8), the fitted max-affine profile (a, b, c, beta, n*) of each one's
 dtype and M-tile, per-stage times, and the CPU oracle timed on the host
 cores as a baseline.
 
@@ -58,6 +59,8 @@ def parse():
     ap.add_argument("--flat2-workload", default="dsv3_decode_fp8",
                     help="a second weight-streaming share (most slots far below n*) for roofline_flat_dsv3")
     ap.add_argument("--no-flat", action="store_true")
+    ap.add_argument("--no-linear", action="store_true",
+                    help="skip the linear-regime grid point (32 slots of 1024 rows, UE8M0 fp8, 256-row tiles)")
     ap.add_argument("--plan", default=None)
     ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, 128 above, 256 for bf16 beyond 128 rows per expert")
     ap.add_argument("--seed", type=int, default=0)
@@ -337,6 +340,29 @@ def roofline(m, copy_gbs=None):
     return out
 
 
+def linear_point(torch, G=32, n=1024):
+    """Stage 2 (both GEMMs) where every slot is in the linear regime: G slots
+    of the Qwen3-235B shape with n rows each (four full 256-row tiles per
+    slot), UE8M0 fp8, timed by the stage-4 harness (median of 30 event-timed
+    executions); flops 6HI per pair against the fp8 MFMA peak."""
+    from paper_2608_13057_amd import profile
+
+    h = profile.Harness(dtype="fp8mx", m_tile=256, max_tokens=G * n)
+    r = h.point(G, n, reps=30, scopes=("gemm",))[0]
+    H, I = h.H, h.I
+    flops = G * n * 6.0 * H * I
+    achieved = flops / (r["t_us"] * 1e-6) / 1e12
+    del h
+    torch.cuda.empty_cache()
+    log(f"linear-regime point G={G} n={n}: stage 2 {r['t_us']:.1f} us, {achieved:.0f} TFLOP/s")
+    return {"bound": "mfma", "achieved": achieved, "peak": MFMA_PEAK_TFLOPS["fp8mx"], "unit": "TFLOP/s",
+            "frac": achieved / MFMA_PEAK_TFLOPS["fp8mx"], "scope": "stage 2 (gate/up and down GEMMs)",
+            "workload": f"{G} slots x {n} rows, Qwen3-235B shape (H {H}, I {I}), fp8 UE8M0, M-tile 256, "
+                        "one weight set of 32 slots (604 MB, beyond the Infinity Cache)",
+            "G": G, "N": G * n, "stage2_us": r["t_us"], "p10_us": r["p10"], "p90_us": r["p90"],
+            "flops_per_launch": flops}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -417,6 +443,8 @@ def main():
                                      "stages_us": f2.stage_us,
                                      "fit": measure.committed_fit(sh2, f2.wl.dtype, f2.m_tile)}
         del f2
+    if not args.no_linear:
+        out["roofline_linear"] = linear_point(torch)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
         out["cpu_baseline"] = cpu_baseline(wl, m.plan, m.x, m.xs, m.w13, m.s13, m.w2, m.s2, m.m_tile,
