@@ -16,8 +16,9 @@ roofline of the dominant kernel (the gate/up GEMM: MFMA-bound at prefill,
 HBM-bound at decode), the same for the bf16 prefill share and for two
 flat-regime decode shares (`roofline_flat`: the Qwen3 share, 512 tokens,
 mixed regime; `roofline_flat_dsv3`: the DeepSeek-V3 share, 256 tokens, most
-slots weight-streaming), stage 2 at a grid point where every slot is in the
-linear regime (`roofline_linear`: 32 slots of 1024 rows, UE8M0 fp8), the fitted max-affine profile (a, b, c, beta, n*) of each one's
+slots weight-streaming), with `--linear` stage 2 at a grid point where every
+slot is in the linear regime (`roofline_linear`: 32 slots of 1024 rows,
+UE8M0 fp8), the fitted max-affine profile (a, b, c, beta, n*) of each one's
 dtype and M-tile, per-stage times, and the CPU oracle timed on the host
 cores as a baseline.
 
@@ -59,8 +60,10 @@ def parse():
     ap.add_argument("--flat2-workload", default="dsv3_decode_fp8",
                     help="a second weight-streaming share (most slots far below n*) for roofline_flat_dsv3")
     ap.add_argument("--no-flat", action="store_true")
-    ap.add_argument("--no-linear", action="store_true",
-                    help="skip the linear-regime grid point (32 slots of 1024 rows, UE8M0 fp8, 256-row tiles)")
+    ap.add_argument("--linear", action="store_true",
+                    help="add the linear-regime grid point (32 slots of 1024 rows, UE8M0 fp8, 256-row tiles); off by "
+                         "default: it runs the headline's gate/up kernel on another workload, which would mix into "
+                         "that kernel's average in a kernel trace of the same command")
     ap.add_argument("--plan", default=None)
     ap.add_argument("--m-tile", type=int, default=0, help="0: 64 for decode-sized batches, 128 above, 256 for bf16 beyond 128 rows per expert")
     ap.add_argument("--seed", type=int, default=0)
@@ -443,7 +446,7 @@ def main():
                                      "stages_us": f2.stage_us,
                                      "fit": measure.committed_fit(sh2, f2.wl.dtype, f2.m_tile)}
         del f2
-    if not args.no_linear:
+    if args.linear:
         out["roofline_linear"] = linear_point(torch)
     if not args.no_cpu_baseline:
         log("timing the CPU oracle")
