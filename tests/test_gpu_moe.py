@@ -26,6 +26,7 @@ from helpers import (Case, bf16_to_f64, identical_share, mirror_err_rows, mirror
 pytestmark = pytest.mark.gpu
 
 TOL_EXACT = {"bf16": 1e-2, "fp8": 5e-2, "fp8mx": 5e-2}
+TOL_EXACT_FP8_H256 = 8e-2  # exact mode, fp8 paths at H 256 with tens of thousands of tokens
 TOL_MIRROR = {"bf16": 1e-3, "fp8": 2e-2, "fp8mx": 2e-2}
 MIRROR_IDENTICAL = {"bf16": 0.999, "fp8": 0.85, "fp8mx": 0.85}
 
@@ -163,6 +164,58 @@ def test_forward_256_row_tiles_every_live_block_count(dtype):
         if mode == "mirror":
             assert identical_share(got[loc], ref[loc]) >= MIRROR_IDENTICAL[dtype]
     assert np.all(y[none] == 0)
+
+
+@pytest.mark.parametrize("dtype,I", [("fp8mx", 512), ("bf16", 128)])
+def test_forward_256_row_tiles_shallow_items(dtype, I):
+    """The large-tile kernels with the fewest sub-steps per item and several
+    items per workgroup: H 256 (a UE8M0 gate/up item is then four sub-steps,
+    as many as its operand ring holds; both GEMMs run the same item cursor)
+    and, for bf16, I 128 (a down item of eight sub-steps, one less than its
+    ring), 64 experts of 1000..1199 rows in over 300 M-tiles, so the DMA
+    cursor of every workgroup is an item or more ahead when an item starts.
+    y on a token sample with one row of every M-tile and every slot's last
+    row against the fp64 oracle (exact and mirror modes); tokens with no
+    local pair exactly zero."""
+    from paper_2608_13057_amd import synth
+
+    rng = np.random.default_rng(23)
+    E, H = 64, 256
+    counts = rng.integers(1000, 1200, E)
+    ids = np.repeat(np.arange(E, dtype=np.int32), counts)
+    rng.shuffle(ids)
+    T = ids.size
+    pl = synth.placement_local_hot(E, E, 0)  # one slot per expert
+    w = rng.uniform(0.1, 1.0, (T, 1)).astype(np.float32)
+    wl = synth.Workload("shallow", dtype, T, T, 1, E, H, I, 0.0, pl, {"uniform": synth.plan_uniform(pl, E)},
+                        ids.reshape(T, 1), w, 0)
+    c = Case(wl, "uniform", 256)
+    print(f"[shallow {dtype} I={I}] running, {T} tokens", flush=True)
+    y, _ = _run_forward(c)
+    d = c.oracle_dispatch()
+    assert np.array_equal(to_host(c.disp.slot_counts), d["slot_counts"])
+    ntiles = int(sum(-(-int(n) // 256) for n in d["slot_counts"]))
+    assert ntiles > 256  # more items than workgroups in both GEMMs
+    loc, none = _local_rows(d, c.T_valid)
+    assert np.all(y[none] == 0)
+    pick = tile_sample(d, 256, np.random.default_rng(2))
+    sel = np.zeros(T, np.uint8)
+    sel[pick] = 1
+    got = bf16_to_f64(y)
+    ref = _oracle_y(c, d, "mirror", sel)
+    err_m = mirror_err_rows(got, ref, pick)
+    same = identical_share(got[pick], ref[pick])
+    ref = _oracle_y(c, d, "exact", sel)
+    err = rel_err_rows(got, ref, pick)
+    print(f"[shallow {dtype} I={I}] {ntiles} tiles, sampled {len(pick)} tokens exact err={err:.2e} "
+          f"mirror err={err_m:.2e} identical={same:.4f}")
+    assert err_m <= TOL_MIRROR[dtype] and same >= MIRROR_IDENTICAL[dtype]
+    # fp8 at H 256: the gate/up contraction spans two 128-element scale
+    # blocks, so the e4m3 rounding of x, the weights and h averages over far
+    # fewer terms than at the model widths the 5e-2 bar is set for (measured
+    # here: 5.7e-2); the mirror mode above, which rounds where the GPU
+    # rounds, is the check of the kernel
+    assert err <= (TOL_EXACT[dtype] if dtype == "bf16" else TOL_EXACT_FP8_H256)
 
 
 @pytest.mark.parametrize("name,m_tile", [("tiny", 64), ("tiny", 256), ("tiny_fp8", 128), ("tiny_fp8mx", 256)])
