@@ -281,6 +281,56 @@ def test_forward_256_row_tiles_random_shapes(dtype, seed):
     _check_many_rows(dtype, err, err_m, same)
 
 
+@pytest.mark.parametrize("m_tile", [64, 128, 192, 256])
+@pytest.mark.parametrize("dtype", ["bf16", "fp8", "fp8mx"])
+def test_forward_stream_k_random_shapes(dtype, m_tile):
+    """The stream-K kernel on random shapes: H and I multiples of 128 (at
+    M 256, H an odd multiple of 128, where the large-tile kernels do not
+    apply and stream-K takes the tile), 3..24 experts of 1..700 rows routed
+    top-1..top-4, some with a second slot, a few padding tokens; stage 1
+    bit-exact, y on a token sample (one row of every M-tile, every slot's
+    last row and 400 random tokens) against the fp64 oracle in exact and
+    mirror modes; tokens with no local pair exactly zero."""
+    from paper_2608_13057_amd import synth
+
+    rng = np.random.default_rng(1000 + 10 * m_tile + ["bf16", "fp8", "fp8mx"].index(dtype))
+    H = int(rng.choice([128, 384, 640, 896] if m_tile == 256 else [128, 256, 512, 896]))
+    I = int(rng.choice([128, 256, 384, 640]))
+    E = int(rng.integers(3, 25))
+    K = int(rng.integers(1, min(E, 4) + 1))
+    counts = rng.integers(1, 700, E)
+    T = int(counts.sum()) // K + 1
+    ids = np.empty((T, K), np.int32)
+    for t in range(T):
+        ids[t] = rng.choice(E, K, replace=False)
+    pl = synth.placement_local_hot(E, E, int(rng.integers(0, min(E, 5) + 1)))
+    w = rng.uniform(0.1, 1.0, (T, K)).astype(np.float32)
+    wl = synth.Workload("random_sk", dtype, T, T - int(rng.integers(0, 3)), K, E, H, I, 0.0, pl,
+                        {"uniform": synth.plan_uniform(pl, E)}, ids, w, 7)
+    c = Case(wl, "uniform", m_tile)
+    print(f"[stream-K {dtype} M={m_tile}] T={T} K={K} E={E} S={pl.slot_expert.size} H={H} I={I}", flush=True)
+    y, _ = _run_forward(c)
+    d = c.oracle_dispatch()
+    assert np.array_equal(to_host(c.disp.slot_counts), d["slot_counts"])
+    assert np.array_equal(to_host(c.disp.pair_row), d["pair_row"])
+    loc, none = _local_rows(d, c.T_valid)
+    assert np.all(y[none] == 0)
+    r2 = np.random.default_rng(m_tile)
+    pick = np.union1d(tile_sample(d, m_tile, r2), r2.choice(loc, min(len(loc), 400), replace=False))
+    pick = pick[pick < c.T_valid]
+    sel = np.zeros(T, np.uint8)
+    sel[pick] = 1
+    got = bf16_to_f64(y)
+    ref = _oracle_y(c, d, "mirror", sel)
+    err_m = mirror_err_rows(got, ref, pick)
+    same = identical_share(got[pick], ref[pick])
+    ref = _oracle_y(c, d, "exact", sel)
+    err = rel_err_rows(got, ref, pick)
+    print(f"[stream-K {dtype} M={m_tile}] sampled {len(pick)} tokens exact err={err:.2e} mirror err={err_m:.2e} "
+          f"identical={same:.4f}")
+    _check_many_rows(dtype, err, err_m, same)
+
+
 @pytest.mark.parametrize("name,m_tile", [("tiny", 64), ("tiny", 256), ("tiny_fp8", 128), ("tiny_fp8mx", 256)])
 def test_stage_events_in_order(name, m_tile):
     """The eight stage events of the forward are recorded in stream order
