@@ -38,6 +38,7 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   gu.C = h;
   gu.Kd = s.H;
   gu.Nout = s.I;
+  gu.cmax = GATEUP_CHUNKS;
   auto mark = [&](int i) { return !ev || !ev[i] || hipEventRecord(ev[i], st) == hipSuccess; };
   if (!mark(0)) return hipErrorLaunchFailure;
   hipLaunchKernelGGL((k_gemm<false, BM, true>), dim3(grid), dim3(GEMM_THREADS), 0, st, gu);
@@ -56,9 +57,12 @@ hipError_t launch_bm(const tempo_moe_shape& s, const tempo_dispatch_out& d, cons
   dn.C = y_perm;
   dn.Kd = s.I;
   dn.Nout = s.H;
+  dn.cmax = DOWN_CHUNKS;
   hipLaunchKernelGGL((k_gemm<false, BM, false>), dim3(grid), dim3(GEMM_THREADS), 0, st, dn);
   if (!mark(3)) return hipErrorLaunchFailure;
-  hipLaunchKernelGGL((k_fixup<false, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
+  // (with one chunk per item no down item is split: nothing to complete)
+  if (dn.cmax > 1)
+    hipLaunchKernelGGL((k_fixup<false, BM, false>), dim3(grid * (BM / 8)), dim3(256), 0, st, dn, grid);
   return hipGetLastError();
 }
 

@@ -8,9 +8,10 @@
 //
 // Work decomposition (stream-K over fixed contraction chunks).  A work item
 // is one (M-tile, output block of 128 weight rows) pair; its contraction of
-// KT steps (128 bytes of every row per step) is cut into C <= 8 fixed chunks
-// of SPC steps, SPC a multiple of CQ = 8 for every tile size (the last chunk
-// is padded with empty steps to a multiple of the pipeline depth DR).  The chunks of all items,
+// KT steps (128 bytes of every row per step) is cut into C fixed chunks of
+// SPC steps (C at most GemmArgs::cmax: 2 for gate/up, 1 for down), SPC a
+// multiple of CQ = 8 for every tile size (the last chunk is padded with
+// empty steps to a multiple of the pipeline depth DR).  The chunks of all items,
 // item by item, form one sequence that is split into contiguous ranges, one
 // per workgroup (one workgroup per CU).  Range boundaries balance estimated
 // time rather than chunk counts: a chunk of an M-tile with m live row blocks
@@ -103,7 +104,17 @@ struct GemmArgs {
   uint64_t* t0;
   uint64_t* t1;
   int timing;
+  int cmax;                 // contraction chunks per work item, 1 .. CMAX (1: items are never split)
 };
+
+// Chunks per item of the two GEMMs (GemmArgs::cmax).  Fewer chunks mean
+// fewer items split over workgroups, so fewer partial tiles to write and add
+// up, against a coarser balance of the ranges.  Measured on the decode
+// shares (64- and 128-row tiles) and the fp8 prefill share: gate/up is
+// fastest with two chunks (its long contraction, H, leaves the ranges too
+// coarse at one), down with one (its output has many blocks, so whole items
+// balance well, and no fixup pass is needed).
+constexpr int GATEUP_CHUNKS = 2, DOWN_CHUNKS = 1;
 
 // Steps in flight per wavefront (DR): the weight slices of DR steps sit in
 // registers (four 16-byte loads per lane and step), the activation rows of
@@ -210,11 +221,12 @@ __device__ int range_lo(const Geo& g, int j, const int32_t* s_off, const int32_t
 
 template <int BM>
 __device__ __forceinline__ Geo make_geo(int KT, int NB, int NT, int b, int grid, const int32_t* s_off,
-                                        const int32_t* s_cnt, const int32_t* s_sw, int S) {
+                                        const int32_t* s_cnt, const int32_t* s_sw, int S, int cmax) {
   Geo g;
   constexpr int DR = gemm_dr(BM);
   g.KT = KT;
-  g.SPC = ((KT + CMAX - 1) / CMAX + CQ - 1) / CQ * CQ;
+  const int cm = min(max(cmax, 1), CMAX);
+  g.SPC = ((KT + cm - 1) / cm + CQ - 1) / CQ * CQ;
   g.C = (KT + g.SPC - 1) / g.SPC;
   g.SL = (KT - (g.C - 1) * g.SPC + DR - 1) / DR * DR;
   g.KTV = (g.C - 1) * g.SPC + g.SL;
@@ -295,7 +307,7 @@ __global__ __launch_bounds__(GEMM_THREADS, 1) void k_gemm(const GemmArgs p) {
   // M-tiles in use, from the stage-1 offsets themselves (every P_s is a
   // multiple of BM), bounded by what the row buffers hold
   const int NT = __builtin_amdgcn_readfirstlane(max(0, min(s_off[p.S] / BM, p.max_tiles)));
-  const Geo g = make_geo<BM>(p.Kd / BK, p.Nout / NCOLS, NT, blockIdx.x, gridDim.x, s_off, s_cnt, s_sw, p.S);
+  const Geo g = make_geo<BM>(p.Kd / BK, p.Nout / NCOLS, NT, blockIdx.x, gridDim.x, s_off, s_cnt, s_sw, p.S, p.cmax);
   if (g.q0 >= g.q1) {  // uniform: the whole workgroup leaves
     if (tid == 0) p.fix[(size_t)blockIdx.x * FIX_WORDS] = -1;
     return;
