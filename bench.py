@@ -22,7 +22,7 @@ UE8M0 fp8), the fitted max-affine profile (a, b, c, beta, n*) of each one's
 dtype and M-tile, per-stage times, and the CPU oracle timed on the host
 cores as a baseline.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload NAME] [--no-flat] [--no-bf16]
+    python bench.py [--gpus 1] [--steps 20] [--warmup 20] [--workload NAME] [--no-flat] [--no-bf16]
 """
 from __future__ import annotations
 
@@ -50,7 +50,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="qwen3_prefill_fp8mx")
     ap.add_argument("--bf16-workload", default="qwen3_prefill_bf16",
                     help="the same share in bf16, measured beside the headline for roofline_bf16")
@@ -247,8 +247,11 @@ def measure_workload(torch, name, m_tile, plan_name, steps, warmup, seed, copies
         with torch.cuda.graph(g):
             fwd[i]()
         graphs.append(g)
-    for i in range(copies):
-        graphs[i].replay()
+    # warm-up of the graph path itself: W replays, every weight copy at least
+    # once (the first replays after capture run a few per cent slower than
+    # the steady state that back-to-back blocks see)
+    for i in range(max(warmup, copies)):
+        graphs[i % copies].replay()
     torch.cuda.synchronize()
     ev_a, ev_b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
