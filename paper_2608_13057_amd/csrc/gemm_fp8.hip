@@ -20,7 +20,9 @@ using namespace gemm;
 // h (fp32, real rows) -> e4m3 with one fp32 scale per row and 128-column block:
 // scale = amax / 448 (1 if the block is all zero), q = e4m3(h / scale) with
 // round-to-nearest-even, magnitudes saturated at 448.  One wavefront per row,
-// two columns per lane per block.  Scales are stored block-major.
+// two columns per lane per block; the loads of up to 16 blocks are issued
+// together before their reductions, so a row waits for one memory latency
+// per 16 blocks rather than one per block.  Scales are stored block-major.
 // MX: the scale is rounded up to a power of two (UE8M0), the smallest one at
 // least amax / 448.
 template <bool MX>
@@ -37,20 +39,31 @@ __global__ __launch_bounds__(256) void k_quant_h(const float* __restrict__ h32, 
     if (row_token[row] < 0) continue;
     const float2* src = reinterpret_cast<const float2*>(h32 + (size_t)row * I);
     uint16_t* dst = reinterpret_cast<uint16_t*>(h8 + (size_t)row * I);
-    for (int b = 0; b < I / 128; b++) {
-      const float2 v = src[b * 64 + lane];
-      float m = fmaxf(fabsf(v.x), fabsf(v.y));
+    constexpr int NBL = 16;  // blocks loaded together
+    const int NB = I / 128;
+#pragma unroll 1
+    for (int b0 = 0; b0 < NB; b0 += NBL) {
+      float2 vb[NBL];
 #pragma unroll
-      for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d));
-      float sc = m > 0.f ? m / 448.0f : 1.0f;
-      if (MX && m > 0.f) {
-        uint32_t bits = __float_as_uint(sc);
-        if (bits & 0x7FFFFFu) bits = (bits & 0xFF800000u) + 0x800000u;  // next power of two up
-        sc = __uint_as_float(bits);
+      for (int k = 0; k < NBL; k++) vb[k] = b0 + k < NB ? src[(b0 + k) * 64 + lane] : make_float2(0.f, 0.f);
+#pragma unroll
+      for (int k = 0; k < NBL; k++) {
+        const int b = b0 + k;
+        if (b >= NB) break;
+        const float2 v = vb[k];
+        float m = fmaxf(fabsf(v.x), fabsf(v.y));
+#pragma unroll
+        for (int d = 32; d >= 1; d >>= 1) m = fmaxf(m, __shfl_xor(m, d));
+        float sc = m > 0.f ? m / 448.0f : 1.0f;
+        if (MX && m > 0.f) {
+          uint32_t bits = __float_as_uint(sc);
+          if (bits & 0x7FFFFFu) bits = (bits & 0xFF800000u) + 0x800000u;  // next power of two up
+          sc = __uint_as_float(bits);
+        }
+        const float q0 = fminf(fmaxf(v.x / sc, -448.f), 448.f), q1 = fminf(fmaxf(v.y / sc, -448.f), 448.f);
+        dst[b * 64 + lane] = (uint16_t)(__builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false) & 0xFFFF);
+        if (lane == 0) h_scale[(size_t)b * row_cap + row] = sc;
       }
-      const float q0 = fminf(fmaxf(v.x / sc, -448.f), 448.f), q1 = fminf(fmaxf(v.y / sc, -448.f), 448.f);
-      dst[b * 64 + lane] = (uint16_t)(__builtin_amdgcn_cvt_pk_fp8_f32(q0, q1, 0, false) & 0xFFFF);
-      if (lane == 0) h_scale[(size_t)b * row_cap + row] = sc;
     }
   }
 }
